@@ -1,0 +1,179 @@
+"""CPU oracle for the frequency-controller hot path (test infrastructure).
+
+Only the test-suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It wraps ``tl_oracle.c`` (plain,
+single-threaded C compiled with gcc) through ctypes and numpy; it shares no
+code with the HIP library and never imports it.
+
+Functions follow the paper: ``project`` (Sec. 4.2, Eq. 1-2, admission check 1
+of Sec. 4.3.2), ``rows`` and ``forest_predict`` (Sec. 4.3.1), ``select`` and
+``select_binary`` (Sec. 4.3.2 checks 2-3, Eq. 3-4, Sec. 4.5), ``latency_ns``
+(T' = 1/T in ns) and ``end_to_end`` (all three stages).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tl_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libtl_oracle.so")
+
+FLAG_BAD_REQUEST, FLAG_LOST, FLAG_OVERCOMMIT, FLAG_OVERFLOW, FLAG_UNSORTED = 1, 2, 4, 8, 16
+STATUS_OK, STATUS_INFEASIBLE, STATUS_LOST, STATUS_INVALID = 0, 1, 2, 3
+NO_DEADLINE = np.uint64(0xFFFFFFFFFFFFFFFF)
+LAT_SATURATED = 1 << 40
+
+
+def build():
+    """Compile the oracle with gcc: -O2, no fast-math, no FMA contraction."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
+           "-fno-fast-math", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    i64, i32, f32 = ctypes.c_int64, ctypes.c_int32, ctypes.c_float
+    lib.tlo_project.argtypes = [i64, i32, i32] + [P] * 15
+    lib.tlo_project.restype = ctypes.c_int
+    lib.tlo_rows.argtypes = [i64, i32, i32, i32, P, P, P, P, P]
+    lib.tlo_rows.restype = ctypes.c_int
+    lib.tlo_forest_predict.argtypes = [i32, i32, i32, f32, P, P, P, P, i64, P]
+    lib.tlo_forest_predict.restype = ctypes.c_int
+    lib.tlo_latency_ns.argtypes = [f32]
+    lib.tlo_latency_ns.restype = ctypes.c_uint64
+    for name in ("tlo_select", "tlo_select_binary"):
+        fn = getattr(lib, name)
+        fn.argtypes = [i64, i32, i32] + [P] * 7
+        fn.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+def project(inp, return_admit=False):
+    """Stage 1 on every scenario of ``inp`` (a dict from ``synth.make_inputs``)."""
+    lib = _load()
+    S, H, N = int(inp["n_scenarios"]), int(inp["horizon"]), int(inp["block_tokens"])
+    off = _c(inp["req_offset"], np.int64)
+    args = [_c(inp[k], t) for k, t in (("prompt", np.int32), ("generated", np.int32),
+                                        ("remaining", np.int32), ("arrival", np.int32))]
+    deadline = _c(inp.get("deadline_ns"), np.uint64)
+    lost = _c(inp.get("lost"), np.uint8)
+    cap = _c(inp["kv_capacity"], np.int32)
+    bcap = _c(inp.get("batch_cap"), np.int32)
+    batch = np.zeros((S, H), np.int32)
+    kv = np.zeros((S, H), np.int32)
+    dl = np.zeros((S, H), np.uint64)
+    n_iters = np.zeros(S, np.int32)
+    flags = np.zeros(S, np.uint32)
+    admit = np.zeros(int(off[-1]) if S else 0, np.int32) if return_admit else None
+    rc = lib.tlo_project(S, H, N, _ptr(off), *[_ptr(a) for a in args], _ptr(deadline), _ptr(lost),
+                         _ptr(cap), _ptr(bcap), _ptr(batch), _ptr(kv), _ptr(dl), _ptr(n_iters),
+                         _ptr(flags), _ptr(admit))
+    if rc:
+        raise ValueError("tlo_project rejected its arguments")
+    out = dict(batch=batch, kv=kv, deadline_at=dl, n_iters=n_iters, flags=flags)
+    if return_admit:
+        out["admit_iter"] = admit
+    return out
+
+
+def rows(freqs, batch, kv, engine=None, n_features=3):
+    """Feature rows [S][F][H][n_features] from projected curves."""
+    lib = _load()
+    batch = _c(batch, np.int32)
+    kv = _c(kv, np.int32)
+    S, H = batch.shape
+    freqs = _c(freqs, np.float32)
+    F = freqs.size
+    engine = _c(engine, np.float32)
+    out = np.zeros((S, F, H, n_features), np.float32)
+    rc = lib.tlo_rows(S, F, H, n_features, _ptr(freqs), _ptr(batch), _ptr(kv), _ptr(engine), _ptr(out))
+    if rc:
+        raise ValueError("tlo_rows rejected its arguments")
+    return out
+
+
+def forest_predict(forest, x):
+    """Ensemble output for every row of ``x`` ([..., n_features] fp32)."""
+    lib = _load()
+    nf = int(forest["n_features"])
+    x = _c(x, np.float32)
+    shape = x.shape[:-1]
+    assert x.shape[-1] == nf
+    n_rows = int(np.prod(shape)) if shape else 1
+    out = np.zeros(n_rows, np.float32)
+    feat = _c(forest["feature"], np.uint8)
+    thr = _c(forest["threshold"], np.float32)
+    leaf = _c(forest["leaf"], np.float32)
+    rc = lib.tlo_forest_predict(int(forest["n_trees"]), int(forest["depth"]), nf,
+                                float(forest["base_score"]), _ptr(feat), _ptr(thr), _ptr(leaf),
+                                _ptr(x), n_rows, _ptr(out))
+    if rc:
+        raise ValueError("tlo_forest_predict rejected its arguments")
+    return out.reshape(shape)
+
+
+def latency_ns(ips):
+    lib = _load()
+    return int(lib.tlo_latency_ns(float(np.float32(ips))))
+
+
+def _select(fn_name, ips, deadline_at, n_iters, tbt_slo_ns, proj_flags):
+    lib = _load()
+    ips = _c(ips, np.float32)
+    S, F, H = ips.shape
+    dl = _c(deadline_at, np.uint64)
+    n_iters = _c(n_iters, np.int32)
+    tbt = _c(tbt_slo_ns, np.uint64)
+    fl = _c(proj_flags, np.uint32)
+    idx = np.zeros(S, np.int32)
+    st = np.zeros(S, np.uint32)
+    rc = getattr(lib, fn_name)(S, F, H, _ptr(ips), _ptr(dl), _ptr(n_iters), _ptr(tbt), _ptr(fl),
+                               _ptr(idx), _ptr(st))
+    if rc:
+        raise ValueError(fn_name + " rejected its arguments")
+    return idx, st
+
+
+def select(ips, deadline_at, n_iters, tbt_slo_ns, proj_flags=None):
+    """Lowest SLO-feasible frequency index per scenario (exhaustive)."""
+    return _select("tlo_select", ips, deadline_at, n_iters, tbt_slo_ns, proj_flags)
+
+
+def select_binary(ips, deadline_at, n_iters, tbt_slo_ns, proj_flags=None):
+    """The paper's binary search over frequencies."""
+    return _select("tlo_select_binary", ips, deadline_at, n_iters, tbt_slo_ns, proj_flags)
+
+
+def end_to_end(inp):
+    """All three stages; returns the projection, the IPS tensor and the choice."""
+    proj = project(inp)
+    x = rows(inp["freqs_mhz"], proj["batch"], proj["kv"], inp.get("engine_size"),
+             int(inp["n_features"]))
+    ips = forest_predict(inp["forest"], x)
+    idx, st = select(ips, proj["deadline_at"], proj["n_iters"], inp["tbt_slo_ns"], proj["flags"])
+    return dict(proj, ips=ips, freq_idx=idx, status=st)
