@@ -1,0 +1,180 @@
+"""Throughput of the batched frequency-controller hot path on one MI355X.
+
+One step = projection (+ feature-row expansion), tree-ensemble prediction on
+every (scenario, frequency, iteration) row, and frequency selection, for one
+batch of synthetic scenarios already resident in HBM.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c3] [--no-cpu-baseline]
+
+Prints one JSON line.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+# 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz: one 32-bit VALU lane
+# operation per lane per clock (no packed math)
+VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+METRIC = "feature rows predicted/sec + scenarios/sec end-to-end; % of HBM peak"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(inp, F, rows):
+    S, H, nf = inp["n_scenarios"], inp["horizon"], inp["n_features"]
+    R = int(inp["req_offset"][-1])
+    f = inp["forest"]
+    n_int = (1 << f["depth"]) - 1
+    forest_bytes = f["n_trees"] * (n_int * 8 + (n_int + 1) * 8)
+    k1 = R * 25 + S * 16 + S * H * 16 + S * 8 + rows * nf * 4
+    k2 = rows * nf * 4 + rows * 4 + forest_bytes
+    k3 = rows * 4 + S * H * 8 + S * 28
+    return dict(project=k1, predict=k2, select=k3)
+
+
+def traffic_record(cfg_name):
+    """HBM bytes per forest launch from committed rocprofv3 counters, if they
+    were taken on the current forest kernel source."""
+    path = os.path.join(ROOT, "profiles", f"forest_{cfg_name.split('_')[0]}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = open(os.path.join(ROOT, "paper_2408_05235_amd", "csrc", "forest.hip"), "rb").read()
+    if rec.get("forest_hip_sha256") != hashlib.sha256(src).hexdigest():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(inp, budget_s=12.0, max_scen=64):
+    import oracle
+    from paper_2408_05235_amd import synth
+    S = inp["n_scenarios"]
+    order = [0, S - 1] + list(np.random.default_rng(0).permutation(S))
+    seen, done, rows, t_used = set(), [], 0, 0.0
+    F, H = inp["n_freqs"], inp["horizon"]
+    for s in order:
+        if s in seen:
+            continue
+        seen.add(s)
+        sub = synth.subset(inp, [s])
+        t0 = time.perf_counter()
+        oracle.end_to_end(sub)
+        t_used += time.perf_counter() - t0
+        done.append(int(s))
+        rows += F * H
+        if t_used >= budget_s or len(done) >= max_scen:
+            break
+    return dict(value=rows / t_used, unit="rows/s", cores=1, kind="oracle",
+                sample=f"{len(done)} of {S} scenarios (all stages, single thread), {t_used:.1f} s",
+                scenarios_per_s=len(done) / t_used)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="c3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(scenarios are independent: shard them across GPUs, one process each)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2408_05235_amd import api, configs, synth
+
+    cfg = configs.get_config(args.config)
+    t0 = time.perf_counter()
+    inp = synth.make_inputs(cfg)
+    log(f"inputs {cfg['name']}: {time.perf_counter() - t0:.1f}s, {int(inp['req_offset'][-1])} requests")
+    torch.cuda.set_device(0)
+    dev_in = api.upload(inp, "cuda:0")
+    forest = api.Forest.from_dict(inp["forest"])
+    ctl = api.Controller(dev_in, forest)
+    S, H, F = inp["n_scenarios"], inp["horizon"], inp["n_freqs"]
+    rows = S * F * H
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        ctl.step()
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        e = ev[k]
+        e[0].record()
+        ctl.project()
+        e[1].record()
+        ctl.predict()
+        e[2].record()
+        ctl.select()
+        e[3].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    log(f"timed {args.steps} steps in {wall:.2f}s")
+
+    st = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] for e in ev])  # ms
+    stage_ms = st.mean(axis=0)
+    step_ms = wall * 1e3 / args.steps
+    byt = algorithmic_bytes(inp, F, rows)
+    tot_bytes = sum(byt.values())
+
+    f = inp["forest"]
+    ops_per_row = f["n_trees"] * (f["depth"] + 1)
+    forest_s = stage_ms[1] / 1e3
+    achieved = ops_per_row * rows / forest_s / 1e12
+    traffic = traffic_record(cfg["name"])
+
+    out = {
+        "metric": METRIC,
+        "value": rows / (step_ms / 1e3),
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": cfg["name"], "scenarios": S, "horizon": H, "freqs": F,
+                   "rows_per_step": rows, "trees": f["n_trees"], "depth": f["depth"],
+                   "features": inp["n_features"], "requests": int(inp["req_offset"][-1])},
+        "scenarios_per_s": S / (step_ms / 1e3),
+        "hbm_frac_end_to_end": tot_bytes / (step_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+        "stages_ms": {"project": stage_ms[0], "predict": stage_ms[1], "select": stage_ms[2]},
+        "stage_hbm_gbs": {k: byt[k] / (v / 1e3) / 1e9 for k, v in
+                          zip(("project", "predict", "select"), stage_ms)},
+        "forest_rows_per_s": rows / forest_s,
+        "roofline": {"kernel": "forest_rows_kernel", "bound": "alu", "achieved": achieved,
+                     "peak": VALU_PEAK_TOPS, "unit": "Tops/s", "frac": achieved / VALU_PEAK_TOPS,
+                     "traffic": traffic,
+                     "ops_per_row": ops_per_row, "ops_note": "trees x (depth compares + 1 leaf add)"},
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(inp)
+    forest.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

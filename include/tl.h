@@ -1,0 +1,208 @@
+/*
+ * tl.h -- C ABI of the MI355X (gfx950) library for the batched hot path of
+ * throttLL'eM's per-iteration GPU-frequency controller (arXiv 2408.05235).
+ *
+ * For many independent what-if scenarios the library runs three stages, each
+ * a HIP kernel on one device:
+ *   tl_project        projected batch size and KV-cache blocks per future
+ *                     iteration (Sec. 4.2, Eq. 1-2), with FIFO admission of
+ *                     queued requests under the KV check of Sec. 4.3.2;
+ *                     optionally the feature rows of the performance model;
+ *   tl_forest_predict the performance model M, a gradient-boosted tree
+ *                     ensemble predicting iterations per second (Sec. 4.3.1);
+ *   tl_select_freq    the throttling controller (Sec. 4.5): per scenario the
+ *                     lowest frequency whose predicted per-iteration times
+ *                     pass the TBT check and the E2E deadlines (Sec. 4.3.2,
+ *                     checks 2 and 3, Eq. 3-4).
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are DEVICE pointers (memory of the device that is current on
+ *     the calling thread) owned by the caller, unless the comment says host.
+ *     The library never frees or retains caller memory.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Calls
+ *     only enqueue work; none synchronizes.  Outputs are valid once the
+ *     stream reaches that point.
+ *   - Argument errors (sizes, NULL pointers, unsupported shapes) are detected
+ *     on the host before anything is enqueued and return TL_EINVAL; nothing
+ *     is written.  A failed HIP call returns TL_EDEVICE.  tl_last_error()
+ *     then describes the failure (thread-local, valid until the next call).
+ *   - Data-dependent anomalies never fail a call: they are reported per
+ *     scenario through TL_FLAG_* bits and TL_STATUS_* values.
+ *   - Results are deterministic: bit-identical across runs and launches.
+ */
+#ifndef TL_H
+#define TL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TL_ABI_VERSION 1
+
+typedef enum tl_status {
+    TL_OK = 0,
+    TL_EINVAL = 1,          /* invalid argument; nothing was enqueued          */
+    TL_ENOMEM = 2,          /* device allocation failed                        */
+    TL_EDEVICE = 3,         /* a HIP runtime call or kernel launch failed      */
+    TL_EUNSUPPORTED = 4     /* valid but beyond this build's limits            */
+} tl_status;
+
+/* Limits of this build. */
+#define TL_MAX_HORIZON 8192         /* H: future iterations per scenario      */
+#define TL_MAX_BLOCK_TOKENS 65536   /* N: tokens per KV block                 */
+#define TL_MAX_FREQS 4096           /* F: candidate frequencies               */
+#define TL_MAX_FEATURES 4           /* model inputs (Sec. 4.3.1 lists four)   */
+#define TL_MAX_DEPTH 14             /* tree depth                             */
+
+/* Per-scenario flags written by tl_project (bitwise OR). */
+#define TL_FLAG_BAD_REQUEST 1u  /* some scoreboard entries were malformed and ignored:
+                                   prompt < 0, generated < 0, remaining < 1,
+                                   arrival < -1, or prompt + generated > 2^30 */
+#define TL_FLAG_LOST        2u  /* an in-flight request is marked lost (Sec. 4.3.2)   */
+#define TL_FLAG_OVERCOMMIT  4u  /* the in-flight batch alone exceeds the KV capacity
+                                   at some iteration, or exceeds the batch cap now    */
+#define TL_FLAG_OVERFLOW    8u  /* scenario not projected: its request range is
+                                   invalid, or sum over valid entries of
+                                   ceil((prompt+generated+H)/N) > 2^31-1, so curves
+                                   could overflow; outputs are zero / no deadline  */
+#define TL_FLAG_UNSORTED   16u  /* queued entries are not in non-decreasing arrival
+                                   order; the queue is still served in array order */
+
+/* Per-scenario status written by tl_select_freq. */
+#define TL_STATUS_OK         0u  /* freq_idx is the lowest feasible index           */
+#define TL_STATUS_INFEASIBLE 1u  /* no frequency passes; freq_idx = F-1            */
+#define TL_STATUS_LOST       2u  /* a lost request forces the maximum; freq_idx = F-1 */
+#define TL_STATUS_INVALID    3u  /* scenario flagged TL_FLAG_OVERFLOW; freq_idx = F-1 */
+
+/* Per-iteration time that stands for "no progress" (IPS <= 0, NaN, or
+ * 1e9/IPS >= 2^40 ns). */
+#define TL_LAT_SATURATED_NS (1ull << 40)
+#define TL_NO_DEADLINE UINT64_MAX
+
+int32_t tl_abi_version(void);        /* returns TL_ABI_VERSION */
+const char* tl_last_error(void);     /* message for the last non-OK status on this thread */
+
+/* ------------------------------------------------------------------------
+ * The performance model M (Sec. 4.3.1): a gradient-boosted decision-tree
+ * ensemble over the inputs the paper names (engine size, batch size, KV-cache
+ * usage, GPU frequency) that predicts iterations per second.
+ *
+ * Trees are complete, of depth `depth`, in heap order: internal node k
+ * (0 <= k < 2^depth - 1) compares x[feature[k]] < threshold[k] in fp32 and
+ * continues at 2k+1 when true, 2k+2 otherwise (a NaN input goes to 2k+2);
+ * after `depth` comparisons the node index minus (2^depth - 1) selects one of
+ * the 2^depth leaves.  A shallower tree is expressed by padding with
+ * threshold +inf (always 2k+1).  The prediction of a row is base_score plus
+ * the selected leaf of every tree, accumulated in fp64 in tree order and
+ * rounded once to fp32.
+ *
+ * feature   host, uint8 [n_trees][2^depth - 1], each < n_features
+ * threshold host, fp32  [n_trees][2^depth - 1]
+ * leaf      host, fp32  [n_trees][2^depth]
+ * The arrays are copied to the current device; the handle owns that copy and
+ * must be used with the same device.  n_trees >= 0 (0 gives base_score),
+ * 0 <= depth <= TL_MAX_DEPTH, 1 <= n_features <= TL_MAX_FEATURES.
+ * Errors: TL_EINVAL (bad sizes, NULL, feature index out of range),
+ * TL_ENOMEM, TL_EDEVICE.  On error *out is set to NULL.
+ * ---------------------------------------------------------------------- */
+typedef struct tl_forest tl_forest;
+
+tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, float base_score,
+                           const uint8_t* feature, const float* threshold, const float* leaf,
+                           tl_forest** out);
+void tl_forest_destroy(tl_forest* forest);   /* NULL is ignored; synchronizes the device */
+
+/* ------------------------------------------------------------------------
+ * Stage 1 -- KV usage and batch-size projection (Sec. 4.2, Eq. 1-2).
+ *
+ * Scenario s owns requests req_offset[s] .. req_offset[s+1]-1 (a scoreboard,
+ * Table 1).  Iterations are relative: j = 0 is the current iteration k.
+ * Request i has prompt length |q_i| = prompt_len[i], has generated
+ * generated[i] tokens and is projected to need remaining[i] more iterations.
+ *   arrival_iter[i] == -1 : in the batch now (scheduled g_i iterations ago);
+ *                           it occupies iterations [0, remaining[i]).
+ *   arrival_iter[i] >= 0  : queued; it becomes eligible at that iteration.
+ * Queued entries form one FIFO in array order.  At iteration j, after the
+ * requests ending at j leave, the head joins (s_a = j, its lifetime is
+ * [j, j + remaining)) iff it has arrived, the batch at j is below
+ * batch_cap[s], and appending it keeps every projected KV value from j to
+ * H-1 at or below kv_capacity[s] (Sec. 4.3.2 check 1); several may join at the
+ * same j; a head that cannot join blocks the queue.
+ *
+ * Outputs ([s][j] row-major, j < H):
+ *   batch[s][j]       number of requests in the batch at iteration j
+ *   kv[s][j]          KV blocks in use: sum of ceil((prompt + generated +
+ *                     (j - start)) / N) over those requests (Eq. 1-2)
+ *   deadline_at[s][j] minimum deadline_ns over non-lost requests whose last
+ *                     iteration in the batch is j (finishing inside the
+ *                     horizon), TL_NO_DEADLINE if none (Eq. 4 checkpoints)
+ *   n_iters[s]        number of projected iterations: min(H, last finish)
+ *   flags[s]          TL_FLAG_* bits
+ * Optional feature rows (rows != NULL), [s][f][j][n_features] fp32:
+ *   (freqs_mhz[f], kv[s][j], batch[s][j] [, engine_size[s]])
+ * the query vector of Sec. 4.3.2 check 2 for every candidate frequency.
+ * freqs_mhz must be ascending; index F-1 is the maximum frequency.
+ * ---------------------------------------------------------------------- */
+typedef struct tl_project_args {
+    uint32_t struct_size;          /* sizeof(tl_project_args) */
+    int32_t horizon;               /* H, 1 .. TL_MAX_HORIZON */
+    int64_t n_scenarios;           /* S >= 0 */
+    int64_t n_requests;            /* total entries; req_offset[S] must equal it */
+    int32_t block_tokens;          /* N, 1 .. TL_MAX_BLOCK_TOKENS */
+    int32_t n_freqs;               /* F (rows only), 1 .. TL_MAX_FREQS */
+    int32_t n_features;            /* 3 or 4 (rows only) */
+    int32_t reserved;
+    const int64_t* req_offset;     /* [S+1] */
+    const int32_t* prompt_len;     /* [n_requests] */
+    const int32_t* generated;      /* [n_requests] */
+    const int32_t* remaining;      /* [n_requests] */
+    const int32_t* arrival_iter;   /* [n_requests] */
+    const uint64_t* deadline_ns;   /* [n_requests], t_dead - t_cur in ns; NULL = none */
+    const uint8_t* lost;           /* [n_requests], nonzero = lost; NULL = none */
+    const int32_t* kv_capacity;    /* [S] blocks */
+    const int32_t* batch_cap;      /* [S]; NULL = unlimited */
+    int32_t* batch;                /* out [S][H] */
+    int32_t* kv;                   /* out [S][H] */
+    uint64_t* deadline_at;         /* out [S][H] */
+    int32_t* n_iters;              /* out [S] */
+    uint32_t* flags;               /* out [S] */
+    const float* freqs_mhz;        /* [F] (rows only) */
+    const float* engine_size;      /* [S] (rows with n_features == 4) */
+    float* rows;                   /* out [S][F][H][n_features]; NULL = no rows */
+} tl_project_args;
+
+tl_status tl_project(const tl_project_args* args, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Stage 2 -- the model M on arbitrary feature rows (Sec. 4.3.1).
+ * rows [n_rows][n_features of the forest] fp32 row-major; out [n_rows] fp32.
+ * ---------------------------------------------------------------------- */
+tl_status tl_forest_predict(const tl_forest* forest, const float* rows, int64_t n_rows,
+                            float* out, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Stage 3 -- frequency selection (Sec. 4.5 with Sec. 4.3.2 checks 2-3).
+ *
+ * ips [S][F][H] fp32: predicted iterations/s of scenario s at frequency f in
+ * iteration j.  With n = clamp(n_iters[s], 0, H) and per-iteration times
+ * lat = ceil(1e9 / ips) ns (one IEEE fp64 division; TL_LAT_SATURATED_NS for
+ * ips <= 0, NaN or 1e9/ips >= 2^40), and T_R[l] = lat[0] + ... + lat[l-1]
+ * (Eq. 3), frequency f is feasible iff n == 0, or
+ *   T_R[n] <= tbt_slo_ns[s] * n            (mean TBT, check 2), and
+ *   T_R[j+1] < deadline_at[s][j] for every j < n with a deadline (Eq. 4).
+ * freq_idx[s] = lowest feasible f (status OK), else F-1 (INFEASIBLE).  If
+ * proj_flags[s] has TL_FLAG_OVERFLOW: F-1, INVALID; else if it has
+ * TL_FLAG_LOST: F-1, LOST (the search is bypassed).  proj_flags may be NULL.
+ * ---------------------------------------------------------------------- */
+tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
+                         const uint64_t* deadline_at, const int32_t* n_iters,
+                         const uint64_t* tbt_slo_ns, const uint32_t* proj_flags,
+                         int32_t* freq_idx, uint32_t* status, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TL_H */

@@ -1,0 +1,255 @@
+"""Python entry points with the names of the C ABI; argument marshalling only.
+
+Every computation runs in the HIP kernels of libtl.so.  Tensors must live on
+the current CUDA(HIP) device; work is enqueued on torch's current stream.
+Unsigned 64-bit quantities (deadlines, SLOs) travel as ``torch.int64``
+tensors holding the same bits; 32-bit flag words as ``torch.int32``.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import check, lib
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _need(t, dtype, name, shape=None):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t
+
+
+def _opt(t, dtype, name, shape=None):
+    return None if t is None else _need(t, dtype, name, shape)
+
+
+def tl_project(req_offset, prompt_len, generated, remaining, arrival_iter, kv_capacity,
+               horizon, block_tokens, deadline_ns=None, lost=None, batch_cap=None,
+               freqs_mhz=None, engine_size=None, n_features=3, want_rows=True, out=None):
+    """Stage 1 (tl_project).  Returns a dict of device tensors:
+    batch, kv [S,H] int32; deadline_at [S,H] int64 (uint64 bits); n_iters [S]
+    int32; flags [S] int32 (uint32 bits); rows [S,F,H,n_features] fp32 when
+    ``want_rows`` and ``freqs_mhz`` is given."""
+    _need(req_offset, torch.int64, "req_offset")
+    S = req_offset.numel() - 1
+    R = prompt_len.numel()
+    for name, t in (("prompt_len", prompt_len), ("generated", generated),
+                    ("remaining", remaining), ("arrival_iter", arrival_iter)):
+        _need(t, torch.int32, name, (R,))
+    _need(kv_capacity, torch.int32, "kv_capacity", (S,))
+    _opt(deadline_ns, torch.int64, "deadline_ns", (R,))
+    _opt(lost, torch.uint8, "lost", (R,))
+    _opt(batch_cap, torch.int32, "batch_cap", (S,))
+    H = int(horizon)
+    dev = req_offset.device
+    rows_on = bool(want_rows and freqs_mhz is not None)
+    F = int(freqs_mhz.numel()) if rows_on else 0
+    if rows_on:
+        _need(freqs_mhz, torch.float32, "freqs_mhz", (F,))
+        if n_features == 4:
+            _need(engine_size, torch.float32, "engine_size", (S,))
+    o = out or {}
+    batch = o.get("batch") if o.get("batch") is not None else torch.empty((S, H), dtype=torch.int32, device=dev)
+    kv = o.get("kv") if o.get("kv") is not None else torch.empty((S, H), dtype=torch.int32, device=dev)
+    dl = o.get("deadline_at") if o.get("deadline_at") is not None else torch.empty((S, H), dtype=torch.int64, device=dev)
+    n_iters = o.get("n_iters") if o.get("n_iters") is not None else torch.empty(S, dtype=torch.int32, device=dev)
+    flags = o.get("flags") if o.get("flags") is not None else torch.empty(S, dtype=torch.int32, device=dev)
+    rows = None
+    if rows_on:
+        rows = o.get("rows") if o.get("rows") is not None else torch.empty((S, F, H, n_features), dtype=torch.float32, device=dev)
+        _need(rows, torch.float32, "rows", (S, F, H, n_features))
+    _need(batch, torch.int32, "batch", (S, H))
+    _need(kv, torch.int32, "kv", (S, H))
+    _need(dl, torch.int64, "deadline_at", (S, H))
+    _need(n_iters, torch.int32, "n_iters", (S,))
+    _need(flags, torch.int32, "flags", (S,))
+    a = _lib.ProjectArgs()
+    a.struct_size = ctypes.sizeof(_lib.ProjectArgs)
+    a.horizon = H
+    a.n_scenarios = S
+    a.n_requests = R
+    a.block_tokens = int(block_tokens)
+    a.n_freqs = F
+    a.n_features = int(n_features) if rows_on else 0
+    a.req_offset = _p(req_offset)
+    a.prompt_len = _p(prompt_len)
+    a.generated = _p(generated)
+    a.remaining = _p(remaining)
+    a.arrival_iter = _p(arrival_iter)
+    a.deadline_ns = _p(deadline_ns)
+    a.lost = _p(lost)
+    a.kv_capacity = _p(kv_capacity)
+    a.batch_cap = _p(batch_cap)
+    a.batch, a.kv, a.deadline_at, a.n_iters, a.flags = _p(batch), _p(kv), _p(dl), _p(n_iters), _p(flags)
+    a.freqs_mhz = _p(freqs_mhz) if rows_on else None
+    a.engine_size = _p(engine_size) if rows_on else None
+    a.rows = _p(rows)
+    check(lib().tl_project(ctypes.byref(a), _stream()))
+    res = dict(batch=batch, kv=kv, deadline_at=dl, n_iters=n_iters, flags=flags)
+    if rows_on:
+        res["rows"] = rows
+    return res
+
+
+class Forest:
+    """Device copy of a tree ensemble (tl_forest_create / tl_forest_destroy)."""
+
+    def __init__(self, n_trees, depth, n_features, base_score, feature, threshold, leaf):
+        feature = np.ascontiguousarray(feature, dtype=np.uint8)
+        threshold = np.ascontiguousarray(threshold, dtype=np.float32)
+        leaf = np.ascontiguousarray(leaf, dtype=np.float32)
+        n_int = (1 << int(depth)) - 1
+        if feature.size != n_trees * n_int or threshold.size != n_trees * n_int or leaf.size != n_trees * (n_int + 1):
+            raise ValueError("tree array sizes do not match n_trees and depth")
+        self.n_trees, self.depth, self.n_features = int(n_trees), int(depth), int(n_features)
+        self.base_score = float(np.float32(base_score))
+        h = ctypes.c_void_p()
+        check(lib().tl_forest_create(self.n_trees, self.depth, self.n_features, self.base_score,
+                                     feature.ctypes.data_as(ctypes.c_void_p),
+                                     threshold.ctypes.data_as(ctypes.c_void_p),
+                                     leaf.ctypes.data_as(ctypes.c_void_p), ctypes.byref(h)))
+        self._h = h
+
+    @classmethod
+    def from_dict(cls, d):
+        return cls(d["n_trees"], d["depth"], d["n_features"], d["base_score"],
+                   d["feature"], d["threshold"], d["leaf"])
+
+    def tl_forest_predict(self, rows, out=None):
+        """IPS for every row of ``rows`` ([..., n_features] fp32 device tensor)."""
+        _need(rows, torch.float32, "rows")
+        if rows.shape[-1] != self.n_features:
+            raise ValueError(f"rows have {rows.shape[-1]} features, forest has {self.n_features}")
+        n = rows.numel() // self.n_features
+        if out is None:
+            out = torch.empty(rows.shape[:-1], dtype=torch.float32, device=rows.device)
+        _need(out, torch.float32, "out")
+        if out.numel() != n:
+            raise ValueError("out has the wrong number of elements")
+        check(lib().tl_forest_predict(self._h, _p(rows), n, _p(out), _stream()))
+        return out
+
+    predict = tl_forest_predict
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().tl_forest_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def tl_select_freq(ips, deadline_at, n_iters, tbt_slo_ns, proj_flags=None, out=None):
+    """Stage 3 (tl_select_freq).  ips [S,F,H] fp32.  Returns (freq_idx int32
+    [S], status int32 [S])."""
+    _need(ips, torch.float32, "ips")
+    if ips.dim() != 3:
+        raise ValueError("ips must be [S, F, H]")
+    S, F, H = ips.shape
+    _need(deadline_at, torch.int64, "deadline_at", (S, H))
+    _need(n_iters, torch.int32, "n_iters", (S,))
+    _need(tbt_slo_ns, torch.int64, "tbt_slo_ns", (S,))
+    _opt(proj_flags, torch.int32, "proj_flags", (S,))
+    o = out or {}
+    idx = o.get("freq_idx") if o.get("freq_idx") is not None else torch.empty(S, dtype=torch.int32, device=ips.device)
+    st = o.get("status") if o.get("status") is not None else torch.empty(S, dtype=torch.int32, device=ips.device)
+    _need(idx, torch.int32, "freq_idx", (S,))
+    _need(st, torch.int32, "status", (S,))
+    check(lib().tl_select_freq(_p(ips), S, F, H, _p(deadline_at), _p(n_iters), _p(tbt_slo_ns),
+                               _p(proj_flags), _p(idx), _p(st), _stream()))
+    return idx, st
+
+
+# short names
+project = tl_project
+select_freq = tl_select_freq
+
+
+def upload(inp, device="cuda"):
+    """Copy a numpy input dict (``synth.make_inputs``) to device tensors."""
+    def t(a, dtype=None):
+        if a is None:
+            return None
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint64:
+            a = a.view(np.int64)
+        if a.dtype == np.uint32:
+            a = a.view(np.int32)
+        return torch.from_numpy(a).to(device)
+
+    return dict(
+        n_scenarios=int(inp["n_scenarios"]), horizon=int(inp["horizon"]),
+        block_tokens=int(inp["block_tokens"]), n_features=int(inp["n_features"]),
+        req_offset=t(inp["req_offset"]), prompt=t(inp["prompt"]), generated=t(inp["generated"]),
+        remaining=t(inp["remaining"]), arrival=t(inp["arrival"]), deadline_ns=t(inp.get("deadline_ns")),
+        lost=t(inp.get("lost")), kv_capacity=t(inp["kv_capacity"]), batch_cap=t(inp.get("batch_cap")),
+        tbt_slo_ns=t(inp["tbt_slo_ns"]), freqs_mhz=t(inp["freqs_mhz"]),
+        engine_size=t(inp.get("engine_size")),
+    )
+
+
+class Controller:
+    """The whole hot path for one batch of scenarios: project -> predict ->
+    select, enqueued back to back on the current stream with preallocated
+    buffers (no host round trip between stages)."""
+
+    def __init__(self, dev_inputs, forest):
+        self.d = dev_inputs
+        self.forest = forest
+        d = dev_inputs
+        S, H = d["n_scenarios"], d["horizon"]
+        F, nf = d["freqs_mhz"].numel(), d["n_features"]
+        dev = d["req_offset"].device
+        self.buf = dict(
+            batch=torch.empty((S, H), dtype=torch.int32, device=dev),
+            kv=torch.empty((S, H), dtype=torch.int32, device=dev),
+            deadline_at=torch.empty((S, H), dtype=torch.int64, device=dev),
+            n_iters=torch.empty(S, dtype=torch.int32, device=dev),
+            flags=torch.empty(S, dtype=torch.int32, device=dev),
+            rows=torch.empty((S, F, H, nf), dtype=torch.float32, device=dev),
+        )
+        self.ips = torch.empty((S, F, H), dtype=torch.float32, device=dev)
+        self.sel = dict(freq_idx=torch.empty(S, dtype=torch.int32, device=dev),
+                        status=torch.empty(S, dtype=torch.int32, device=dev))
+
+    def project(self):
+        d = self.d
+        return tl_project(d["req_offset"], d["prompt"], d["generated"], d["remaining"], d["arrival"],
+                          d["kv_capacity"], d["horizon"], d["block_tokens"], d["deadline_ns"],
+                          d["lost"], d["batch_cap"], d["freqs_mhz"], d["engine_size"],
+                          d["n_features"], True, self.buf)
+
+    def predict(self):
+        return self.forest.tl_forest_predict(self.buf["rows"], self.ips)
+
+    def select(self):
+        return tl_select_freq(self.ips, self.buf["deadline_at"], self.buf["n_iters"],
+                              self.d["tbt_slo_ns"], self.buf["flags"], self.sel)
+
+    def step(self):
+        self.project()
+        self.predict()
+        return self.select()

@@ -1,0 +1,207 @@
+// Host side of the C ABI: argument validation (before anything is enqueued),
+// forest upload, kernel dispatch and error reporting.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "device_util.h"
+#include "tl.h"
+#include "tl_internal.h"
+
+struct tl_forest {
+    int device;
+    tl::ForestDev dev;
+    void* nodes_mem;
+    void* leaves_mem;
+};
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+tl_status fail(tl_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+tl_status ok() {
+    g_err[0] = '\0';
+    return TL_OK;
+}
+
+tl_status from_hip(hipError_t e, const char* what) {
+    if (e == hipSuccess) return ok();
+    return fail(e == hipErrorOutOfMemory ? TL_ENOMEM : TL_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t tl_abi_version(void) { return TL_ABI_VERSION; }
+
+const char* tl_last_error(void) { return g_err; }
+
+tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, float base_score,
+                           const uint8_t* feature, const float* threshold, const float* leaf,
+                           tl_forest** out) {
+    if (!out) return fail(TL_EINVAL, "tl_forest_create: out is NULL");
+    *out = nullptr;
+    if (n_trees < 0) return fail(TL_EINVAL, "tl_forest_create: n_trees %d < 0", n_trees);
+    if (depth < 0 || depth > TL_MAX_DEPTH)
+        return fail(TL_EINVAL, "tl_forest_create: depth %d outside [0, %d]", depth, TL_MAX_DEPTH);
+    if (n_features < 1 || n_features > TL_MAX_FEATURES)
+        return fail(TL_EINVAL, "tl_forest_create: n_features %d outside [1, %d]", n_features, TL_MAX_FEATURES);
+    const int64_t n_int = (1ll << depth) - 1;
+    const int64_t n_leaf = 1ll << depth;
+    if (n_trees > 0 && (!leaf || (n_int > 0 && (!feature || !threshold))))
+        return fail(TL_EINVAL, "tl_forest_create: NULL tree array");
+    std::vector<uint2> nodes((size_t)(n_trees * n_int > 0 ? n_trees * n_int : 1));
+    std::vector<double> leaves((size_t)(n_trees * n_leaf > 0 ? n_trees * n_leaf : 1));
+    for (int64_t i = 0; i < (int64_t)n_trees * n_int; ++i) {
+        if (feature[i] >= n_features)
+            return fail(TL_EINVAL, "tl_forest_create: node %lld uses feature %d >= n_features %d",
+                        (long long)i, (int)feature[i], n_features);
+        uint32_t bits;
+        std::memcpy(&bits, &threshold[i], 4);
+        nodes[(size_t)i] = make_uint2(bits, feature[i]);
+    }
+    for (int64_t i = 0; i < (int64_t)n_trees * n_leaf; ++i) leaves[(size_t)i] = (double)leaf[i];
+
+    tl_forest* f = new (std::nothrow) tl_forest();
+    if (!f) return fail(TL_ENOMEM, "tl_forest_create: host allocation failed");
+    hipError_t e = hipGetDevice(&f->device);
+    if (e != hipSuccess) { delete f; return from_hip(e, "tl_forest_create: hipGetDevice"); }
+    e = hipMalloc(&f->nodes_mem, nodes.size() * sizeof(uint2));
+    if (e != hipSuccess) { delete f; return from_hip(e, "tl_forest_create: hipMalloc(nodes)"); }
+    e = hipMalloc(&f->leaves_mem, leaves.size() * sizeof(double));
+    if (e != hipSuccess) { (void)hipFree(f->nodes_mem); delete f; return from_hip(e, "tl_forest_create: hipMalloc(leaves)"); }
+    e = hipMemcpy(f->nodes_mem, nodes.data(), nodes.size() * sizeof(uint2), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(f->leaves_mem, leaves.data(), leaves.size() * sizeof(double), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(f->nodes_mem);
+        (void)hipFree(f->leaves_mem);
+        delete f;
+        return from_hip(e, "tl_forest_create: hipMemcpy");
+    }
+    f->dev.n_trees = n_trees;
+    f->dev.depth = depth;
+    f->dev.n_features = n_features;
+    f->dev.base_score = base_score;
+    f->dev.nodes = (const uint2*)f->nodes_mem;
+    f->dev.leaves = (const double*)f->leaves_mem;
+    *out = f;
+    return ok();
+}
+
+void tl_forest_destroy(tl_forest* f) {
+    if (!f) return;
+    (void)hipDeviceSynchronize();
+    (void)hipFree(f->nodes_mem);
+    (void)hipFree(f->leaves_mem);
+    delete f;
+}
+
+tl_status tl_project(const tl_project_args* a, void* stream) {
+    if (!a) return fail(TL_EINVAL, "tl_project: args is NULL");
+    if (a->struct_size < sizeof(tl_project_args))
+        return fail(TL_EINVAL, "tl_project: struct_size %u < %zu", a->struct_size, sizeof(tl_project_args));
+    if (a->n_scenarios < 0 || a->n_scenarios > 0x7fffffffll)
+        return fail(TL_EINVAL, "tl_project: n_scenarios %lld outside [0, 2^31-1]", (long long)a->n_scenarios);
+    if (a->horizon < 1 || a->horizon > TL_MAX_HORIZON)
+        return fail(TL_EINVAL, "tl_project: horizon %d outside [1, %d]", a->horizon, TL_MAX_HORIZON);
+    if (a->block_tokens < 1 || a->block_tokens > TL_MAX_BLOCK_TOKENS)
+        return fail(TL_EINVAL, "tl_project: block_tokens %d outside [1, %d]", a->block_tokens, TL_MAX_BLOCK_TOKENS);
+    if (a->n_requests < 0) return fail(TL_EINVAL, "tl_project: n_requests < 0");
+    if (!a->req_offset || !a->kv_capacity || !a->batch || !a->kv || !a->deadline_at || !a->n_iters || !a->flags)
+        return fail(TL_EINVAL, "tl_project: NULL required pointer");
+    if (a->n_requests > 0 && (!a->prompt_len || !a->generated || !a->remaining || !a->arrival_iter))
+        return fail(TL_EINVAL, "tl_project: NULL request array");
+    if (a->rows) {
+        if (a->n_freqs < 1 || a->n_freqs > TL_MAX_FREQS)
+            return fail(TL_EINVAL, "tl_project: n_freqs %d outside [1, %d]", a->n_freqs, TL_MAX_FREQS);
+        if (a->n_features != 3 && a->n_features != 4)
+            return fail(TL_EINVAL, "tl_project: n_features %d is not 3 or 4", a->n_features);
+        if (!a->freqs_mhz) return fail(TL_EINVAL, "tl_project: rows requested without freqs_mhz");
+        if (a->n_features == 4 && !a->engine_size)
+            return fail(TL_EINVAL, "tl_project: 4 features need engine_size");
+        if (a->n_features == 4 && ((uintptr_t)a->rows & 15u))
+            return fail(TL_EINVAL, "tl_project: rows must be 16-byte aligned for 4 features");
+    }
+    if (a->n_scenarios == 0) return ok();
+    tl::ProjectParams p{};
+    p.n_scenarios = a->n_scenarios;
+    p.n_requests = a->n_requests;
+    p.H = a->horizon;
+    p.N = a->block_tokens;
+    const tl::DivU32 dv = tl::make_divu32((uint32_t)a->block_tokens);
+    p.div_m = dv.m;
+    p.div_l = dv.l;
+    p.off = a->req_offset;
+    p.prompt = a->prompt_len;
+    p.gen = a->generated;
+    p.rem = a->remaining;
+    p.arr = a->arrival_iter;
+    p.deadline = a->deadline_ns;
+    p.lost = a->lost;
+    p.kv_cap = a->kv_capacity;
+    p.batch_cap = a->batch_cap;
+    p.batch = a->batch;
+    p.kv = a->kv;
+    p.deadline_at = a->deadline_at;
+    p.n_iters = a->n_iters;
+    p.flags = a->flags;
+    p.rows = a->rows;
+    p.F = a->rows ? a->n_freqs : 0;
+    p.nf = a->rows ? a->n_features : 0;
+    p.freqs = a->freqs_mhz;
+    p.engine = a->engine_size;
+    return from_hip(tl::launch_project(p, (hipStream_t)stream), "tl_project: launch");
+}
+
+tl_status tl_forest_predict(const tl_forest* f, const float* rows, int64_t n_rows, float* out, void* stream) {
+    if (!f) return fail(TL_EINVAL, "tl_forest_predict: forest is NULL");
+    if (n_rows < 0) return fail(TL_EINVAL, "tl_forest_predict: n_rows < 0");
+    if (n_rows > 0 && (!rows || !out)) return fail(TL_EINVAL, "tl_forest_predict: NULL rows or out");
+    if (n_rows > (int64_t)0x7fffffff * 256 * 4)
+        return fail(TL_EUNSUPPORTED, "tl_forest_predict: n_rows %lld too large", (long long)n_rows);
+    if (n_rows == 0) return ok();
+    return from_hip(tl::launch_forest_rows(f->dev, rows, n_rows, out, (hipStream_t)stream),
+                    "tl_forest_predict: launch");
+}
+
+tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
+                         const uint64_t* deadline_at, const int32_t* n_iters, const uint64_t* tbt_slo_ns,
+                         const uint32_t* proj_flags, int32_t* freq_idx, uint32_t* status, void* stream) {
+    if (n_scenarios < 0 || n_scenarios > 0x7fffffffll)
+        return fail(TL_EINVAL, "tl_select_freq: n_scenarios %lld outside [0, 2^31-1]", (long long)n_scenarios);
+    if (n_freqs < 1 || n_freqs > TL_MAX_FREQS)
+        return fail(TL_EINVAL, "tl_select_freq: n_freqs %d outside [1, %d]", n_freqs, TL_MAX_FREQS);
+    if (horizon < 1) return fail(TL_EINVAL, "tl_select_freq: horizon %d < 1", horizon);
+    if (n_scenarios > 0 && (!ips || !deadline_at || !n_iters || !tbt_slo_ns || !freq_idx || !status))
+        return fail(TL_EINVAL, "tl_select_freq: NULL required pointer");
+    if (n_scenarios == 0) return ok();
+    tl::SelectParams p{};
+    p.ips = ips;
+    p.S = n_scenarios;
+    p.F = n_freqs;
+    p.H = horizon;
+    p.deadline_at = deadline_at;
+    p.n_iters = n_iters;
+    p.tbt_slo_ns = tbt_slo_ns;
+    p.proj_flags = proj_flags;
+    p.freq_idx = freq_idx;
+    p.status = status;
+    return from_hip(tl::launch_select(p, (hipStream_t)stream), "tl_select_freq: launch");
+}
+
+}  // extern "C"

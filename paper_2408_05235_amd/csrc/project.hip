@@ -1,0 +1,336 @@
+// Stage 1: KV usage and batch-size projection (Sec. 4.2, Eq. 1-2) with FIFO
+// admission of queued requests under the KV check of Sec. 4.3.2.
+//
+// One 64-lane wavefront per scenario; the per-iteration curves live in LDS.
+//
+// In-flight requests are turned into O(1) events each instead of O(r) curve
+// updates.  For a request with c cached tokens active on [0, e):
+//   KV_i[j] = ceil((c + j) / N)   (Eq. 1 with j - s_i = g_i + j)
+// starts at ceil(c / N), grows by one block at every j >= 1 with
+// c + j == 1 (mod N) -- a comb of period N beginning at j0 -- and drops to 0
+// at e.  So KV = prefix-sum over j of
+//   (jumps at 0 and e)  +  C[j],  C[j] = C[j - N] + comb_diff[j],
+// where comb_diff gets +1 at j0 and -1 at the first comb point >= e.  The
+// batch curve is the prefix sum of +1 at 0 / -1 at e.
+//
+// Queued requests are admitted iteration by iteration in FIFO order by the
+// same wave: the head's KV contribution over its in-horizon lifetime is
+// checked against the capacity with all 64 lanes, then added into the LDS
+// KV curve.  Admissions only happen after the last iteration at which the
+// in-flight batch alone exceeds the capacity, which makes the lifetime check
+// equal to checking the whole projected vector from the current iteration on.
+#include "device_util.h"
+#include "tl_internal.h"
+
+namespace tl {
+namespace {
+
+constexpr uint64_t kNoDeadline = ~0ull;
+
+__device__ __forceinline__ bool entry_ok(int32_t p, int32_t g, int32_t r, int32_t a) {
+    return p >= 0 && g >= 0 && r >= 1 && a >= -1 && (int64_t)p + (int64_t)g <= (1ll << 30);
+}
+
+// sum of DA[t] for t in (j, j2], j2 < H; every lane returns the same value
+__device__ __forceinline__ int32_t sum_range(const int32_t* DA, int32_t j, int32_t j2) {
+    if (j2 == j + 1) return DA[j2];
+    int32_t acc = 0;
+    for (int32_t t0 = j + 1; t0 <= j2; t0 += kWave) {
+        int32_t t = t0 + lane_id();
+        acc += (t <= j2) ? DA[t] : 0;
+    }
+    return wave_sum(acc);
+}
+
+__global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
+    extern __shared__ int32_t lds[];
+    const int32_t H = P.H;
+    const int32_t N = P.N;
+    const DivU32 divN{(uint32_t)N, P.div_m, P.div_l};
+    int32_t* KV = lds;            // KV curve (diff, then values)
+    int32_t* BI = lds + H;        // in-flight batch curve (diff, then values)
+    int32_t* CD = lds + 2 * H;    // comb diff / prefix; later the admitted-batch diff
+    const int lane = lane_id();
+    const int64_t s = blockIdx.x;
+    int32_t* outB = P.batch + s * H;
+    int32_t* outKV = P.kv + s * H;
+    uint64_t* outDL = P.deadline_at + s * H;
+
+    for (int32_t t = lane; t < H; t += kWave) {
+        KV[t] = 0;
+        BI[t] = 0;
+        CD[t] = 0;
+        outDL[t] = kNoDeadline;
+    }
+    __threadfence();
+    __syncthreads();
+
+    const int64_t lo = P.off[s];
+    const int64_t hi = P.off[s + 1];
+    const bool bad_range = lo < 0 || hi < lo || hi > P.n_requests || hi - lo > 0x7fffffffll;
+
+    // pass A: validity, size guard, lost / queue information
+    uint64_t bound = 0;
+    uint32_t fl = 0;
+    int32_t has_queue = 0;
+    if (!bad_range) {
+        int32_t arr_carry = -1;
+        for (int64_t base = lo; base < hi; base += kWave) {
+            const int64_t i = base + lane;
+            const bool in = i < hi;
+            int32_t p = 0, g = 0, r = 0, a = -1;
+            if (in) { p = P.prompt[i]; g = P.gen[i]; r = P.rem[i]; a = P.arr[i]; }
+            const bool ok = in && entry_ok(p, g, r, a);
+            if (in && !ok) fl |= TL_FLAG_BAD_REQUEST;
+            if (ok) bound += ceil_div_u32((uint32_t)(p + g + H), divN);
+            if (ok && a == -1 && P.lost && P.lost[i]) fl |= TL_FLAG_LOST;
+            const bool queued = ok && a >= 0;
+            if (queued && a < H) has_queue = 1;
+            // queue order: each queued arrival must be >= every earlier one
+            const int32_t v = queued ? a : -1;
+            const int32_t incl = wave_incl_max(v);
+            int32_t excl = __shfl_up(incl, 1);
+            if (lane == 0) excl = -1;
+            excl = max(excl, arr_carry);
+            if (queued && a < excl) fl |= TL_FLAG_UNSORTED;
+            arr_carry = max(arr_carry, __shfl(incl, kWave - 1));
+        }
+    }
+    bound = wave_sum_u64(bound);
+    fl = wave_or(fl);
+    has_queue = wave_max(has_queue);
+
+    if (bad_range || bound > 0x7fffffffull) {
+        for (int32_t t = lane; t < H; t += kWave) { outB[t] = 0; outKV[t] = 0; }
+        if (P.rows) {
+            for (int32_t f = 0; f < P.F; ++f)
+                for (int32_t t = lane; t < H; t += kWave) {
+                    float* row = P.rows + (((int64_t)s * P.F + f) * H + t) * P.nf;
+                    row[0] = P.freqs[f];
+                    row[1] = 0.0f;
+                    row[2] = 0.0f;
+                    if (P.nf == 4) row[3] = P.engine[s];
+                }
+        }
+        if (lane == 0) {
+            P.n_iters[s] = 0;
+            P.flags[s] = bad_range ? TL_FLAG_OVERFLOW : ((fl & TL_FLAG_BAD_REQUEST) | TL_FLAG_OVERFLOW);
+        }
+        return;
+    }
+
+    // pass B: in-flight requests -> events
+    int32_t n_end = 0, n_in = 0, kv0 = 0;
+    for (int64_t base = lo; base < hi; base += kWave) {
+        const int64_t i = base + lane;
+        if (i >= hi) continue;
+        const int32_t p = P.prompt[i], g = P.gen[i], r = P.rem[i], a = P.arr[i];
+        if (!entry_ok(p, g, r, a) || a != -1) continue;
+        const int32_t c = p + g;
+        const int32_t e = r;
+        ++n_in;
+        kv0 += (int32_t)ceil_div_u32((uint32_t)c, divN);
+        const int32_t lim = min(e, H);
+        n_end = max(n_end, lim);
+        if (e < H) {
+            atomicAdd(&BI[e], -1);
+            atomicAdd(&KV[e], -(int32_t)ceil_div_u32((uint32_t)(c + e - 1), divN));
+        }
+        const int32_t rc = (int32_t)((uint32_t)c - div_u32((uint32_t)c, divN) * (uint32_t)N);
+        const int32_t j0 = (rc == 0) ? 1 : (N + 1 - rc);
+        if (j0 < lim) {
+            atomicAdd(&CD[j0], 1);
+            if (e < H) {
+                const int32_t jend = j0 + N * (int32_t)ceil_div_u32((uint32_t)(e - j0), divN);
+                if (jend < H) atomicAdd(&CD[jend], -1);
+            }
+        }
+        const bool is_lost = P.lost && P.lost[i];
+        const uint64_t d = P.deadline ? P.deadline[i] : kNoDeadline;
+        if (e <= H && !is_lost && d != kNoDeadline) atomicMin((unsigned long long*)&outDL[e - 1], (unsigned long long)d);
+    }
+    n_in = wave_sum(n_in);
+    kv0 = wave_sum(kv0);
+    n_end = wave_max(n_end);
+    if (lane == 0) {
+        BI[0] += n_in;
+        KV[0] += kv0;
+    }
+    __syncthreads();
+
+    // scans: comb (stride N) then KV and batch prefix sums; last over-capacity iteration
+    const int32_t cap = P.kv_cap[s];
+    int32_t last_over = -1;
+    {
+        const int32_t lane_mod = lane % N;
+        int32_t carry_kv = 0, carry_b = 0;
+        for (int32_t t0 = 0; t0 < H; t0 += kWave) {
+            const int32_t t = t0 + lane;
+            const bool in = t < H;
+            int32_t c = in ? CD[t] : 0;
+            for (int32_t d = N; d < kWave; d <<= 1) {
+                const int32_t u = __shfl_up(c, d);
+                if (lane >= d) c += u;
+            }
+            const int32_t prev = t0 + lane_mod - N;
+            if (prev >= 0 && in) c += CD[prev];
+            if (in) CD[t] = c;
+            int32_t y = wave_incl_scan((in ? KV[t] : 0) + c) + carry_kv;
+            carry_kv = __shfl(y, kWave - 1);
+            int32_t b = wave_incl_scan(in ? BI[t] : 0) + carry_b;
+            carry_b = __shfl(b, kWave - 1);
+            if (in) {
+                KV[t] = y;
+                BI[t] = b;
+                if (y > cap) last_over = t;
+            }
+        }
+    }
+    last_over = wave_max(last_over);
+    const bool has_bcap = P.batch_cap != nullptr;
+    const int32_t bcap = has_bcap ? P.batch_cap[s] : 0;
+    if (last_over >= 0 || (has_bcap && n_in > bcap)) fl |= TL_FLAG_OVERCOMMIT;
+
+    // FIFO admission of queued requests
+    int32_t* DA = CD;   // admitted-batch difference array
+    if (has_queue) {
+        for (int32_t t = lane; t < H; t += kWave) DA[t] = 0;
+        __syncthreads();
+        int32_t j = 0, run = 0;
+        int64_t cb = lo;
+        int32_t q_arr = 0, q_c = 0, q_len = 0, q_lost = 0;
+        uint64_t q_dl = kNoDeadline;
+        uint64_t mask = 0;
+        {
+            const int64_t i = cb + lane;
+            bool q = false;
+            if (i < hi) {
+                q_arr = P.arr[i];
+                const int32_t p = P.prompt[i], g = P.gen[i];
+                q_len = P.rem[i];
+                q = entry_ok(p, g, q_len, q_arr) && q_arr >= 0;
+                q_c = p + g;
+                q_lost = P.lost ? P.lost[i] : 0;
+                q_dl = P.deadline ? P.deadline[i] : kNoDeadline;
+            }
+            mask = __ballot(q);
+        }
+        for (;;) {
+            while (mask == 0) {
+                cb += kWave;
+                if (cb >= hi) break;
+                const int64_t i = cb + lane;
+                bool q = false;
+                if (i < hi) {
+                    q_arr = P.arr[i];
+                    const int32_t p = P.prompt[i], g = P.gen[i];
+                    q_len = P.rem[i];
+                    q = entry_ok(p, g, q_len, q_arr) && q_arr >= 0;
+                    q_c = p + g;
+                    q_lost = P.lost ? P.lost[i] : 0;
+                    q_dl = P.deadline ? P.deadline[i] : kNoDeadline;
+                }
+                mask = __ballot(q);
+            }
+            if (mask == 0) break;
+            const int hl = __ffsll((unsigned long long)mask) - 1;
+            const int32_t h_arr = __shfl(q_arr, hl);
+            const int32_t h_c = __shfl(q_c, hl);
+            const int32_t h_len = __shfl(q_len, hl);
+            const int32_t h_lost = __shfl(q_lost, hl);
+            const uint64_t h_dl = __shfl(q_dl, hl);
+            int32_t target = max(max(h_arr, j), last_over + 1);
+            if (h_arr >= H || target >= H) break;
+            if (target > j) {
+                run += sum_range(DA, j, target);
+                j = target;
+            }
+            bool admitted = false;
+            for (;;) {
+                bool ok = !has_bcap || (BI[j] + run < bcap);
+                if (ok) {
+                    const int32_t lim = (int32_t)min((int64_t)j + h_len, (int64_t)H);
+                    for (int32_t t0 = j; t0 < lim; t0 += kWave) {
+                        const int32_t t = t0 + lane;
+                        bool badt = false;
+                        if (t < lim)
+                            badt = KV[t] + (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN) > cap;
+                        if (__ballot(badt)) { ok = false; break; }
+                    }
+                }
+                if (ok) { admitted = true; break; }
+                if (j + 1 >= H) break;
+                run += DA[j + 1];
+                ++j;
+            }
+            if (!admitted) break;
+            const int64_t e = (int64_t)j + h_len;
+            const int32_t lim = (int32_t)min(e, (int64_t)H);
+            for (int32_t t0 = j; t0 < lim; t0 += kWave) {
+                const int32_t t = t0 + lane;
+                if (t < lim) KV[t] += (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN);
+            }
+            if (lane == 0) {
+                DA[j] += 1;
+                if (e < H) DA[e] -= 1;
+                if (e <= H && !h_lost && h_dl != kNoDeadline)
+                    atomicMin((unsigned long long*)&outDL[e - 1], (unsigned long long)h_dl);
+            }
+            __syncthreads();
+            run += 1;
+            n_end = max(n_end, lim);
+            mask &= mask - 1;
+        }
+    }
+    __syncthreads();
+
+    // outputs: curves, optional feature rows, scalars
+    {
+        int32_t carry_a = 0;
+        const float eng = (P.rows && P.nf == 4) ? P.engine[s] : 0.0f;
+        for (int32_t t0 = 0; t0 < H; t0 += kWave) {
+            const int32_t t = t0 + lane;
+            const bool in = t < H;
+            int32_t da = (has_queue && in) ? DA[t] : 0;
+            da = wave_incl_scan(da) + carry_a;
+            carry_a = __shfl(da, kWave - 1);
+            if (!in) continue;
+            const int32_t b = BI[t] + da;
+            const int32_t k = KV[t];
+            outB[t] = b;
+            outKV[t] = k;
+            if (P.rows) {
+                const float kf = (float)k, bf = (float)b;
+                for (int32_t f = 0; f < P.F; ++f) {
+                    float* row = P.rows + (((int64_t)s * P.F + f) * H + t) * P.nf;
+                    if (P.nf == 4) {
+                        *(float4*)row = make_float4(P.freqs[f], kf, bf, eng);
+                    } else {
+                        row[0] = P.freqs[f];
+                        row[1] = kf;
+                        row[2] = bf;
+                    }
+                }
+            }
+        }
+    }
+    if (lane == 0) {
+        P.n_iters[s] = n_end;
+        P.flags[s] = fl;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_project(const ProjectParams& p, hipStream_t stream) {
+    const size_t lds = (size_t)3 * p.H * sizeof(int32_t);
+    if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)project_kernel,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(project_kernel, dim3((unsigned)p.n_scenarios), dim3(64), lds, stream, p);
+    return hipGetLastError();
+}
+
+}  // namespace tl

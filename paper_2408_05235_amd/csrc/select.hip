@@ -1,0 +1,92 @@
+// Stage 3: the throttling controller (Sec. 4.5) with the TBT and E2E checks of
+// Sec. 4.3.2 (checks 2 and 3, Eq. 3-4).
+//
+// One 256-thread workgroup per scenario; its four wavefronts take the
+// candidate frequencies in turn.  For one frequency a wave walks the projected
+// iterations 64 at a time: per-iteration time in integer ns, an inclusive
+// wave scan plus the running carry gives Eq. 3's cumulative time T_R[j+1],
+// which is compared with the deadline of requests ending at j.  The walk stops
+// at the first violated deadline.  Feasible frequencies are collected as a
+// bitmask in LDS and the lowest one is taken.
+#include "device_util.h"
+#include "tl_internal.h"
+
+namespace tl {
+namespace {
+
+constexpr uint64_t kNoDeadline = ~0ull;
+constexpr uint64_t kSat = 1ull << 40;
+
+// T'_j = 1 / T_j in whole ns, rounded up; IEEE fp64 division
+__device__ __forceinline__ uint64_t latency_ns(float ips) {
+    if (!(ips > 0.0f)) return kSat;
+    const double q = 1e9 / (double)ips;
+    if (!(q < 1099511627776.0)) return kSat;
+    return (uint64_t)ceil(q);
+}
+
+constexpr int kWavesPerBlock = 4;
+
+__global__ __launch_bounds__(256) void select_kernel(SelectParams P) {
+    __shared__ uint32_t feasible[TL_MAX_FREQS / 32];
+    const int64_t s = blockIdx.x;
+    const int wave = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const int32_t F = P.F, H = P.H;
+    const uint32_t fl = P.proj_flags ? P.proj_flags[s] : 0u;
+    if (fl & (TL_FLAG_OVERFLOW | TL_FLAG_LOST)) {
+        if (threadIdx.x == 0) {
+            P.freq_idx[s] = F - 1;
+            P.status[s] = (fl & TL_FLAG_OVERFLOW) ? TL_STATUS_INVALID : TL_STATUS_LOST;
+        }
+        return;
+    }
+    const int32_t n = min(max(P.n_iters[s], 0), H);
+    if (n == 0) {
+        if (threadIdx.x == 0) {
+            P.freq_idx[s] = 0;
+            P.status[s] = TL_STATUS_OK;
+        }
+        return;
+    }
+    const int32_t n_words = (F + 31) / 32;
+    for (int w = threadIdx.x; w < n_words; w += blockDim.x) feasible[w] = 0;
+    __syncthreads();
+
+    const uint64_t slo = P.tbt_slo_ns[s];
+    const uint64_t budget = (slo > ~0ull / (uint64_t)n) ? ~0ull : slo * (uint64_t)n;
+    const uint64_t* dl = P.deadline_at + s * H;
+    for (int32_t f = wave; f < F; f += kWavesPerBlock) {
+        const float* ips = P.ips + ((int64_t)s * F + f) * H;
+        uint64_t carry = 0;
+        bool ok = true;
+        for (int32_t j0 = 0; j0 < n; j0 += kWave) {
+            const int32_t j = j0 + lane;
+            const bool in = j < n;
+            const uint64_t lat = in ? latency_ns(ips[j]) : 0ull;
+            const uint64_t tr = wave_incl_scan_u64(lat) + carry;
+            const uint64_t d = in ? dl[j] : kNoDeadline;
+            const bool bad = in && d != kNoDeadline && !(tr < d);
+            carry = __shfl(tr, kWave - 1);
+            if (__ballot(bad)) { ok = false; break; }
+        }
+        if (ok && carry <= budget && lane == 0) atomicOr(&feasible[f >> 5], 1u << (f & 31));
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t best = -1;
+        for (int32_t w = 0; w < n_words; ++w)
+            if (feasible[w]) { best = w * 32 + __ffs(feasible[w]) - 1; break; }
+        P.freq_idx[s] = best >= 0 ? best : F - 1;
+        P.status[s] = best >= 0 ? TL_STATUS_OK : TL_STATUS_INFEASIBLE;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_select(const SelectParams& p, hipStream_t stream) {
+    hipLaunchKernelGGL(select_kernel, dim3((unsigned)p.S), dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
+}  // namespace tl

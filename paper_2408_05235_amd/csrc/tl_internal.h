@@ -1,0 +1,64 @@
+// Internal interface between the host API (api.cpp) and the kernel sources.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tl.h"
+
+namespace tl {
+
+struct ProjectParams {
+    int64_t n_scenarios;
+    int64_t n_requests;
+    int32_t H;
+    int32_t N;
+    uint32_t div_m, div_l;          // invariant-divisor constants for N
+    const int64_t* off;
+    const int32_t* prompt;
+    const int32_t* gen;
+    const int32_t* rem;
+    const int32_t* arr;
+    const uint64_t* deadline;       // nullable
+    const uint8_t* lost;            // nullable
+    const int32_t* kv_cap;
+    const int32_t* batch_cap;       // nullable
+    int32_t* batch;
+    int32_t* kv;
+    uint64_t* deadline_at;
+    int32_t* n_iters;
+    uint32_t* flags;
+    int32_t F;
+    int32_t nf;
+    const float* freqs;
+    const float* engine;
+    float* rows;                    // nullable
+};
+
+struct SelectParams {
+    const float* ips;
+    int64_t S;
+    int32_t F;
+    int32_t H;
+    const uint64_t* deadline_at;
+    const int32_t* n_iters;
+    const uint64_t* tbt_slo_ns;
+    const uint32_t* proj_flags;     // nullable
+    int32_t* freq_idx;
+    uint32_t* status;
+};
+
+// Device copy of a tree ensemble.
+struct ForestDev {
+    int32_t n_trees, depth, n_features;
+    float base_score;
+    const uint2* nodes;     // [T][2^d - 1]: .x = threshold bits, .y = feature
+    const double* leaves;   // [T][2^d], exact fp64 copies of the fp32 leaves
+};
+
+hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
+hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,
+                              hipStream_t stream);
+hipError_t launch_select(const SelectParams& p, hipStream_t stream);
+
+}  // namespace tl

@@ -1,0 +1,357 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Projections, selected frequencies and statuses must match bit for bit; the
+ensemble outputs must match within 1e-5 relative (they are expected to be
+bit-identical, and the tests also count exact matches).  Inputs come only
+from the seeded generator or are written here; expected values come only
+from the oracle or the hand-computed fixtures.
+"""
+import numpy as np
+import pytest
+
+import goldens
+import oracle
+from paper_2408_05235_amd import configs, synth
+
+pytestmark = pytest.mark.gpu
+
+NONE = np.uint64(0xFFFFFFFFFFFFFFFF)
+RTOL = 1e-5
+
+
+def _api():
+    from paper_2408_05235_amd import api
+    return api
+
+
+def _np(t, dtype=None):
+    a = t.detach().cpu().numpy()
+    if dtype is not None:
+        a = a.view(dtype)
+    return a
+
+
+def gpu_project(inp, rows=False, freqs=None, engine=None, n_features=3):
+    import torch
+    api = _api()
+    d = api.upload(dict(inp, tbt_slo_ns=np.zeros(inp["n_scenarios"], np.uint64),
+                        freqs_mhz=np.zeros(1, np.float32) if freqs is None else freqs,
+                        engine_size=engine, n_features=n_features))
+    out = api.tl_project(d["req_offset"], d["prompt"], d["generated"], d["remaining"], d["arrival"],
+                         d["kv_capacity"], d["horizon"], d["block_tokens"], d["deadline_ns"], d["lost"],
+                         d["batch_cap"], d["freqs_mhz"] if rows else None, d["engine_size"], n_features, rows)
+    torch.cuda.synchronize()
+    res = dict(batch=_np(out["batch"]), kv=_np(out["kv"]), deadline_at=_np(out["deadline_at"], np.uint64),
+               n_iters=_np(out["n_iters"]), flags=_np(out["flags"], np.uint32))
+    if rows:
+        res["rows"] = _np(out["rows"])
+    return res
+
+
+def assert_projection_equal(g, o, where=""):
+    for k in ("batch", "kv", "deadline_at", "n_iters", "flags"):
+        a, b = np.asarray(g[k]), np.asarray(o[k])
+        if not np.array_equal(a, b):
+            bad = np.argwhere(a != b)
+            raise AssertionError(f"{where} {k} differs at {bad[:5].tolist()}: gpu {a[tuple(bad[0])]} oracle {b[tuple(bad[0])]}")
+
+
+def assert_ips_close(g, o, where=""):
+    g = np.asarray(g, np.float32)
+    o = np.asarray(o, np.float32)
+    assert g.shape == o.shape
+    both_nan = np.isnan(g) & np.isnan(o)
+    ok = both_nan | (g == o) | (np.abs(g.astype(np.float64) - o) <= RTOL * np.abs(o.astype(np.float64)))
+    assert ok.all(), f"{where} ips mismatch at {np.argwhere(~ok)[:5].tolist()}"
+    return int(((g == o) | both_nan).sum())
+
+
+# --------------------------------------------------------------- fixtures
+
+@pytest.mark.parametrize("name", ["proj_inflight_eq1_eq2.json", "proj_batchcap_fifo.json",
+                                  "proj_kv_blocked_fifo.json", "proj_overcommit_blocks_queue.json"])
+def test_golden_projection_gpu(gpu, name):
+    g = goldens.load(name)
+    out = gpu_project(goldens.scoreboard(g))
+    ex = g["expect"]
+    assert out["batch"][0].tolist() == ex["batch"]
+    assert out["kv"][0].tolist() == ex["kv"]
+    assert np.array_equal(out["deadline_at"][0], goldens.deadline_map(ex["deadline_at"]))
+    assert int(out["n_iters"][0]) == ex["n_iters"]
+    assert int(out["flags"][0]) == ex["flags"]
+
+
+def test_golden_selection_gpu(gpu):
+    import torch
+    api = _api()
+    g = goldens.load("select_two_stumps.json")
+    forest = api.Forest.from_dict(goldens.forest(g))
+    freqs = np.array(g["freqs_mhz"], np.float32)
+    for case in g["cases"]:
+        sigma = case["sigma_ns"]
+        inp = goldens.scoreboard(g, deadline_ns=[sigma * r for r in g["remaining"]], lost=case["lost"])
+        inp.update(tbt_slo_ns=np.array([sigma], np.uint64), freqs_mhz=freqs, engine_size=None, n_features=3)
+        d = api.upload(inp)
+        ctl = api.Controller(d, forest)
+        idx, st = ctl.step()
+        torch.cuda.synchronize()
+        assert _np(ctl.ips)[0].tolist() == g["expect_ips"]
+        assert (int(idx[0]), int(st[0])) == (case["freq_idx"], case["status"]), case
+
+
+# -------------------------------------------------- projection, random boards
+
+def random_boards(rng, S, H, N, rmax=40, qfrac=0.3, bad=0.03, lost=0.02, unsorted=False, cap=None):
+    counts = rng.integers(0, rmax + 1, S)
+    counts[rng.random(S) < 0.05] = 0                     # empty scenarios
+    off = np.zeros(S + 1, np.int64)
+    np.cumsum(counts, out=off[1:])
+    R = int(off[-1])
+    prompt = rng.integers(0, 3 * N * 8 + 50, R).astype(np.int32)
+    gen = rng.integers(0, 30, R).astype(np.int32)
+    rem = rng.integers(1, 2 * H + 2, R).astype(np.int32)
+    arr = np.full(R, -1, np.int32)
+    for s in range(S):
+        lo, hi = off[s], off[s + 1]
+        nq = int(rng.binomial(hi - lo, qfrac))
+        if nq:
+            a = np.sort(rng.integers(0, H + 5, nq)).astype(np.int32)
+            if unsorted and nq > 1 and rng.random() < 0.5:
+                rng.shuffle(a)
+            arr[hi - nq:hi] = a
+            gen[hi - nq:hi] = 0
+    m = rng.random(R) < bad
+    prompt[m & (rng.random(R) < 0.5)] = -3
+    rem[m & (rng.random(R) < 0.5)] = 0
+    dl = (rng.integers(1, 10 ** 9, R)).astype(np.uint64)
+    dl[rng.random(R) < 0.2] = NONE
+    if cap is None:
+        cap = rng.integers(N * 4, N * 40 + 200, S).astype(np.int32)
+    return dict(n_scenarios=S, horizon=H, block_tokens=N, req_offset=off, prompt=prompt, generated=gen,
+                remaining=rem, arrival=arr, deadline_ns=dl,
+                lost=(rng.random(R) < lost).astype(np.uint8),
+                kv_capacity=np.asarray(cap, np.int32),
+                batch_cap=rng.integers(1, 30, S).astype(np.int32) if rng.random() < 0.5 else None)
+
+
+@pytest.mark.parametrize("H,N,seed", [(1, 16, 0), (7, 1, 1), (64, 16, 2), (100, 3, 3), (513, 16, 4),
+                                      (1000, 64, 5), (257, 100, 6), (2048, 16, 7), (130, 7, 8)])
+def test_project_random_boards(gpu, H, N, seed):
+    rng = np.random.default_rng(seed)
+    inp = random_boards(rng, 300, H, N, unsorted=(seed % 2 == 1))
+    g = gpu_project(inp)
+    o = oracle.project(inp)
+    assert_projection_equal(g, o, f"H={H} N={N}")
+    # the cases that matter were exercised
+    fl = o["flags"]
+    assert (fl & oracle.FLAG_BAD_REQUEST).any() and (fl & oracle.FLAG_LOST).any()
+
+
+def test_project_max_horizon_and_long_lifetimes(gpu):
+    rng = np.random.default_rng(42)
+    inp = random_boards(rng, 24, 8192, 16, rmax=60, qfrac=0.5)
+    inp["remaining"] = rng.integers(1, 9000, inp["prompt"].size).astype(np.int32)
+    assert_projection_equal(gpu_project(inp), oracle.project(inp), "H=8192")
+
+
+def test_project_overcommit_and_caps(gpu):
+    rng = np.random.default_rng(9)
+    inp = random_boards(rng, 400, 300, 4, rmax=50, qfrac=0.5, cap=rng.integers(0, 120, 400))
+    o = oracle.project(inp)
+    assert (o["flags"] & oracle.FLAG_OVERCOMMIT).any()
+    assert_projection_equal(gpu_project(inp), o, "overcommit")
+
+
+def test_project_size_guard(gpu):
+    H, N = 16, 1
+    big = 1 << 30
+    inp = dict(n_scenarios=3, horizon=H, block_tokens=N, req_offset=np.array([0, 1, 4, 4], np.int64),
+               prompt=np.array([big, big, big, big], np.int32), generated=np.zeros(4, np.int32),
+               remaining=np.array([4, 4, 4, 4], np.int32), arrival=np.full(4, -1, np.int32),
+               deadline_ns=None, lost=None, kv_capacity=np.array([2 ** 31 - 1] * 3, np.int32), batch_cap=None)
+    g = gpu_project(inp)
+    assert_projection_equal(g, oracle.project(inp), "guard")
+    assert g["flags"].tolist() == [0, oracle.FLAG_OVERFLOW, 0]
+
+
+def test_project_rejects_bad_request_ranges_on_device(gpu):
+    """Offsets outside [0, n_requests] are flagged, not read."""
+    inp = dict(n_scenarios=3, horizon=8, block_tokens=4, req_offset=np.array([0, 2, 1, 3], np.int64),
+               prompt=np.array([4, 4, 4], np.int32), generated=np.zeros(3, np.int32),
+               remaining=np.array([3, 3, 3], np.int32), arrival=np.full(3, -1, np.int32),
+               deadline_ns=None, lost=None, kv_capacity=np.array([100] * 3, np.int32), batch_cap=None)
+    g = gpu_project(inp)
+    assert g["flags"].tolist() == [0, oracle.FLAG_OVERFLOW, 0]
+    assert g["batch"][1].sum() == 0
+
+
+def test_project_rows(gpu):
+    rng = np.random.default_rng(3)
+    inp = random_boards(rng, 50, 200, 16)
+    freqs = synth.frequency_grid(17)
+    for nf in (3, 4):
+        engine = rng.choice([1.0, 2.0, 4.0, 8.0], 50).astype(np.float32) if nf == 4 else None
+        g = gpu_project(inp, rows=True, freqs=freqs, engine=engine, n_features=nf)
+        o = oracle.project(inp)
+        assert_projection_equal(g, o, "rows")
+        x = oracle.rows(freqs, o["batch"], o["kv"], engine, nf)
+        assert np.array_equal(g["rows"], x)
+
+
+# ------------------------------------------------------------------ forest
+
+def random_forest(rng, T, d, nf, kvmax=5000, bmax=300):
+    n_int = (1 << d) - 1
+    feat = rng.integers(0, nf, (T, n_int)).astype(np.uint8)
+    hi = np.array([2000.0, kvmax, bmax, 8.0][:nf])
+    lo = np.array([1000.0, 0.0, 0.0, 1.0][:nf])
+    thr = (lo[feat] + (hi[feat] - lo[feat]) * rng.random((T, n_int))).astype(np.float32)
+    snap = rng.random((T, n_int)) < 0.2
+    thr[snap] = np.rint(thr[snap])
+    thr[rng.random((T, n_int)) < 0.01] = np.inf
+    thr[rng.random((T, n_int)) < 0.01] = -np.inf
+    leaf = rng.normal(0, 1, (T, 1 << d)).astype(np.float32)
+    return dict(n_trees=T, depth=d, n_features=nf, base_score=np.float32(rng.normal(40, 5)),
+                feature=feat, threshold=thr, leaf=leaf)
+
+
+def random_rows(rng, n, nf, kvmax=5000, bmax=300):
+    cols = [rng.choice(synth.frequency_grid(64), n), rng.integers(0, kvmax, n), rng.integers(0, bmax, n),
+            rng.choice([1.0, 2.0, 4.0, 8.0], n)]
+    x = np.stack(cols[:nf], axis=1).astype(np.float32)
+    x[rng.random(x.shape) < 0.001] = np.nan
+    return x
+
+
+@pytest.mark.parametrize("T,d,nf,n", [(0, 3, 3, 100), (1, 0, 3, 77), (5, 1, 1, 1000), (50, 6, 3, 12345),
+                                      (20, 10, 4, 4099), (7, 14, 2, 513), (300, 8, 3, 65537)])
+def test_forest_random(gpu, T, d, nf, n):
+    import torch
+    api = _api()
+    rng = np.random.default_rng(T * 31 + d)
+    fd = random_forest(rng, T, d, nf)
+    x = random_rows(rng, n, nf)
+    f = api.Forest.from_dict(fd)
+    got = _np(f.tl_forest_predict(torch.from_numpy(x).cuda()))
+    torch.cuda.synchronize()
+    exp = oracle.forest_predict(fd, x)
+    exact = assert_ips_close(got, exp, f"T={T} d={d}")
+    assert exact == n      # tree-order fp64 accumulation on both sides
+
+
+# --------------------------------------------------------------- selection
+
+def random_selection(rng, S, F, H):
+    ips = rng.uniform(5, 120, (S, F, H)).astype(np.float32)
+    special = rng.random((S, F, H))
+    ips[special < 0.002] = 0.0
+    ips[(special >= 0.002) & (special < 0.003)] = np.nan
+    ips[(special >= 0.003) & (special < 0.004)] = -1.0
+    ips[(special >= 0.004) & (special < 0.005)] = np.inf
+    ips[(special >= 0.005) & (special < 0.006)] = 1e-9
+    n = rng.integers(-2, H + 3, S).astype(np.int32)
+    dl = np.full((S, H), NONE, np.uint64)
+    nd = rng.integers(0, 6, S)
+    for s in range(S):
+        js = rng.integers(0, H, nd[s])
+        dl[s, js] = (rng.uniform(0.5, 1.5, js.size) * 30e6 * (js + 1)).astype(np.uint64)
+    tbt = rng.integers(5_000_000, 60_000_000, S).astype(np.uint64)
+    tbt[rng.random(S) < 0.01] = NONE          # saturating SLO budget
+    flags = np.zeros(S, np.uint32)
+    flags[rng.random(S) < 0.03] = oracle.FLAG_LOST
+    flags[rng.random(S) < 0.01] |= oracle.FLAG_OVERFLOW
+    flags[rng.random(S) < 0.05] |= oracle.FLAG_OVERCOMMIT
+    return ips, dl, n, tbt, flags
+
+
+def gpu_select(ips, dl, n, tbt, flags):
+    import torch
+    api = _api()
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    idx, st = api.tl_select_freq(t(ips), t(dl.view(np.int64)), t(n), t(tbt.view(np.int64)),
+                                 None if flags is None else t(flags.view(np.int32)))
+    torch.cuda.synchronize()
+    return _np(idx), _np(st)
+
+
+@pytest.mark.parametrize("S,F,H,seed", [(1, 1, 1, 0), (50, 17, 512, 1), (200, 64, 100, 2), (40, 100, 300, 3),
+                                        (300, 5, 65, 4), (10, 4096, 8, 5)])
+def test_select_random(gpu, S, F, H, seed):
+    rng = np.random.default_rng(seed)
+    ips, dl, n, tbt, flags = random_selection(rng, S, F, H)
+    gi, gs = gpu_select(ips, dl, n, tbt, flags)
+    oi, os_ = oracle.select(ips, dl, n, tbt, flags)
+    assert np.array_equal(gi, oi) and np.array_equal(gs.view(np.uint32), os_)
+    gi, gs = gpu_select(ips, dl, n, tbt, None)
+    oi, os_ = oracle.select(ips, dl, n, tbt, None)
+    assert np.array_equal(gi, oi) and np.array_equal(gs.view(np.uint32), os_)
+
+
+def test_select_full_shape_generated_ips(gpu):
+    """Selection alone at the forest-bound workload's shape (S=4096, F=64,
+    H=1024) on generated predictions, every scenario compared."""
+    rng = np.random.default_rng(77)
+    S, F, H = 4096, 64, 1024
+    ips = rng.normal(40, 6, (S, F, H)).astype(np.float32)
+    n = rng.integers(0, H + 1, S).astype(np.int32)
+    dl = np.full((S, H), NONE, np.uint64)
+    js = rng.integers(0, H, (S, 8))
+    for k in range(8):
+        dl[np.arange(S), js[:, k]] = (rng.uniform(0.8, 1.6, S) * 25e6 * (js[:, k] + 1)).astype(np.uint64)
+    tbt = rng.integers(10_000_000, 50_000_001, S).astype(np.uint64)
+    flags = np.zeros(S, np.uint32)
+    gi, gs = gpu_select(ips, dl, n, tbt, flags)
+    oi, os_ = oracle.select(ips, dl, n, tbt, flags)
+    assert np.array_equal(gi, oi) and np.array_equal(gs.view(np.uint32), os_)
+    assert len(np.unique(oi)) > 10
+
+
+# ---------------------------------------------------------- whole pipeline
+
+SCALED = [
+    (0, dict()),
+    (1, dict(n_scenarios=12)),
+    (2, dict(n_scenarios=6)),
+    (3, dict(n_scenarios=3, forest_n_trees=300)),
+    (4, dict(n_scenarios=6)),
+]
+
+
+@pytest.mark.parametrize("ci,over", SCALED, ids=[c["name"] for c in configs.CONFIGS])
+def test_pipeline_scaled_configs(gpu, ci, over):
+    import torch
+    api = _api()
+    cfg = synth.scaled(configs.get_config(ci), **over)
+    inp = synth.make_inputs(cfg)
+    ctl = api.Controller(api.upload(inp), api.Forest.from_dict(inp["forest"]))
+    idx, st = ctl.step()
+    torch.cuda.synchronize()
+    o = oracle.end_to_end(inp)
+    g = dict(batch=_np(ctl.buf["batch"]), kv=_np(ctl.buf["kv"]),
+             deadline_at=_np(ctl.buf["deadline_at"], np.uint64), n_iters=_np(ctl.buf["n_iters"]),
+             flags=_np(ctl.buf["flags"], np.uint32))
+    assert_projection_equal(g, o, cfg["name"])
+    exact = assert_ips_close(_np(ctl.ips), o["ips"], cfg["name"])
+    assert exact == o["ips"].size
+    assert np.array_equal(_np(idx), o["freq_idx"]) and np.array_equal(_np(st).view(np.uint32), o["status"])
+
+
+def test_determinism(gpu):
+    import torch
+    api = _api()
+    cfg = synth.scaled(configs.get_config(1), n_scenarios=20)
+    inp = synth.make_inputs(cfg)
+    ctl = api.Controller(api.upload(inp), api.Forest.from_dict(inp["forest"]))
+    ctl.step()
+    torch.cuda.synchronize()
+    a = [_np(ctl.ips).copy(), _np(ctl.buf["kv"]).copy(), _np(ctl.sel["freq_idx"]).copy()]
+    ctl.step()
+    torch.cuda.synchronize()
+    b = [_np(ctl.ips), _np(ctl.buf["kv"]), _np(ctl.sel["freq_idx"])]
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    # the same rows evaluated at a different offset (different launch grid)
+    rows = ctl.buf["rows"].reshape(-1, 3)
+    part = ctl.forest.tl_forest_predict(rows[1001:].contiguous())
+    torch.cuda.synchronize()
+    assert np.array_equal(_np(part), _np(ctl.ips).reshape(-1)[1001:])
