@@ -183,6 +183,23 @@ tl_status tl_forest_predict(const tl_forest* forest, const float* rows, int64_t 
                             float* out, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Stage 2 on the projection grid, fused with the row expansion: the same
+ * values tl_forest_predict gives for the rows tl_project would write, without
+ * materializing them (Sec. 4.3.2 check 2 and Sec. 4.5 query M for every
+ * projected iteration at every candidate frequency).
+ *   out[s][f][j] = M(freqs_mhz[f], kv[s][j], batch[s][j] [, engine_size[s]])
+ * freqs_mhz [F]; kv, batch [S][H] int32 as written by tl_project (converted
+ * to fp32); engine_size [S], required when the forest has 4 features and
+ * ignored otherwise; out [S][F][H] fp32.  The forest must have 3 or 4
+ * features in the order (frequency, KV, batch[, engine size]).
+ * 1 <= F <= TL_MAX_FREQS, 1 <= H <= TL_MAX_HORIZON.
+ * ---------------------------------------------------------------------- */
+tl_status tl_forest_predict_grid(const tl_forest* forest, int64_t n_scenarios, int32_t n_freqs,
+                                 int32_t horizon, const float* freqs_mhz, const int32_t* kv,
+                                 const int32_t* batch, const float* engine_size, float* out,
+                                 void* stream);
+
+/* ------------------------------------------------------------------------
  * Stage 3 -- frequency selection (Sec. 4.5 with Sec. 4.3.2 checks 2-3).
  *
  * ips [S][F][H] fp32: predicted iterations/s of scenario s at frequency f in

@@ -20,7 +20,7 @@ STATUS_OK, STATUS_INFEASIBLE, STATUS_LOST, STATUS_INVALID = 0, 1, 2, 3
 MAX_HORIZON, MAX_BLOCK_TOKENS, MAX_FREQS, MAX_FEATURES, MAX_DEPTH = 8192, 65536, 4096, 4, 14
 
 EXPORTED = ("tl_abi_version", "tl_last_error", "tl_forest_create", "tl_forest_destroy",
-            "tl_project", "tl_forest_predict", "tl_select_freq")
+            "tl_project", "tl_forest_predict", "tl_forest_predict_grid", "tl_select_freq")
 
 
 class ProjectArgs(ctypes.Structure):
@@ -66,6 +66,8 @@ def lib():
     L.tl_project.restype = ctypes.c_int
     L.tl_forest_predict.argtypes = [P, P, i64, P, P]
     L.tl_forest_predict.restype = ctypes.c_int
+    L.tl_forest_predict_grid.argtypes = [P, i64, i32, i32, P, P, P, P, P, P]
+    L.tl_forest_predict_grid.restype = ctypes.c_int
     L.tl_select_freq.argtypes = [P, i64, i32, i32, P, P, P, P, P, P, P]
     L.tl_select_freq.restype = ctypes.c_int
     _lib = L

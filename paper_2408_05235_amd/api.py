@@ -150,6 +150,27 @@ class Forest:
 
     predict = tl_forest_predict
 
+    def tl_forest_predict_grid(self, freqs_mhz, kv, batch, engine_size=None, out=None):
+        """IPS on the projection grid: out[s, f, j] = M(freqs[f], kv[s, j],
+        batch[s, j] [, engine[s]]) without materializing the rows."""
+        _need(kv, torch.int32, "kv")
+        if kv.dim() != 2:
+            raise ValueError("kv must be [S, H]")
+        S, H = kv.shape
+        F = freqs_mhz.numel()
+        _need(freqs_mhz, torch.float32, "freqs_mhz", (F,))
+        _need(batch, torch.int32, "batch", (S, H))
+        if self.n_features == 4:
+            _need(engine_size, torch.float32, "engine_size", (S,))
+        else:
+            engine_size = None
+        if out is None:
+            out = torch.empty((S, F, H), dtype=torch.float32, device=kv.device)
+        _need(out, torch.float32, "out", (S, F, H))
+        check(lib().tl_forest_predict_grid(self._h, S, F, H, _p(freqs_mhz), _p(kv), _p(batch),
+                                           _p(engine_size), _p(out), _stream()))
+        return out
+
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:
             lib().tl_forest_destroy(self._h)
@@ -214,11 +235,16 @@ def upload(inp, device="cuda"):
 class Controller:
     """The whole hot path for one batch of scenarios: project -> predict ->
     select, enqueued back to back on the current stream with preallocated
-    buffers (no host round trip between stages)."""
+    buffers (no host round trip between stages).
 
-    def __init__(self, dev_inputs, forest):
+    By default the feature rows are formed inside the forest kernel
+    (tl_forest_predict_grid); with ``materialize_rows=True`` tl_project writes
+    them and tl_forest_predict reads them back (same results)."""
+
+    def __init__(self, dev_inputs, forest, materialize_rows=False):
         self.d = dev_inputs
         self.forest = forest
+        self.materialize_rows = materialize_rows
         d = dev_inputs
         S, H = d["n_scenarios"], d["horizon"]
         F, nf = d["freqs_mhz"].numel(), d["n_features"]
@@ -229,8 +255,9 @@ class Controller:
             deadline_at=torch.empty((S, H), dtype=torch.int64, device=dev),
             n_iters=torch.empty(S, dtype=torch.int32, device=dev),
             flags=torch.empty(S, dtype=torch.int32, device=dev),
-            rows=torch.empty((S, F, H, nf), dtype=torch.float32, device=dev),
         )
+        if materialize_rows:
+            self.buf["rows"] = torch.empty((S, F, H, nf), dtype=torch.float32, device=dev)
         self.ips = torch.empty((S, F, H), dtype=torch.float32, device=dev)
         self.sel = dict(freq_idx=torch.empty(S, dtype=torch.int32, device=dev),
                         status=torch.empty(S, dtype=torch.int32, device=dev))
@@ -240,10 +267,13 @@ class Controller:
         return tl_project(d["req_offset"], d["prompt"], d["generated"], d["remaining"], d["arrival"],
                           d["kv_capacity"], d["horizon"], d["block_tokens"], d["deadline_ns"],
                           d["lost"], d["batch_cap"], d["freqs_mhz"], d["engine_size"],
-                          d["n_features"], True, self.buf)
+                          d["n_features"], self.materialize_rows, self.buf)
 
     def predict(self):
-        return self.forest.tl_forest_predict(self.buf["rows"], self.ips)
+        if self.materialize_rows:
+            return self.forest.tl_forest_predict(self.buf["rows"], self.ips)
+        return self.forest.tl_forest_predict_grid(self.d["freqs_mhz"], self.buf["kv"], self.buf["batch"],
+                                                  self.d["engine_size"], self.ips)
 
     def select(self):
         return tl_select_freq(self.ips, self.buf["deadline_at"], self.buf["n_iters"],

@@ -18,11 +18,47 @@ struct tl_forest {
     tl::ForestDev dev;
     void* nodes_mem;
     void* leaves_mem;
+    void* box_mem;
 };
 
 namespace {
 
 thread_local char g_err[512] = "";
+
+// KV / batch box of every leaf: the constraints that its path puts on
+// features 1 and 2.  Going to 2k+1 means x < thr (an upper bound); going to
+// 2k+2 means !(x < thr), i.e. x >= thr for non-NaN x (a lower bound).  A NaN
+// threshold sends every row to 2k+2: no constraint there, and nothing reaches
+// the 2k+1 side, whose leaves get an empty box.
+void leaf_boxes(int32_t n_trees, int32_t depth, const uint8_t* feature, const float* threshold,
+                std::vector<float4>& out) {
+    const int64_t n_int = (1ll << depth) - 1;
+    const int64_t n_leaf = 1ll << depth;
+    out.assign((size_t)(n_trees * n_leaf > 0 ? n_trees * n_leaf : 1), make_float4(0, 0, 0, 0));
+    for (int64_t t = 0; t < n_trees; ++t) {
+        const uint8_t* ft = feature + t * n_int;
+        const float* th = threshold + t * n_int;
+        for (int64_t L = 0; L < n_leaf; ++L) {
+            float lo[2] = {-INFINITY, -INFINITY}, hi[2] = {INFINITY, INFINITY};
+            bool empty = false;
+            int64_t k = 0;
+            for (int32_t l = 0; l < depth; ++l) {
+                const int bit = (int)((L >> (depth - 1 - l)) & 1);   // 0: to 2k+1, 1: to 2k+2
+                const float thr = th[k];
+                const int f = ft[k];
+                if (bit == 0) {
+                    if (std::isnan(thr)) empty = true;
+                    else if (f == 1 || f == 2) hi[f - 1] = std::fmin(hi[f - 1], thr);
+                } else if (!std::isnan(thr) && (f == 1 || f == 2)) {
+                    lo[f - 1] = std::fmax(lo[f - 1], thr);
+                }
+                k = 2 * k + 1 + bit;
+            }
+            out[(size_t)(t * n_leaf + L)] = empty ? make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY)
+                                                  : make_float4(lo[0], hi[0], lo[1], hi[1]);
+        }
+    }
+}
 
 tl_status fail(tl_status st, const char* fmt, ...) {
     va_list ap;
@@ -75,6 +111,8 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
         nodes[(size_t)i] = make_uint2(bits, feature[i]);
     }
     for (int64_t i = 0; i < (int64_t)n_trees * n_leaf; ++i) leaves[(size_t)i] = (double)leaf[i];
+    std::vector<float4> boxes;
+    if (n_features >= 3) leaf_boxes(n_trees, depth, feature, threshold, boxes);
 
     tl_forest* f = new (std::nothrow) tl_forest();
     if (!f) return fail(TL_ENOMEM, "tl_forest_create: host allocation failed");
@@ -84,12 +122,25 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     if (e != hipSuccess) { delete f; return from_hip(e, "tl_forest_create: hipMalloc(nodes)"); }
     e = hipMalloc(&f->leaves_mem, leaves.size() * sizeof(double));
     if (e != hipSuccess) { (void)hipFree(f->nodes_mem); delete f; return from_hip(e, "tl_forest_create: hipMalloc(leaves)"); }
+    f->box_mem = nullptr;
+    if (!boxes.empty()) {
+        e = hipMalloc(&f->box_mem, boxes.size() * sizeof(float4));
+        if (e != hipSuccess) {
+            (void)hipFree(f->nodes_mem);
+            (void)hipFree(f->leaves_mem);
+            delete f;
+            return from_hip(e, "tl_forest_create: hipMalloc(boxes)");
+        }
+    }
     e = hipMemcpy(f->nodes_mem, nodes.data(), nodes.size() * sizeof(uint2), hipMemcpyHostToDevice);
     if (e == hipSuccess)
         e = hipMemcpy(f->leaves_mem, leaves.data(), leaves.size() * sizeof(double), hipMemcpyHostToDevice);
+    if (e == hipSuccess && f->box_mem)
+        e = hipMemcpy(f->box_mem, boxes.data(), boxes.size() * sizeof(float4), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipFree(f->nodes_mem);
         (void)hipFree(f->leaves_mem);
+        if (f->box_mem) (void)hipFree(f->box_mem);
         delete f;
         return from_hip(e, "tl_forest_create: hipMemcpy");
     }
@@ -99,6 +150,7 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     f->dev.base_score = base_score;
     f->dev.nodes = (const uint2*)f->nodes_mem;
     f->dev.leaves = (const double*)f->leaves_mem;
+    f->dev.kvb_box = (const float4*)f->box_mem;
     *out = f;
     return ok();
 }
@@ -108,6 +160,7 @@ void tl_forest_destroy(tl_forest* f) {
     (void)hipDeviceSynchronize();
     (void)hipFree(f->nodes_mem);
     (void)hipFree(f->leaves_mem);
+    if (f->box_mem) (void)hipFree(f->box_mem);
     delete f;
 }
 
@@ -177,6 +230,36 @@ tl_status tl_forest_predict(const tl_forest* f, const float* rows, int64_t n_row
     if (n_rows == 0) return ok();
     return from_hip(tl::launch_forest_rows(f->dev, rows, n_rows, out, (hipStream_t)stream),
                     "tl_forest_predict: launch");
+}
+
+tl_status tl_forest_predict_grid(const tl_forest* f, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
+                                 const float* freqs_mhz, const int32_t* kv, const int32_t* batch,
+                                 const float* engine_size, float* out, void* stream) {
+    if (!f) return fail(TL_EINVAL, "tl_forest_predict_grid: forest is NULL");
+    if (f->dev.n_features != 3 && f->dev.n_features != 4)
+        return fail(TL_EINVAL, "tl_forest_predict_grid: the forest has %d features, the grid needs 3 or 4",
+                    f->dev.n_features);
+    if (n_scenarios < 0 || n_scenarios > 0x7fffffffll)
+        return fail(TL_EINVAL, "tl_forest_predict_grid: n_scenarios %lld outside [0, 2^31-1]", (long long)n_scenarios);
+    if (n_freqs < 1 || n_freqs > TL_MAX_FREQS)
+        return fail(TL_EINVAL, "tl_forest_predict_grid: n_freqs %d outside [1, %d]", n_freqs, TL_MAX_FREQS);
+    if (horizon < 1 || horizon > TL_MAX_HORIZON)
+        return fail(TL_EINVAL, "tl_forest_predict_grid: horizon %d outside [1, %d]", horizon, TL_MAX_HORIZON);
+    if (n_scenarios > 0 && (!freqs_mhz || !kv || !batch || !out))
+        return fail(TL_EINVAL, "tl_forest_predict_grid: NULL required pointer");
+    if (n_scenarios > 0 && f->dev.n_features == 4 && !engine_size)
+        return fail(TL_EINVAL, "tl_forest_predict_grid: a 4-feature forest needs engine_size");
+    if (n_scenarios == 0) return ok();
+    tl::GridParams g{};
+    g.S = n_scenarios;
+    g.F = n_freqs;
+    g.H = horizon;
+    g.freqs = freqs_mhz;
+    g.kv = kv;
+    g.batch = batch;
+    g.engine = f->dev.n_features == 4 ? engine_size : nullptr;
+    g.out = out;
+    return from_hip(tl::launch_forest_grid(f->dev, g, (hipStream_t)stream), "tl_forest_predict_grid: launch");
 }
 
 tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,

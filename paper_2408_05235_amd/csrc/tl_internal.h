@@ -54,11 +54,30 @@ struct ForestDev {
     float base_score;
     const uint2* nodes;     // [T][2^d - 1]: .x = threshold bits, .y = feature
     const double* leaves;   // [T][2^d], exact fp64 copies of the fp32 leaves
+    // Per leaf, the KV (feature 1) and batch (feature 2) constraints of its
+    // root-to-leaf path as half-open intervals (kv_lo, kv_hi, batch_lo,
+    // batch_hi): a row with lo <= x < hi in both features, and with the
+    // frequency and engine size of a row known to reach the leaf, reaches the
+    // same leaf.  Empty (lo = +inf) for leaves no row can reach.  Only present
+    // when n_features >= 3.
+    const float4* kvb_box;  // [T][2^d] or NULL
+};
+
+struct GridParams {
+    int64_t S;
+    int32_t F;
+    int32_t H;
+    const float* freqs;     // [F]
+    const int32_t* kv;      // [S][H]
+    const int32_t* batch;   // [S][H]
+    const float* engine;    // [S] (4 features) or NULL
+    float* out;             // [S][F][H]
 };
 
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,
                               hipStream_t stream);
+hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, hipStream_t stream);
 hipError_t launch_select(const SelectParams& p, hipStream_t stream);
 
 }  // namespace tl

@@ -239,6 +239,57 @@ def test_forest_random(gpu, T, d, nf, n):
     assert exact == n      # tree-order fp64 accumulation on both sides
 
 
+def random_curves(rng, S, H, kvmax=5000, bmax=300):
+    """Slowly varying KV / batch curves with jumps, like projections."""
+    kv = np.clip(rng.integers(0, kvmax, (S, 1)) + np.cumsum(rng.integers(-12, 10, (S, H)), axis=1), 0, None)
+    bs = np.clip(rng.integers(0, bmax, (S, 1)) + np.cumsum(rng.integers(-1, 1, (S, H)) * (rng.random((S, H)) < 0.2), axis=1), 0, None)
+    jump = rng.random((S, H)) < 0.01
+    kv = np.where(jump, rng.integers(0, kvmax, (S, H)), kv)
+    return kv.astype(np.int32), bs.astype(np.int32)
+
+
+@pytest.mark.parametrize("S,F,H,T,d,nf", [(3, 64, 1024, 40, 10, 4), (5, 17, 100, 30, 6, 3), (2, 130, 70, 20, 8, 3),
+                                          (4, 48, 33, 25, 8, 3), (1, 1, 1, 3, 2, 4), (2, 64, 64, 0, 4, 3),
+                                          (3, 32, 95, 10, 0, 3)])
+def test_forest_grid(gpu, S, F, H, T, d, nf):
+    """The fused grid kernel equals the oracle on the rows it stands for."""
+    import torch
+    api = _api()
+    rng = np.random.default_rng(S * 1000 + F + H + T)
+    fd = random_forest(rng, T, d, nf)
+    kv, bs = random_curves(rng, S, H)
+    freqs = synth.frequency_grid(F)
+    eng = rng.choice([1.0, 2.0, 4.0, 8.0], S).astype(np.float32) if nf == 4 else None
+    f = api.Forest.from_dict(fd)
+    t = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    got = _np(f.tl_forest_predict_grid(t(freqs), t(kv), t(bs), t(eng)))
+    torch.cuda.synchronize()
+    exp = oracle.forest_predict(fd, oracle.rows(freqs, bs, kv, eng, nf))
+    assert assert_ips_close(got, exp, "grid") == exp.size
+
+
+def test_forest_grid_nan_and_infinite_thresholds(gpu):
+    """Leaves behind NaN thresholds are unreachable; +-inf thresholds bound
+    nothing.  The box reuse must still give the tree-walk result."""
+    import torch
+    api = _api()
+    rng = np.random.default_rng(5)
+    fd = random_forest(rng, 30, 7, 3)
+    thr = fd["threshold"]
+    m = rng.random(thr.shape)
+    thr[m < 0.05] = np.nan
+    thr[(m >= 0.05) & (m < 0.1)] = np.inf
+    thr[(m >= 0.1) & (m < 0.15)] = -np.inf
+    kv, bs = random_curves(rng, 4, 300)
+    freqs = synth.frequency_grid(40)
+    f = api.Forest.from_dict(fd)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    got = _np(f.tl_forest_predict_grid(t(freqs), t(kv), t(bs)))
+    torch.cuda.synchronize()
+    exp = oracle.forest_predict(fd, oracle.rows(freqs, bs, kv, None, 3))
+    assert assert_ips_close(got, exp, "grid-nan") == exp.size
+
+
 # --------------------------------------------------------------- selection
 
 def random_selection(rng, S, F, H):
@@ -323,7 +374,8 @@ def test_pipeline_scaled_configs(gpu, ci, over):
     api = _api()
     cfg = synth.scaled(configs.get_config(ci), **over)
     inp = synth.make_inputs(cfg)
-    ctl = api.Controller(api.upload(inp), api.Forest.from_dict(inp["forest"]))
+    ctl = api.Controller(api.upload(inp), api.Forest.from_dict(inp["forest"]),
+                         materialize_rows=(ci % 2 == 1))
     idx, st = ctl.step()
     torch.cuda.synchronize()
     o = oracle.end_to_end(inp)
@@ -350,8 +402,11 @@ def test_determinism(gpu):
     b = [_np(ctl.ips), _np(ctl.buf["kv"]), _np(ctl.sel["freq_idx"])]
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
-    # the same rows evaluated at a different offset (different launch grid)
-    rows = ctl.buf["rows"].reshape(-1, 3)
+    # the materialized rows through the generic kernel, at an offset (a
+    # different launch grid), give the same values as the fused grid kernel
+    ctl2 = api.Controller(ctl.d, ctl.forest, materialize_rows=True)
+    ctl2.project()
+    rows = ctl2.buf["rows"].reshape(-1, 3)
     part = ctl.forest.tl_forest_predict(rows[1001:].contiguous())
     torch.cuda.synchronize()
     assert np.array_equal(_np(part), _np(ctl.ips).reshape(-1)[1001:])
