@@ -34,7 +34,7 @@ void leaf_boxes(int32_t n_trees, int32_t depth, const uint8_t* feature, const fl
                 std::vector<float4>& out) {
     const int64_t n_int = (1ll << depth) - 1;
     const int64_t n_leaf = 1ll << depth;
-    out.assign((size_t)(n_trees * n_leaf > 0 ? n_trees * n_leaf : 1), make_float4(0, 0, 0, 0));
+    out.assign((size_t)(n_trees * n_leaf), make_float4(0, 0, 0, 0));
     for (int64_t t = 0; t < n_trees; ++t) {
         const uint8_t* ft = feature + t * n_int;
         const float* th = threshold + t * n_int;
@@ -100,19 +100,27 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     const int64_t n_leaf = 1ll << depth;
     if (n_trees > 0 && (!leaf || (n_int > 0 && (!feature || !threshold))))
         return fail(TL_EINVAL, "tl_forest_create: NULL tree array");
-    std::vector<uint2> nodes((size_t)(n_trees * n_int > 0 ? n_trees * n_int : 1));
-    std::vector<double> leaves((size_t)(n_trees * n_leaf > 0 ? n_trees * n_leaf : 1));
-    for (int64_t i = 0; i < (int64_t)n_trees * n_int; ++i) {
-        if (feature[i] >= n_features)
-            return fail(TL_EINVAL, "tl_forest_create: node %lld uses feature %d >= n_features %d",
-                        (long long)i, (int)feature[i], n_features);
-        uint32_t bits;
-        std::memcpy(&bits, &threshold[i], 4);
-        nodes[(size_t)i] = make_uint2(bits, feature[i]);
-    }
-    for (int64_t i = 0; i < (int64_t)n_trees * n_leaf; ++i) leaves[(size_t)i] = (double)leaf[i];
+    // device arrays use a per-tree stride of 2^d entries and 64 bytes of tail
+    // padding, so staged blocks are whole, aligned 16-byte words
+    const size_t cells = (size_t)n_trees * n_leaf;
+    std::vector<uint2> nodes(cells + 8, make_uint2(0, 0));
+    std::vector<float> leaves(cells + 16, 0.0f);
+    for (int64_t t = 0; t < n_trees; ++t)
+        for (int64_t k = 0; k < n_int; ++k) {
+            const int64_t i = t * n_int + k;
+            if (feature[i] >= n_features)
+                return fail(TL_EINVAL, "tl_forest_create: node %lld uses feature %d >= n_features %d",
+                            (long long)i, (int)feature[i], n_features);
+            uint32_t bits;
+            std::memcpy(&bits, &threshold[i], 4);
+            nodes[(size_t)(t * n_leaf + k)] = make_uint2(bits, feature[i]);
+        }
+    for (size_t i = 0; i < cells; ++i) leaves[i] = leaf[i];
     std::vector<float4> boxes;
-    if (n_features >= 3) leaf_boxes(n_trees, depth, feature, threshold, boxes);
+    if (n_features >= 3) {
+        leaf_boxes(n_trees, depth, feature, threshold, boxes);
+        boxes.resize(cells + 4, make_float4(0, 0, 0, 0));
+    }
 
     tl_forest* f = new (std::nothrow) tl_forest();
     if (!f) return fail(TL_ENOMEM, "tl_forest_create: host allocation failed");
@@ -120,21 +128,20 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     if (e != hipSuccess) { delete f; return from_hip(e, "tl_forest_create: hipGetDevice"); }
     e = hipMalloc(&f->nodes_mem, nodes.size() * sizeof(uint2));
     if (e != hipSuccess) { delete f; return from_hip(e, "tl_forest_create: hipMalloc(nodes)"); }
-    e = hipMalloc(&f->leaves_mem, leaves.size() * sizeof(double));
+    e = hipMalloc(&f->leaves_mem, leaves.size() * sizeof(float));
     if (e != hipSuccess) { (void)hipFree(f->nodes_mem); delete f; return from_hip(e, "tl_forest_create: hipMalloc(leaves)"); }
     f->box_mem = nullptr;
-    if (!boxes.empty()) {
-        e = hipMalloc(&f->box_mem, boxes.size() * sizeof(float4));
-        if (e != hipSuccess) {
-            (void)hipFree(f->nodes_mem);
-            (void)hipFree(f->leaves_mem);
-            delete f;
-            return from_hip(e, "tl_forest_create: hipMalloc(boxes)");
-        }
+    if (!boxes.empty()) e = hipMalloc(&f->box_mem, boxes.size() * sizeof(float4));
+    if (e != hipSuccess) {
+        (void)hipFree(f->nodes_mem);
+        (void)hipFree(f->leaves_mem);
+        if (f->box_mem) (void)hipFree(f->box_mem);
+        delete f;
+        return from_hip(e, "tl_forest_create: hipMalloc");
     }
     e = hipMemcpy(f->nodes_mem, nodes.data(), nodes.size() * sizeof(uint2), hipMemcpyHostToDevice);
     if (e == hipSuccess)
-        e = hipMemcpy(f->leaves_mem, leaves.data(), leaves.size() * sizeof(double), hipMemcpyHostToDevice);
+        e = hipMemcpy(f->leaves_mem, leaves.data(), leaves.size() * sizeof(float), hipMemcpyHostToDevice);
     if (e == hipSuccess && f->box_mem)
         e = hipMemcpy(f->box_mem, boxes.data(), boxes.size() * sizeof(float4), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
@@ -149,7 +156,7 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     f->dev.n_features = n_features;
     f->dev.base_score = base_score;
     f->dev.nodes = (const uint2*)f->nodes_mem;
-    f->dev.leaves = (const double*)f->leaves_mem;
+    f->dev.leaves = (const float*)f->leaves_mem;
     f->dev.kvb_box = (const float4*)f->box_mem;
     *out = f;
     return ok();

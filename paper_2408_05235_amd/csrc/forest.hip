@@ -1,28 +1,37 @@
 // Stage 2: the performance model M (Sec. 4.3.1), a gradient-boosted tree
-// ensemble, evaluated on fp32 feature rows.
+// ensemble, evaluated on fp32 feature rows.  Every kernel here computes, for
+// each row, base + the leaf of every tree, accumulated in fp64 in tree order
+// and rounded once to fp32.
 //
-// Two kernels compute the same function.
-//
-// forest_grid_kernel evaluates the rows of the projection grid without
+// Grid kernels evaluate the rows of the projection grid without
 // materializing them: row (s, f, j) = (freq[f], kv[s][j], batch[s][j]
 // [, engine[s]]).  One wavefront takes one scenario and J consecutive future
 // iterations; its lanes are the candidate frequencies, so every lane sees the
 // same (KV, batch) sequence.  For each tree (in order) a lane keeps the leaf
-// reached by its previous row together with that leaf's KV / batch box; the
-// next row reuses the leaf while its (KV, batch) stays inside the box, which
-// is exact because frequency and engine size are fixed for the lane.  Only
-// rows that leave the box walk the tree again.  Between consecutive future
+// reached by its previous row together with the KV / batch box of that leaf
+// (the bounds its root-to-leaf path puts on those two features); the next row
+// reuses the leaf while its (KV, batch) stays inside the box.  This is exact:
+// frequency and engine size are fixed for the lane, so a row inside the box
+// takes every decision of the path the same way.  Between consecutive future
 // iterations KV and batch move little, so most rows cost a box test and one
-// fp64 add per tree instead of a depth-long walk.
+// fp64 add per tree; a walk happens on roughly one row in twenty.
 //
-// forest_rows_kernel evaluates arbitrary rows.  Each thread evaluates RPT
-// consecutive rows.  Rows produced by the projection
-// are ordered [scenario][frequency][iteration], so a thread's rows -- and the
-// 64 x RPT rows of a wavefront -- are consecutive future iterations at one
-// frequency.  Their (KV, batch) values change slowly, so lanes of a wave walk
-// the same nodes most of the time and node loads are mostly broadcasts.
-// Trees are visited in order and the leaf values are accumulated in fp64 in
-// that order, then rounded once to fp32.
+//   forest_grid_lds_kernel     (depth <= 11) A 1024-thread workgroup (16
+//       wavefronts, 16 x 16 x 64 rows) walks the ensemble in blocks of trees
+//       that are staged in LDS, double-buffered: the next block is fetched
+//       into registers while the current one is evaluated: nodes, leaf
+//       values and leaf boxes.  Tree walks read LDS only.  The wavefront's
+//       (KV, batch) pairs are uniform and live in scalar registers.
+//   forest_grid_global_kernel  (deeper trees) The same per-lane scheme with
+//       nodes, leaves and boxes read from global memory.
+//
+// Device layout (built by tl_forest_create): nodes [T][2^d] (8 bytes:
+// threshold bits, feature; the last entry of each tree is padding), leaves
+// [T][2^d] fp32, and for 3-4 features the leaf boxes [T][2^d] (kv_lo, kv_hi,
+// batch_lo, batch_hi).
+//
+// forest_rows_kernel evaluates arbitrary rows: each thread walks RPT
+// consecutive rows through every tree.
 #include "device_util.h"
 #include "tl_internal.h"
 
@@ -37,9 +46,16 @@ __device__ __forceinline__ float pick(const float (&x)[4], uint32_t f) {
     return f == 0 ? x[0] : (f == 1 ? x[1] : (f == 2 ? x[2] : x[3]));
 }
 
+// grid row features: 0 frequency, 1 KV, 2 batch, 3 engine size
+template <int NF>
+__device__ __forceinline__ float pick_grid(uint32_t ft, float xf, float kv, float bs, float xe) {
+    if (NF == 3) return ft == 0 ? xf : (ft == 1 ? kv : bs);
+    return ft == 0 ? xf : (ft == 1 ? kv : (ft == 2 ? bs : xe));
+}
+
 template <int NF, int RPT>
 __global__ __launch_bounds__(256) void forest_rows_kernel(const uint2* __restrict__ nodes,
-                                                          const double* __restrict__ leaves,
+                                                          const float* __restrict__ leaves,
                                                           int32_t n_trees, int32_t depth, float base,
                                                           const float* __restrict__ rows, int64_t n_rows,
                                                           float* __restrict__ out) {
@@ -62,8 +78,8 @@ __global__ __launch_bounds__(256) void forest_rows_kernel(const uint2* __restric
     const int32_t n_int = (1 << depth) - 1;
     const int32_t n_leaf = 1 << depth;
     for (int32_t t = 0; t < n_trees; ++t) {
-        const uint2* nt = nodes + (int64_t)t * n_int;
-        const double* lt = leaves + (int64_t)t * n_leaf;
+        const uint2* nt = nodes + (int64_t)t * n_leaf;
+        const float* lt = leaves + (int64_t)t * n_leaf;
         int32_t k[RPT];
 #pragma unroll
         for (int r = 0; r < RPT; ++r) k[r] = 0;
@@ -76,47 +92,233 @@ __global__ __launch_bounds__(256) void forest_rows_kernel(const uint2* __restric
             }
         }
 #pragma unroll
-        for (int r = 0; r < RPT; ++r) acc[r] += lt[k[r] - n_int];
+        for (int r = 0; r < RPT; ++r) acc[r] += (double)lt[k[r] - n_int];
     }
 #pragma unroll
     for (int r = 0; r < RPT; ++r)
         if (r < nr) out[r0 + r] = (float)acc[r];
 }
 
-constexpr int kGridJ = 32;            // iterations per wavefront
-constexpr int kGridWaves = 4;         // wavefronts per workgroup
+constexpr int kLdsJ = 16;                // future iterations per wavefront (LDS kernel)
+constexpr int kGlobalJ = 32;             // future iterations per wavefront (global kernel)
 
-template <int NF, int J>
-__global__ __launch_bounds__(256) void forest_grid_kernel(const uint2* __restrict__ nodes,
-                                                          const double* __restrict__ leaves,
-                                                          const float4* __restrict__ boxes,
-                                                          int32_t n_trees, int32_t depth, float base,
-                                                          GridParams P) {
-    __shared__ float2 kvb[kGridWaves][J];
-    const int wave = threadIdx.x / kWave;
-    const int lane = lane_id();
-    const int32_t H = P.H, F = P.F;
-    const int32_t n_chunks = (H + J - 1) / J;
-    const int32_t n_fg = (F + kWave - 1) / kWave;
-    const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kGridWaves + wave);
-    const bool valid = item < P.S * n_fg * n_chunks;   // uniform per wave
-    const int64_t it = valid ? item : 0;
+// Which (scenario, frequency group, iteration chunk) a wavefront evaluates.
+struct GridItem {
+    bool valid;
+    int64_t s;
+    int32_t f, j0, nj;
+};
+
+__device__ __forceinline__ GridItem grid_item(const GridParams& P, int64_t item, int J) {
+    const int32_t n_chunks = (P.H + J - 1) / J;
+    const int32_t n_fg = (P.F + kWave - 1) / kWave;
+    GridItem g;
+    g.valid = item < P.S * n_fg * n_chunks;
+    const int64_t it = g.valid ? item : 0;
     const int32_t chunk = (int32_t)(it % n_chunks);
     const int64_t rest = it / n_chunks;
-    const int32_t fg = (int32_t)(rest % n_fg);
-    const int64_t s = rest / n_fg;
-    const int32_t f = fg * kWave + lane;
-    const bool active = valid && f < F;
-    const float xf = P.freqs[f < F ? f : F - 1];
-    const float xe = (NF == 4) ? P.engine[s] : 0.0f;
-    const int32_t j0 = chunk * J;
-    const int32_t nj = min(J, H - j0);
-    if (lane < J) {
-        const int32_t j = j0 + min(lane, nj - 1);
-        kvb[wave][lane] = make_float2((float)P.kv[s * H + j], (float)P.batch[s * H + j]);
+    g.f = (int32_t)(rest % n_fg) * kWave + lane_id();
+    g.s = rest / n_fg;
+    g.j0 = chunk * J;
+    g.nj = min(J, P.H - g.j0);
+    return g;
+}
+
+// ---------------------------------------------------------------- LDS-staged
+
+constexpr int kLdsWaves = 16;            // wavefronts per workgroup
+constexpr int kLdsThreads = kLdsWaves * kWave;
+constexpr int kStageRegs = 4;            // staged 16-byte words per thread per block
+constexpr int kMaxLdsDepth = 11;
+
+// Per staged tree: 2^d nodes (8 bytes, the last one padding), 2^d leaf
+// values (4 bytes) and 2^d leaf boxes (16 bytes), each segment contiguous
+// over the trees of a block.
+struct StageLayout {
+    uint32_t nodes, vals, boxes, stride;   // byte offsets inside a buffer, buffer size
+};
+
+__host__ __device__ inline StageLayout stage_layout(int32_t tb, int32_t n_leaf) {
+    StageLayout L;
+    L.nodes = 0;
+    L.vals = (uint32_t)tb * n_leaf * 8u;
+    L.boxes = L.vals + (((uint32_t)tb * n_leaf * 4u + 15u) & ~15u);
+    L.stride = L.boxes + (uint32_t)tb * n_leaf * 16u;
+    return L;
+}
+
+template <int NF, int J>
+__global__ __launch_bounds__(kLdsThreads) void forest_grid_lds_kernel(const uint2* __restrict__ nodes,
+                                                                      const float* __restrict__ leaves,
+                                                                      const float4* __restrict__ boxes,
+                                                                      int32_t n_trees, int32_t depth,
+                                                                      int32_t tb, float base, GridParams P) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int32_t n_int = (1 << depth) - 1;
+    const int32_t n_leaf = 1 << depth;
+    const StageLayout L = stage_layout(tb, n_leaf);
+
+    const int wave = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kLdsWaves + wave);
+    const GridItem g = grid_item(P, item, J);
+    const int32_t F = P.F, H = P.H;
+    const bool active = g.valid && g.f < F;
+    const float xf = P.freqs[g.f < F ? g.f : F - 1];
+    const float xe = (NF == 4) ? P.engine[g.s] : 0.0f;
+    // the J (KV, batch) pairs of this wavefront are the same for every lane:
+    // keep them in scalar registers
+    float skv[J], sbs[J];
+    {
+        const int32_t j = g.j0 + min(lane % J, g.nj - 1);
+        const float kvl = (float)P.kv[g.s * H + j], bsl = (float)P.batch[g.s * H + j];
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            skv[jj] = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(kvl), jj));
+            sbs[jj] = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(bsl), jj));
+        }
+    }
+
+    // staging: block b holds trees [b*tb, b*tb + cnt), copied as 16-byte words
+    // from the three global arrays (the host pads them so whole words exist).
+    // Each thread moves up to kStageRegs words: one load per word straight
+    // into its own register, so the loads stay in flight while the current
+    // block is evaluated.
+    const int32_t n_blocks = (n_trees + tb - 1) / tb;
+    static_assert(kStageRegs == 4, "staging code below moves four words per thread");
+    uint4 rw0 = make_uint4(0, 0, 0, 0), rw1 = rw0, rw2 = rw0, rw3 = rw0;
+    double acc[J];
+#pragma unroll
+    for (int jj = 0; jj < J; ++jj) acc[jj] = (double)base;
+
+#define TL_STAGE_WORDS(b)                                                      \
+    const int32_t cnt_ = min(tb, n_trees - (b) * tb);                          \
+    const int32_t wn = (cnt_ * n_leaf * 8 + 15) / 16;                          \
+    const int32_t wv = (cnt_ * n_leaf * 4 + 15) / 16;                          \
+    const int32_t wt = wn + wv + cnt_ * n_leaf;
+#define TL_FETCH_WORD(r, reg)                                                  \
+    {                                                                          \
+        /* unconditional (threads past the block re-read word 0), so the   */ \
+        /* four loads issue back to back without waits between them        */ \
+        const int32_t i0 = (int32_t)threadIdx.x + (r) * kLdsThreads;           \
+        const int32_t i = i0 < wt ? i0 : 0;                                    \
+        const uint4* src = i < wn ? sn : (i < wn + wv ? sv : sb);              \
+        reg = src[i];                                                          \
+    }
+#define TL_FETCH(b)                                                            \
+    {                                                                          \
+        TL_STAGE_WORDS(b)                                                      \
+        const int64_t t0 = (int64_t)(b) * tb;                                  \
+        const uint4* sn = (const uint4*)(nodes + t0 * n_leaf);                 \
+        const uint4* sv = (const uint4*)(leaves + t0 * n_leaf) - wn;           \
+        const uint4* sb = (const uint4*)(boxes + t0 * n_leaf) - (wn + wv);     \
+        TL_FETCH_WORD(0, rw0) TL_FETCH_WORD(1, rw1)                            \
+        TL_FETCH_WORD(2, rw2) TL_FETCH_WORD(3, rw3)                            \
+    }
+#define TL_STORE_WORD(r, reg)                                                  \
+    {                                                                          \
+        const int32_t i = (int32_t)threadIdx.x + (r) * kLdsThreads;            \
+        uint4* dst = i < wn ? dn : (i < wn + wv ? dv : db);                    \
+        if (i < wt) dst[i] = reg;                                              \
+    }
+#define TL_STORE(b, buf)                                                       \
+    {                                                                          \
+        TL_STAGE_WORDS(b)                                                      \
+        unsigned char* bp = smem + (buf) * L.stride;                           \
+        uint4* dn = (uint4*)(bp + L.nodes);                                    \
+        uint4* dv = (uint4*)(bp + L.vals) - wn;                                \
+        uint4* db = (uint4*)(bp + L.boxes) - (wn + wv);                        \
+        TL_STORE_WORD(0, rw0) TL_STORE_WORD(1, rw1)                            \
+        TL_STORE_WORD(2, rw2) TL_STORE_WORD(3, rw3)                            \
+    }
+
+    // Make the lane's frequency / engine size complete here, before any
+    // staging load is in flight: otherwise the walks inside the loop would
+    // each wait for all outstanding loads, including the prefetch.
+    asm volatile("" ::"v"(xf), "v"(xe));
+    if (n_blocks > 0) {
+        TL_FETCH(0)
+        TL_STORE(0, 0)
     }
     __syncthreads();
-    if (!valid) return;
+    for (int32_t b = 0; b < n_blocks; ++b) {
+        const int cur = b & 1;
+        if (b + 1 < n_blocks) TL_FETCH(b + 1)
+        if (g.valid) {
+            const int32_t cnt = min(tb, n_trees - b * tb);
+            for (int32_t tt = 0; tt < cnt; ++tt) {
+                const unsigned char* bp = smem + cur * L.stride;
+                const uint2* nt = (const uint2*)(bp + L.nodes) + tt * n_leaf;
+                const float* vt = (const float*)(bp + L.vals) + tt * n_leaf;
+                const float4* bt = (const float4*)(bp + L.boxes) + tt * n_leaf;
+                float lo_k = INFINITY, hi_k = -INFINITY, lo_b = INFINITY, hi_b = -INFINITY;
+                double val = 0.0;
+#pragma unroll
+                for (int jj = 0; jj < J; ++jj) {
+                    const float kvj = skv[jj], bsj = sbs[jj];
+                    const bool hit = (kvj >= lo_k) & (kvj < hi_k) & (bsj >= lo_b) & (bsj < hi_b);
+                    if (!hit) {
+                        int32_t k = 0;
+                        for (int32_t level = 0; level < depth; ++level) {
+                            const uint2 nd = nt[k];
+                            float x = xf;
+                            x = nd.y == 1u ? kvj : x;
+                            x = nd.y == 2u ? bsj : x;
+                            if (NF == 4) x = nd.y == 3u ? xe : x;
+                            k = 2 * k + 2 - (int32_t)(x < __uint_as_float(nd.x));
+                        }
+                        val = (double)vt[k - n_int];
+                        const float4 bx = bt[k - n_int];
+                        lo_k = bx.x;
+                        hi_k = bx.y;
+                        lo_b = bx.z;
+                        hi_b = bx.w;
+                    }
+                    acc[jj] += val;
+                }
+            }
+        }
+        if (b + 1 < n_blocks) TL_STORE(b + 1, cur ^ 1)
+        __syncthreads();
+    }
+#undef TL_STORE
+#undef TL_STORE_WORD
+#undef TL_FETCH
+#undef TL_FETCH_WORD
+#undef TL_STAGE_WORDS
+    if (active) {
+        float* o = P.out + ((int64_t)g.s * F + g.f) * H + g.j0;
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj)
+            if (jj < g.nj) o[jj] = (float)acc[jj];
+    }
+}
+
+// ------------------------------------------------------------ global memory
+
+constexpr int kGlobalWaves = 4;
+
+template <int NF, int J>
+__global__ __launch_bounds__(256) void forest_grid_global_kernel(const uint2* __restrict__ nodes,
+                                                                 const float* __restrict__ leaves,
+                                                                 const float4* __restrict__ boxes,
+                                                                 int32_t n_trees, int32_t depth, float base,
+                                                                 GridParams P) {
+    __shared__ float2 kvb[kGlobalWaves][J];
+    const int wave = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kGlobalWaves + wave);
+    const GridItem g = grid_item(P, item, J);
+    const int32_t F = P.F, H = P.H;
+    const bool active = g.valid && g.f < F;
+    const float xf = P.freqs[g.f < F ? g.f : F - 1];
+    const float xe = (NF == 4) ? P.engine[g.s] : 0.0f;
+    if (lane < J) {
+        const int32_t j = g.j0 + min(lane, g.nj - 1);
+        kvb[wave][lane] = make_float2((float)P.kv[g.s * H + j], (float)P.batch[g.s * H + j]);
+    }
+    __syncthreads();
+    if (!g.valid) return;
 
     double acc[J];
 #pragma unroll
@@ -124,8 +326,8 @@ __global__ __launch_bounds__(256) void forest_grid_kernel(const uint2* __restric
     const int32_t n_int = (1 << depth) - 1;
     const int32_t n_leaf = 1 << depth;
     for (int32_t t = 0; t < n_trees; ++t) {
-        const uint2* nt = nodes + (int64_t)t * n_int;
-        const double* lv = leaves + (int64_t)t * n_leaf;
+        const uint2* nt = nodes + (int64_t)t * n_leaf;
+        const float* lv = leaves + (int64_t)t * n_leaf;
         const float4* bx = boxes + (int64_t)t * n_leaf;
         float lo_k = INFINITY, hi_k = -INFINITY, lo_b = INFINITY, hi_b = -INFINITY;
         double val = 0.0;
@@ -137,12 +339,11 @@ __global__ __launch_bounds__(256) void forest_grid_kernel(const uint2* __restric
                 int32_t k = 0;
                 for (int32_t level = 0; level < depth; ++level) {
                     const uint2 nd = nt[k];
-                    const uint32_t ft = nd.y;
-                    const float x = ft == 0 ? xf : (ft == 1 ? v2.x : (ft == 2 ? v2.y : xe));
+                    const float x = pick_grid<NF>(nd.y, xf, v2.x, v2.y, xe);
                     k = 2 * k + ((x < __uint_as_float(nd.x)) ? 1 : 2);
                 }
                 const int32_t leaf = k - n_int;
-                val = lv[leaf];
+                val = (double)lv[leaf];
                 const float4 b = bx[leaf];
                 lo_k = b.x;
                 hi_k = b.y;
@@ -153,10 +354,10 @@ __global__ __launch_bounds__(256) void forest_grid_kernel(const uint2* __restric
         }
     }
     if (active) {
-        float* o = P.out + ((int64_t)s * F + f) * H + j0;
+        float* o = P.out + ((int64_t)g.s * F + g.f) * H + g.j0;
 #pragma unroll
         for (int jj = 0; jj < J; ++jj)
-            if (jj < nj) o[jj] = (float)acc[jj];
+            if (jj < g.nj) o[jj] = (float)acc[jj];
     }
 }
 
@@ -171,20 +372,60 @@ hipError_t launch_nf(const ForestDev& f, const float* rows, int64_t n_rows, floa
     return hipGetLastError();
 }
 
-}  // namespace
+// Trees per staged block for the LDS kernel: two blocks must fit the LDS
+// budget and one block the staging registers; the value segments of a block
+// must be whole 16-byte words.  0 = the LDS kernel cannot run.
+int32_t lds_trees_per_block(const ForestDev& f, size_t* lds_bytes) {
+    if (f.depth > kMaxLdsDepth || !f.kvb_box) return 0;
+    const int32_t n_leaf = 1 << f.depth;
+    const size_t budget = 152 * 1024;
+    auto fits = [&](int32_t tb) {
+        const StageLayout L = stage_layout(tb, n_leaf);
+        const size_t words = (size_t)tb * n_leaf * 28 / 16 + 2;
+        return 2 * (size_t)L.stride <= budget && words <= (size_t)kStageRegs * kLdsThreads;
+    };
+    const int32_t step = n_leaf >= 4 ? 1 : 4 / n_leaf;   // whole 16-byte words per block
+    int32_t tb = 64;
+    while (tb > step && !fits(tb)) tb -= step;
+    if (!fits(tb)) return 0;
+    *lds_bytes = 2 * (size_t)stage_layout(tb, n_leaf).stride;
+    return tb;
+}
 
-hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, hipStream_t stream) {
-    const int64_t n_chunks = (g.H + kGridJ - 1) / kGridJ;
+template <int NF>
+hipError_t launch_grid_lds(const ForestDev& f, const GridParams& g, int32_t tb, size_t lds, hipStream_t stream) {
+    const auto kern = forest_grid_lds_kernel<NF, kLdsJ>;
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    const int64_t n_chunks = (g.H + kLdsJ - 1) / kLdsJ;
     const int64_t n_fg = (g.F + kWave - 1) / kWave;
     const int64_t items = g.S * n_fg * n_chunks;
-    const int64_t blocks = (items + kGridWaves - 1) / kGridWaves;
-    if (f.n_features == 4)
-        hipLaunchKernelGGL((forest_grid_kernel<4, kGridJ>), dim3((unsigned)blocks), dim3(kGridWaves * kWave), 0,
-                           stream, f.nodes, f.leaves, f.kvb_box, f.n_trees, f.depth, f.base_score, g);
-    else
-        hipLaunchKernelGGL((forest_grid_kernel<3, kGridJ>), dim3((unsigned)blocks), dim3(kGridWaves * kWave), 0,
-                           stream, f.nodes, f.leaves, f.kvb_box, f.n_trees, f.depth, f.base_score, g);
+    const int64_t blocks = (items + kLdsWaves - 1) / kLdsWaves;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kLdsThreads), lds, stream, f.nodes, f.leaves,
+                       f.kvb_box, f.n_trees, f.depth, tb, f.base_score, g);
     return hipGetLastError();
+}
+
+template <int NF>
+hipError_t launch_grid_global(const ForestDev& f, const GridParams& g, hipStream_t stream) {
+    const int64_t n_chunks = (g.H + kGlobalJ - 1) / kGlobalJ;
+    const int64_t n_fg = (g.F + kWave - 1) / kWave;
+    const int64_t items = g.S * n_fg * n_chunks;
+    const int64_t blocks = (items + kGlobalWaves - 1) / kGlobalWaves;
+    hipLaunchKernelGGL((forest_grid_global_kernel<NF, kGlobalJ>), dim3((unsigned)blocks), dim3(kGlobalWaves * kWave),
+                       0, stream, f.nodes, f.leaves, f.kvb_box, f.n_trees, f.depth, f.base_score, g);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+
+hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, hipStream_t stream) {
+    size_t lds = 0;
+    const int32_t tb = lds_trees_per_block(f, &lds);
+    if (tb > 0)
+        return f.n_features == 4 ? launch_grid_lds<4>(f, g, tb, lds, stream) : launch_grid_lds<3>(f, g, tb, lds, stream);
+    return f.n_features == 4 ? launch_grid_global<4>(f, g, stream) : launch_grid_global<3>(f, g, stream);
 }
 
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,

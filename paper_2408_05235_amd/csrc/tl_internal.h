@@ -48,19 +48,19 @@ struct SelectParams {
     uint32_t* status;
 };
 
-// Device copy of a tree ensemble.
+// Device copy of a tree ensemble.  Arrays are padded by at least 64 bytes.
 struct ForestDev {
     int32_t n_trees, depth, n_features;
     float base_score;
-    const uint2* nodes;     // [T][2^d - 1]: .x = threshold bits, .y = feature
-    const double* leaves;   // [T][2^d], exact fp64 copies of the fp32 leaves
+    const uint2* nodes;     // [T][2^d]: .x = threshold bits, .y = feature (entry 2^d - 1 unused)
+    const float* leaves;    // [T][2^d]
     // Per leaf, the KV (feature 1) and batch (feature 2) constraints of its
     // root-to-leaf path as half-open intervals (kv_lo, kv_hi, batch_lo,
     // batch_hi): a row with lo <= x < hi in both features, and with the
     // frequency and engine size of a row known to reach the leaf, reaches the
-    // same leaf.  Empty (lo = +inf) for leaves no row can reach.  Only present
-    // when n_features >= 3.
-    const float4* kvb_box;  // [T][2^d] or NULL
+    // same leaf.  Empty (lo = +inf) for leaves no row can reach.  Present when
+    // n_features >= 3, else NULL.
+    const float4* kvb_box;  // [T][2^d]
 };
 
 struct GridParams {

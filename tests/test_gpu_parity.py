@@ -250,7 +250,8 @@ def random_curves(rng, S, H, kvmax=5000, bmax=300):
 
 @pytest.mark.parametrize("S,F,H,T,d,nf", [(3, 64, 1024, 40, 10, 4), (5, 17, 100, 30, 6, 3), (2, 130, 70, 20, 8, 3),
                                           (4, 48, 33, 25, 8, 3), (1, 1, 1, 3, 2, 4), (2, 64, 64, 0, 4, 3),
-                                          (3, 32, 95, 10, 0, 3)])
+                                          (3, 32, 95, 10, 0, 3), (2, 20, 40, 150, 3, 3), (3, 64, 50, 7, 12, 4),
+                                          (2, 40, 77, 5, 13, 3), (1, 64, 37, 3, 14, 4)])
 def test_forest_grid(gpu, S, F, H, T, d, nf):
     """The fused grid kernel equals the oracle on the rows it stands for."""
     import torch
