@@ -19,6 +19,7 @@ struct tl_forest {
     void* nodes_mem;
     void* leaves_mem;
     void* box_mem;
+    void* nodes4_mem;
 };
 
 namespace {
@@ -117,9 +118,21 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
         }
     for (size_t i = 0; i < cells; ++i) leaves[i] = leaf[i];
     std::vector<float4> boxes;
+    std::vector<float4> nodes4;
     if (n_features >= 3) {
         leaf_boxes(n_trees, depth, feature, threshold, boxes);
         boxes.resize(cells + 4, make_float4(0, 0, 0, 0));
+        // one threshold per feature: the tested one (NaN -> -inf, which sends
+        // every row the same way), NaN elsewhere
+        nodes4.assign(cells + 4, make_float4(NAN, NAN, NAN, NAN));
+        for (int64_t t = 0; t < n_trees; ++t)
+            for (int64_t k = 0; k < n_int; ++k) {
+                const int64_t i = t * n_int + k;
+                const float thr = std::isnan(threshold[i]) ? -INFINITY : threshold[i];
+                float v[4] = {NAN, NAN, NAN, NAN};
+                v[feature[i]] = thr;
+                nodes4[(size_t)(t * n_leaf + k)] = make_float4(v[0], v[1], v[2], v[3]);
+            }
     }
 
     tl_forest* f = new (std::nothrow) tl_forest();
@@ -131,11 +144,14 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     e = hipMalloc(&f->leaves_mem, leaves.size() * sizeof(float));
     if (e != hipSuccess) { (void)hipFree(f->nodes_mem); delete f; return from_hip(e, "tl_forest_create: hipMalloc(leaves)"); }
     f->box_mem = nullptr;
+    f->nodes4_mem = nullptr;
     if (!boxes.empty()) e = hipMalloc(&f->box_mem, boxes.size() * sizeof(float4));
+    if (e == hipSuccess && !nodes4.empty()) e = hipMalloc(&f->nodes4_mem, nodes4.size() * sizeof(float4));
     if (e != hipSuccess) {
         (void)hipFree(f->nodes_mem);
         (void)hipFree(f->leaves_mem);
         if (f->box_mem) (void)hipFree(f->box_mem);
+        if (f->nodes4_mem) (void)hipFree(f->nodes4_mem);
         delete f;
         return from_hip(e, "tl_forest_create: hipMalloc");
     }
@@ -144,10 +160,13 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
         e = hipMemcpy(f->leaves_mem, leaves.data(), leaves.size() * sizeof(float), hipMemcpyHostToDevice);
     if (e == hipSuccess && f->box_mem)
         e = hipMemcpy(f->box_mem, boxes.data(), boxes.size() * sizeof(float4), hipMemcpyHostToDevice);
+    if (e == hipSuccess && f->nodes4_mem)
+        e = hipMemcpy(f->nodes4_mem, nodes4.data(), nodes4.size() * sizeof(float4), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipFree(f->nodes_mem);
         (void)hipFree(f->leaves_mem);
         if (f->box_mem) (void)hipFree(f->box_mem);
+        if (f->nodes4_mem) (void)hipFree(f->nodes4_mem);
         delete f;
         return from_hip(e, "tl_forest_create: hipMemcpy");
     }
@@ -158,6 +177,7 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     f->dev.nodes = (const uint2*)f->nodes_mem;
     f->dev.leaves = (const float*)f->leaves_mem;
     f->dev.kvb_box = (const float4*)f->box_mem;
+    f->dev.nodes4 = (const uint4*)f->nodes4_mem;
     *out = f;
     return ok();
 }
@@ -168,6 +188,7 @@ void tl_forest_destroy(tl_forest* f) {
     (void)hipFree(f->nodes_mem);
     (void)hipFree(f->leaves_mem);
     if (f->box_mem) (void)hipFree(f->box_mem);
+    if (f->nodes4_mem) (void)hipFree(f->nodes4_mem);
     delete f;
 }
 

@@ -17,10 +17,13 @@
 // fp64 add per tree; a walk happens on roughly one row in twenty.
 //
 //   forest_grid_lds_kernel     (depth <= 11) A 1024-thread workgroup (16
-//       wavefronts, 16 x 16 x 64 rows) walks the ensemble in blocks of trees
+//       wavefronts, 16 x 32 x 64 rows) walks the ensemble in blocks of trees
 //       that are staged in LDS, double-buffered: the next block is fetched
 //       into registers while the current one is evaluated: nodes, leaf
-//       values and leaf boxes.  Tree walks read LDS only.  The wavefront's
+//       values and leaf boxes.  Tree walks read LDS only.  Nodes hold one
+//       threshold per feature (NaN for the features they do not test) so a
+//       step is four compares and no feature selection.  Trees are walked in
+//       pairs so that two chains of dependent LDS reads overlap.  The wavefront's
 //       (KV, batch) pairs are uniform and live in scalar registers.
 //   forest_grid_global_kernel  (deeper trees) The same per-lane scheme with
 //       nodes, leaves and boxes read from global memory.
@@ -28,7 +31,7 @@
 // Device layout (built by tl_forest_create): nodes [T][2^d] (8 bytes:
 // threshold bits, feature; the last entry of each tree is padding), leaves
 // [T][2^d] fp32, and for 3-4 features the leaf boxes [T][2^d] (kv_lo, kv_hi,
-// batch_lo, batch_hi).
+// batch_lo, batch_hi) and the 16-byte nodes of the LDS kernel [T][2^d].
 //
 // forest_rows_kernel evaluates arbitrary rows: each thread walks RPT
 // consecutive rows through every tree.
@@ -99,7 +102,16 @@ __global__ __launch_bounds__(256) void forest_rows_kernel(const uint2* __restric
         if (r < nr) out[r0 + r] = (float)acc[r];
 }
 
-constexpr int kLdsJ = 16;                // future iterations per wavefront (LDS kernel)
+#ifndef TL_LDS_J
+#define TL_LDS_J 32
+#endif
+#ifndef TL_LDS_WAVES
+#define TL_LDS_WAVES 16
+#endif
+#ifndef TL_LDS_BUDGET_KIB
+#define TL_LDS_BUDGET_KIB 152
+#endif
+constexpr int kLdsJ = TL_LDS_J;          // future iterations per wavefront (LDS kernel)
 constexpr int kGlobalJ = 32;             // future iterations per wavefront (global kernel)
 
 // Which (scenario, frequency group, iteration chunk) a wavefront evaluates.
@@ -126,12 +138,37 @@ __device__ __forceinline__ GridItem grid_item(const GridParams& P, int64_t item,
 
 // ---------------------------------------------------------------- LDS-staged
 
-constexpr int kLdsWaves = 16;            // wavefronts per workgroup
+// Whether (kv, batch) lies in a leaf box (kv_lo, kv_hi, batch_lo, batch_hi).
+__device__ __forceinline__ bool in_box(const float4& b, float kv, float bs) {
+    return (kv >= b.x) & (kv < b.y) & (bs >= b.z) & (bs < b.w);
+}
+
+// Lane mask of the lanes that go to 2k+1 at a node holding one threshold per
+// feature: the node's own feature carries its threshold, the others NaN,
+// which no "not >=" test (compare predicate 12: unordered or less than) can
+// fail.  The tests run as wavefront lane masks.
+template <int NF>
+__device__ __forceinline__ uint64_t go_left(const float4& nd, float xf, float kv, float bs, float xe) {
+    uint64_t m = __builtin_amdgcn_fcmpf(xf, nd.x, 12) & __builtin_amdgcn_fcmpf(kv, nd.y, 12) &
+                 __builtin_amdgcn_fcmpf(bs, nd.z, 12);
+    if (NF == 4) m &= __builtin_amdgcn_fcmpf(xe, nd.w, 12);
+    return m;
+}
+
+// 1 for lanes whose bit is set in the wavefront lane mask m (go to 2k+1),
+// 2 otherwise: one v_cndmask on the mask instead of extracting the lane's bit.
+__device__ __forceinline__ int32_t child_step(uint64_t m) {
+    int32_t step;
+    asm("v_cndmask_b32_e64 %0, 2, 1, %1" : "=v"(step) : "s"(m));
+    return step;
+}
+
+constexpr int kLdsWaves = TL_LDS_WAVES;  // wavefronts per workgroup
 constexpr int kLdsThreads = kLdsWaves * kWave;
-constexpr int kStageRegs = 4;            // staged 16-byte words per thread per block
+constexpr int kStageRegs = 4 * 16 / TL_LDS_WAVES;  // staged 16-byte words per thread per block
 constexpr int kMaxLdsDepth = 11;
 
-// Per staged tree: 2^d nodes (8 bytes, the last one padding), 2^d leaf
+// Per staged tree: 2^d nodes (16 bytes, the last one padding), 2^d leaf
 // values (4 bytes) and 2^d leaf boxes (16 bytes), each segment contiguous
 // over the trees of a block.
 struct StageLayout {
@@ -141,14 +178,14 @@ struct StageLayout {
 __host__ __device__ inline StageLayout stage_layout(int32_t tb, int32_t n_leaf) {
     StageLayout L;
     L.nodes = 0;
-    L.vals = (uint32_t)tb * n_leaf * 8u;
+    L.vals = (uint32_t)tb * n_leaf * 16u;
     L.boxes = L.vals + (((uint32_t)tb * n_leaf * 4u + 15u) & ~15u);
     L.stride = L.boxes + (uint32_t)tb * n_leaf * 16u;
     return L;
 }
 
 template <int NF, int J>
-__global__ __launch_bounds__(kLdsThreads) void forest_grid_lds_kernel(const uint2* __restrict__ nodes,
+__global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const uint4* __restrict__ nodes4,
                                                                       const float* __restrict__ leaves,
                                                                       const float4* __restrict__ boxes,
                                                                       int32_t n_trees, int32_t depth,
@@ -164,8 +201,12 @@ __global__ __launch_bounds__(kLdsThreads) void forest_grid_lds_kernel(const uint
     const GridItem g = grid_item(P, item, J);
     const int32_t F = P.F, H = P.H;
     const bool active = g.valid && g.f < F;
-    const float xf = P.freqs[g.f < F ? g.f : F - 1];
-    const float xe = (NF == 4) ? P.engine[g.s] : 0.0f;
+    // A NaN input takes every right turn at its own nodes, as +inf does; +inf
+    // also passes the "not >=" tests of the other features' NaN thresholds.
+    float xf = P.freqs[g.f < F ? g.f : F - 1];
+    float xe = (NF == 4) ? P.engine[g.s] : 0.0f;
+    xf = (xf == xf) ? xf : INFINITY;
+    xe = (xe == xe) ? xe : INFINITY;
     // the J (KV, batch) pairs of this wavefront are the same for every lane:
     // keep them in scalar registers
     float skv[J], sbs[J];
@@ -185,15 +226,16 @@ __global__ __launch_bounds__(kLdsThreads) void forest_grid_lds_kernel(const uint
     // into its own register, so the loads stay in flight while the current
     // block is evaluated.
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
-    static_assert(kStageRegs == 4, "staging code below moves four words per thread");
+    static_assert(kStageRegs == 4 || kStageRegs == 8, "staging code below moves four or eight words");
     uint4 rw0 = make_uint4(0, 0, 0, 0), rw1 = rw0, rw2 = rw0, rw3 = rw0;
+    uint4 rw4 = rw0, rw5 = rw0, rw6 = rw0, rw7 = rw0;
     double acc[J];
 #pragma unroll
     for (int jj = 0; jj < J; ++jj) acc[jj] = (double)base;
 
 #define TL_STAGE_WORDS(b)                                                      \
     const int32_t cnt_ = min(tb, n_trees - (b) * tb);                          \
-    const int32_t wn = (cnt_ * n_leaf * 8 + 15) / 16;                          \
+    const int32_t wn = cnt_ * n_leaf;                                          \
     const int32_t wv = (cnt_ * n_leaf * 4 + 15) / 16;                          \
     const int32_t wt = wn + wv + cnt_ * n_leaf;
 #define TL_FETCH_WORD(r, reg)                                                  \
@@ -209,11 +251,15 @@ __global__ __launch_bounds__(kLdsThreads) void forest_grid_lds_kernel(const uint
     {                                                                          \
         TL_STAGE_WORDS(b)                                                      \
         const int64_t t0 = (int64_t)(b) * tb;                                  \
-        const uint4* sn = (const uint4*)(nodes + t0 * n_leaf);                 \
+        const uint4* sn = nodes4 + t0 * n_leaf;                                \
         const uint4* sv = (const uint4*)(leaves + t0 * n_leaf) - wn;           \
         const uint4* sb = (const uint4*)(boxes + t0 * n_leaf) - (wn + wv);     \
         TL_FETCH_WORD(0, rw0) TL_FETCH_WORD(1, rw1)                            \
         TL_FETCH_WORD(2, rw2) TL_FETCH_WORD(3, rw3)                            \
+        if (kStageRegs == 8) {                                                 \
+            TL_FETCH_WORD(4, rw4) TL_FETCH_WORD(5, rw5)                        \
+            TL_FETCH_WORD(6, rw6) TL_FETCH_WORD(7, rw7)                        \
+        }                                                                      \
     }
 #define TL_STORE_WORD(r, reg)                                                  \
     {                                                                          \
@@ -230,6 +276,10 @@ __global__ __launch_bounds__(kLdsThreads) void forest_grid_lds_kernel(const uint
         uint4* db = (uint4*)(bp + L.boxes) - (wn + wv);                        \
         TL_STORE_WORD(0, rw0) TL_STORE_WORD(1, rw1)                            \
         TL_STORE_WORD(2, rw2) TL_STORE_WORD(3, rw3)                            \
+        if (kStageRegs == 8) {                                                 \
+            TL_STORE_WORD(4, rw4) TL_STORE_WORD(5, rw5)                        \
+            TL_STORE_WORD(6, rw6) TL_STORE_WORD(7, rw7)                        \
+        }                                                                      \
     }
 
     // Make the lane's frequency / engine size complete here, before any
@@ -246,35 +296,61 @@ __global__ __launch_bounds__(kLdsThreads) void forest_grid_lds_kernel(const uint
         if (b + 1 < n_blocks) TL_FETCH(b + 1)
         if (g.valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
-            for (int32_t tt = 0; tt < cnt; ++tt) {
-                const unsigned char* bp = smem + cur * L.stride;
-                const uint2* nt = (const uint2*)(bp + L.nodes) + tt * n_leaf;
-                const float* vt = (const float*)(bp + L.vals) + tt * n_leaf;
-                const float4* bt = (const float4*)(bp + L.boxes) + tt * n_leaf;
-                float lo_k = INFINITY, hi_k = -INFINITY, lo_b = INFINITY, hi_b = -INFINITY;
-                double val = 0.0;
+            const unsigned char* bp = smem + cur * L.stride;
+            const float4* nb = (const float4*)(bp + L.nodes);
+            const float* vb = (const float*)(bp + L.vals);
+            const float4* bb = (const float4*)(bp + L.boxes);
+            // Trees are taken two at a time: when either tree's leaf must be
+            // found again, both are walked in one pass, so the two chains of
+            // dependent LDS reads overlap.  A lane still inside its box walks
+            // back to the same leaf, so no per-tree selection is needed.
+            int32_t tt = 0;
+            for (; tt + 1 < cnt; tt += 2) {
+                const float4* na = nb + tt * n_leaf;
+                const float4* nc = na + n_leaf;
+                float4 ba = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY), bc = ba;
+                double va = 0.0, vc = 0.0;
 #pragma unroll
                 for (int jj = 0; jj < J; ++jj) {
                     const float kvj = skv[jj], bsj = sbs[jj];
-                    const bool hit = (kvj >= lo_k) & (kvj < hi_k) & (bsj >= lo_b) & (bsj < hi_b);
+                    const bool hit = in_box(ba, kvj, bsj) & in_box(bc, kvj, bsj);
                     if (!hit) {
-                        int32_t k = 0;
+                        int32_t ka = 0, kc = 0;
                         for (int32_t level = 0; level < depth; ++level) {
-                            const uint2 nd = nt[k];
-                            float x = xf;
-                            x = nd.y == 1u ? kvj : x;
-                            x = nd.y == 2u ? bsj : x;
-                            if (NF == 4) x = nd.y == 3u ? xe : x;
-                            k = 2 * k + 2 - (int32_t)(x < __uint_as_float(nd.x));
+                            const float4 da = na[ka], dc = nc[kc];
+                            ka = 2 * ka + child_step(go_left<NF>(da, xf, kvj, bsj, xe));
+                            kc = 2 * kc + child_step(go_left<NF>(dc, xf, kvj, bsj, xe));
                         }
-                        val = (double)vt[k - n_int];
-                        const float4 bx = bt[k - n_int];
-                        lo_k = bx.x;
-                        hi_k = bx.y;
-                        lo_b = bx.z;
-                        hi_b = bx.w;
+                        const int32_t la = tt * n_leaf + ka - n_int, lc = la + n_leaf + kc - ka;
+                        va = (double)vb[la];
+                        vc = (double)vb[lc];
+                        ba = bb[la];
+                        bc = bb[lc];
                     }
-                    acc[jj] += val;
+                    acc[jj] += va;
+                    acc[jj] += vc;
+                    // consume the sum here so the adds are not sunk to the end
+                    // of the loop (that would keep J leaf-value pairs live)
+                    asm volatile("" ::"v"(acc[jj]));
+                }
+            }
+            for (; tt < cnt; ++tt) {
+                const float4* na = nb + tt * n_leaf;
+                float4 ba = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
+                double va = 0.0;
+#pragma unroll
+                for (int jj = 0; jj < J; ++jj) {
+                    const float kvj = skv[jj], bsj = sbs[jj];
+                    if (!in_box(ba, kvj, bsj)) {
+                        int32_t ka = 0;
+                        for (int32_t level = 0; level < depth; ++level)
+                            ka = 2 * ka + child_step(go_left<NF>(na[ka], xf, kvj, bsj, xe));
+                        const int32_t la = tt * n_leaf + ka - n_int;
+                        va = (double)vb[la];
+                        ba = bb[la];
+                    }
+                    acc[jj] += va;
+                    asm volatile("" ::"v"(acc[jj]));
                 }
             }
         }
@@ -376,12 +452,12 @@ hipError_t launch_nf(const ForestDev& f, const float* rows, int64_t n_rows, floa
 // budget and one block the staging registers; the value segments of a block
 // must be whole 16-byte words.  0 = the LDS kernel cannot run.
 int32_t lds_trees_per_block(const ForestDev& f, size_t* lds_bytes) {
-    if (f.depth > kMaxLdsDepth || !f.kvb_box) return 0;
+    if (f.depth > kMaxLdsDepth || !f.kvb_box || !f.nodes4) return 0;
     const int32_t n_leaf = 1 << f.depth;
-    const size_t budget = 152 * 1024;
+    const size_t budget = (size_t)TL_LDS_BUDGET_KIB * 1024;
     auto fits = [&](int32_t tb) {
         const StageLayout L = stage_layout(tb, n_leaf);
-        const size_t words = (size_t)tb * n_leaf * 28 / 16 + 2;
+        const size_t words = (size_t)tb * n_leaf * 36 / 16 + 2;
         return 2 * (size_t)L.stride <= budget && words <= (size_t)kStageRegs * kLdsThreads;
     };
     const int32_t step = n_leaf >= 4 ? 1 : 4 / n_leaf;   // whole 16-byte words per block
@@ -401,7 +477,7 @@ hipError_t launch_grid_lds(const ForestDev& f, const GridParams& g, int32_t tb, 
     const int64_t n_fg = (g.F + kWave - 1) / kWave;
     const int64_t items = g.S * n_fg * n_chunks;
     const int64_t blocks = (items + kLdsWaves - 1) / kLdsWaves;
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kLdsThreads), lds, stream, f.nodes, f.leaves,
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kLdsThreads), lds, stream, f.nodes4, f.leaves,
                        f.kvb_box, f.n_trees, f.depth, tb, f.base_score, g);
     return hipGetLastError();
 }

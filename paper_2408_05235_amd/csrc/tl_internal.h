@@ -61,6 +61,11 @@ struct ForestDev {
     // same leaf.  Empty (lo = +inf) for leaves no row can reach.  Present when
     // n_features >= 3, else NULL.
     const float4* kvb_box;  // [T][2^d]
+    // Per node one threshold per feature, (f0, f1, f2, f3): the node's own
+    // feature carries its threshold, the others NaN; a NaN threshold is
+    // stored as -inf (both send every row to 2k+2).  A row goes to 2k+1 iff
+    // !(x_c >= t_c) for every feature c.  Present when n_features >= 3.
+    const uint4* nodes4;    // [T][2^d]
 };
 
 struct GridParams {
