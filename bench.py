@@ -21,9 +21,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz: one 32-bit VALU lane
-# operation per lane per clock (no packed math)
+# 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz: one non-packed VALU lane
+# operation (an fp32 compare, an fp64 add) per lane per clock
 VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+FOREST_KERNEL = "forest_grid_lds_kernel"
 METRIC = "feature rows predicted/sec + scenarios/sec end-to-end; % of HBM peak"
 
 
@@ -32,13 +33,15 @@ def log(msg):
 
 
 def algorithmic_bytes(inp, F, rows):
-    S, H, nf = inp["n_scenarios"], inp["horizon"], inp["n_features"]
+    """Bytes each stage must move at least (inputs read once, outputs written
+    once) for one step of the fused pipeline (rows are never materialized)."""
+    S, H = inp["n_scenarios"], inp["horizon"]
     R = int(inp["req_offset"][-1])
     f = inp["forest"]
-    n_int = (1 << f["depth"]) - 1
-    forest_bytes = f["n_trees"] * (n_int * 8 + (n_int + 1) * 8)
-    k1 = R * 25 + S * 16 + S * H * 16 + S * 8 + rows * nf * 4
-    k2 = rows * nf * 4 + rows * 4 + forest_bytes
+    n_leaf = 1 << f["depth"]
+    forest_bytes = f["n_trees"] * n_leaf * (16 + 4 + 16)   # device nodes, leaves, boxes
+    k1 = R * 25 + S * 8 + S * 8 + S * H * 16 + S * 8        # requests; offsets, caps; curves; scalars
+    k2 = S * H * 8 + F * 4 + S * 4 + forest_bytes + rows * 4
     k3 = rows * 4 + S * H * 8 + S * 28
     return dict(project=k1, predict=k2, select=k3)
 
@@ -140,7 +143,10 @@ def main():
     tot_bytes = sum(byt.values())
 
     f = inp["forest"]
-    ops_per_row = f["n_trees"] * (f["depth"] + 1)
+    # algorithmic work of the forest stage: every (row, tree) pair needs at
+    # least its leaf accumulated (one fp64 add); walks that leaf reuse avoids
+    # are not counted, so this is the floor any implementation must execute
+    ops_per_row = f["n_trees"]
     forest_s = stage_ms[1] / 1e3
     achieved = ops_per_row * rows / forest_s / 1e12
     traffic = traffic_record(cfg["name"])
@@ -167,10 +173,11 @@ def main():
         "stage_hbm_gbs": {k: byt[k] / (v / 1e3) / 1e9 for k, v in
                           zip(("project", "predict", "select"), stage_ms)},
         "forest_rows_per_s": rows / forest_s,
-        "roofline": {"kernel": "forest_rows_kernel", "bound": "alu", "achieved": achieved,
+        "forest_node_visits_per_s_equiv": rows * f["n_trees"] * f["depth"] / forest_s,
+        "roofline": {"kernel": FOREST_KERNEL, "bound": "alu", "achieved": achieved,
                      "peak": VALU_PEAK_TOPS, "unit": "Tops/s", "frac": achieved / VALU_PEAK_TOPS,
-                     "traffic": traffic,
-                     "ops_per_row": ops_per_row, "ops_note": "trees x (depth compares + 1 leaf add)"},
+                     "traffic": traffic, "ops_per_row": ops_per_row,
+                     "ops_note": "one fp64 leaf add per (row, tree); peak = non-packed VALU lane ops"},
     }
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4
