@@ -1,0 +1,79 @@
+"""Summarize rocprofv3 CSV output into the short text files kept in profiles/.
+
+    python -m paper_2408_05235_amd.prof_summary stats  <kernel_stats.csv> <out.md> <command>
+    python -m paper_2408_05235_amd.prof_summary traffic <fetch_counter_collection.csv> \
+        <write_counter_collection.csv> <kernel substring> <copy bytes> <out.json> <command>
+
+`traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of one kernel into
+bytes per launch, each scaled by what the same counter reads for the last
+copy dispatch of the run, a copy of known size (the counters' byte formulas
+need not match the request sizes a kernel uses).
+"""
+from __future__ import annotations
+
+import csv
+import hashlib
+import json
+import os
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+
+
+def _short(name):
+    return name.replace("tl::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+
+
+def kernel_stats(csv_path, out_md, command, title=""):
+    rows = list(csv.DictReader(open(csv_path)))
+    lines = [f"# {title or 'rocprofv3 kernel statistics'}", "", "Command:", "", "```", command, "```", "",
+             "| kernel | calls | average ms | min ms | max ms | share |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e6:.3f} | "
+                     f"{float(r['MinNs']) / 1e6:.3f} | {float(r['MaxNs']) / 1e6:.3f} | "
+                     f"{float(r['Percentage']):.2f}% |")
+    open(out_md, "w").write("\n".join(lines) + "\n")
+    return rows
+
+
+def _per_dispatch(csv_path, counter):
+    out = []
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] == counter:
+            out.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+    agg = {}
+    for d, k, v in out:
+        agg.setdefault(d, [k, 0.0])[1] += v
+    return [(d, k, v) for d, (k, v) in sorted(agg.items())]
+
+
+def traffic(fetch_csv, write_csv, kernel, copy_bytes, out_json, command):
+    res = {}
+    for name, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
+        disp = _per_dispatch(path, counter)
+        copies = [v for d, k, v in disp if "copyBuffer" in k]
+        if not copies:
+            raise SystemExit(f"no copy dispatch in {path}")
+        scale = copy_bytes / (copies[-1] * 1024.0)
+        vals = [v for d, k, v in disp if kernel in k]
+        if not vals:
+            raise SystemExit(f"no dispatch of {kernel} in {path}")
+        res[name] = dict(kib_per_launch=sum(vals) / len(vals), copy_kib=copies[-1], scale=scale,
+                         bytes_per_launch=sum(vals) / len(vals) * 1024.0 * scale)
+    src = open(os.path.join(PKG, "csrc", "forest.hip"), "rb").read()
+    rec = dict(kernel=kernel, command=command, copy_bytes=copy_bytes,
+               fetch=res["fetch"], write=res["write"],
+               bytes_per_launch=res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"],
+               forest_hip_sha256=hashlib.sha256(src).hexdigest())
+    json.dump(rec, open(out_json, "w"), indent=1)
+    return rec
+
+
+if __name__ == "__main__":
+    if sys.argv[1] == "stats":
+        kernel_stats(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5] if len(sys.argv) > 5 else "")
+    elif sys.argv[1] == "traffic":
+        print(json.dumps(traffic(sys.argv[2], sys.argv[3], sys.argv[4], int(sys.argv[5]), sys.argv[6],
+                                 sys.argv[7]), indent=1))
+    else:
+        raise SystemExit(__doc__)
