@@ -19,7 +19,7 @@ struct tl_forest {
     void* nodes_mem;
     void* leaves_mem;
     void* box_mem;
-    void* nodes4_mem;
+    void* records_mem;
 };
 
 namespace {
@@ -118,21 +118,31 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
         }
     for (size_t i = 0; i < cells; ++i) leaves[i] = leaf[i];
     std::vector<float4> boxes;
-    std::vector<float4> nodes4;
+    std::vector<unsigned char> records;
     if (n_features >= 3) {
         leaf_boxes(n_trees, depth, feature, threshold, boxes);
-        boxes.resize(cells + 4, make_float4(0, 0, 0, 0));
-        // one threshold per feature: the tested one (NaN -> -inf, which sends
-        // every row the same way), NaN elsewhere
-        nodes4.assign(cells + 4, make_float4(NAN, NAN, NAN, NAN));
-        for (int64_t t = 0; t < n_trees; ++t)
-            for (int64_t k = 0; k < n_int; ++k) {
-                const int64_t i = t * n_int + k;
-                const float thr = std::isnan(threshold[i]) ? -INFINITY : threshold[i];
-                float v[4] = {NAN, NAN, NAN, NAN};
-                v[feature[i]] = thr;
-                nodes4[(size_t)(t * n_leaf + k)] = make_float4(v[0], v[1], v[2], v[3]);
+        if (depth <= tl::kMaxRecordDepth) {
+            // per tree: nodes with one threshold per feature (the tested one,
+            // NaN -> -inf, which sends every row the same way; NaN elsewhere),
+            // leaf values, leaf boxes
+            const tl::RecordLayout R = tl::record_layout(depth);
+            records.assign((size_t)n_trees * R.bytes + 64, 0);
+            for (int64_t t = 0; t < n_trees; ++t) {
+                unsigned char* rec = records.data() + (size_t)t * R.bytes;
+                float4* nd = (float4*)rec;
+                for (int64_t k = 0; k < n_leaf; ++k) {
+                    float v[4] = {NAN, NAN, NAN, NAN};
+                    if (k < n_int) {
+                        const int64_t i = t * n_int + k;
+                        v[feature[i]] = std::isnan(threshold[i]) ? -INFINITY : threshold[i];
+                    }
+                    nd[k] = make_float4(v[0], v[1], v[2], v[3]);
+                }
+                std::memcpy(rec + R.vals, leaf + t * n_leaf, (size_t)n_leaf * 4);
+                std::memcpy(rec + R.boxes, boxes.data() + t * n_leaf, (size_t)n_leaf * 16);
             }
+        }
+        boxes.resize(cells + 4, make_float4(0, 0, 0, 0));
     }
 
     tl_forest* f = new (std::nothrow) tl_forest();
@@ -144,14 +154,14 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     e = hipMalloc(&f->leaves_mem, leaves.size() * sizeof(float));
     if (e != hipSuccess) { (void)hipFree(f->nodes_mem); delete f; return from_hip(e, "tl_forest_create: hipMalloc(leaves)"); }
     f->box_mem = nullptr;
-    f->nodes4_mem = nullptr;
+    f->records_mem = nullptr;
     if (!boxes.empty()) e = hipMalloc(&f->box_mem, boxes.size() * sizeof(float4));
-    if (e == hipSuccess && !nodes4.empty()) e = hipMalloc(&f->nodes4_mem, nodes4.size() * sizeof(float4));
+    if (e == hipSuccess && !records.empty()) e = hipMalloc(&f->records_mem, records.size());
     if (e != hipSuccess) {
         (void)hipFree(f->nodes_mem);
         (void)hipFree(f->leaves_mem);
         if (f->box_mem) (void)hipFree(f->box_mem);
-        if (f->nodes4_mem) (void)hipFree(f->nodes4_mem);
+        if (f->records_mem) (void)hipFree(f->records_mem);
         delete f;
         return from_hip(e, "tl_forest_create: hipMalloc");
     }
@@ -160,13 +170,13 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
         e = hipMemcpy(f->leaves_mem, leaves.data(), leaves.size() * sizeof(float), hipMemcpyHostToDevice);
     if (e == hipSuccess && f->box_mem)
         e = hipMemcpy(f->box_mem, boxes.data(), boxes.size() * sizeof(float4), hipMemcpyHostToDevice);
-    if (e == hipSuccess && f->nodes4_mem)
-        e = hipMemcpy(f->nodes4_mem, nodes4.data(), nodes4.size() * sizeof(float4), hipMemcpyHostToDevice);
+    if (e == hipSuccess && f->records_mem)
+        e = hipMemcpy(f->records_mem, records.data(), records.size(), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipFree(f->nodes_mem);
         (void)hipFree(f->leaves_mem);
         if (f->box_mem) (void)hipFree(f->box_mem);
-        if (f->nodes4_mem) (void)hipFree(f->nodes4_mem);
+        if (f->records_mem) (void)hipFree(f->records_mem);
         delete f;
         return from_hip(e, "tl_forest_create: hipMemcpy");
     }
@@ -177,7 +187,7 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     f->dev.nodes = (const uint2*)f->nodes_mem;
     f->dev.leaves = (const float*)f->leaves_mem;
     f->dev.kvb_box = (const float4*)f->box_mem;
-    f->dev.nodes4 = (const uint4*)f->nodes4_mem;
+    f->dev.records = (const uint4*)f->records_mem;
     *out = f;
     return ok();
 }
@@ -188,7 +198,7 @@ void tl_forest_destroy(tl_forest* f) {
     (void)hipFree(f->nodes_mem);
     (void)hipFree(f->leaves_mem);
     if (f->box_mem) (void)hipFree(f->box_mem);
-    if (f->nodes4_mem) (void)hipFree(f->nodes4_mem);
+    if (f->records_mem) (void)hipFree(f->records_mem);
     delete f;
 }
 

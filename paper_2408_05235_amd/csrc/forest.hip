@@ -19,19 +19,21 @@
 //   forest_grid_lds_kernel     (depth <= 11) A 1024-thread workgroup (16
 //       wavefronts, 16 x 32 x 64 rows) walks the ensemble in blocks of trees
 //       that are staged in LDS, double-buffered: the next block is fetched
-//       into registers while the current one is evaluated: nodes, leaf
-//       values and leaf boxes.  Tree walks read LDS only.  Nodes hold one
-//       threshold per feature (NaN for the features they do not test) so a
-//       step is four compares and no feature selection.  Trees are walked in
-//       pairs so that two chains of dependent LDS reads overlap.  The wavefront's
-//       (KV, batch) pairs are uniform and live in scalar registers.
+//       into registers while the current one is evaluated.  A tree is one
+//       record (nodes, leaf values, leaf boxes), so a block is one contiguous
+//       copy.  Tree walks read LDS only.  Nodes hold one threshold per
+//       feature (NaN for the features they do not test) so a step is four
+//       compares and no feature selection.  Trees are taken in pairs that
+//       share one box test and one walk pass, and rows in groups of eight
+//       whose (KV, batch) hull is tested before any single row.
 //   forest_grid_global_kernel  (deeper trees) The same per-lane scheme with
-//       nodes, leaves and boxes read from global memory.
+//       nodes, leaves and boxes read from global memory, one row at a time.
 //
 // Device layout (built by tl_forest_create): nodes [T][2^d] (8 bytes:
 // threshold bits, feature; the last entry of each tree is padding), leaves
 // [T][2^d] fp32, and for 3-4 features the leaf boxes [T][2^d] (kv_lo, kv_hi,
-// batch_lo, batch_hi) and the 16-byte nodes of the LDS kernel [T][2^d].
+// batch_lo, batch_hi) and, up to depth 11, the tree records of the LDS
+// kernel.
 //
 // forest_rows_kernel evaluates arbitrary rows: each thread walks RPT
 // consecutive rows through every tree.
@@ -165,35 +167,106 @@ __device__ __forceinline__ int32_t child_step(uint64_t m) {
 
 constexpr int kLdsWaves = TL_LDS_WAVES;  // wavefronts per workgroup
 constexpr int kLdsThreads = kLdsWaves * kWave;
-constexpr int kStageRegs = 4 * 16 / TL_LDS_WAVES;  // staged 16-byte words per thread per block
-constexpr int kMaxLdsDepth = 11;
+#ifndef TL_STAGE_REGS
+#define TL_STAGE_REGS (8 * 16 / TL_LDS_WAVES)
+#endif
+constexpr int kStageRegs = TL_STAGE_REGS;  // staged 16-byte words per thread per block
 
-// Per staged tree: 2^d nodes (16 bytes, the last one padding), 2^d leaf
-// values (4 bytes) and 2^d leaf boxes (16 bytes), each segment contiguous
-// over the trees of a block.
-struct StageLayout {
-    uint32_t nodes, vals, boxes, stride;   // byte offsets inside a buffer, buffer size
-};
+// A wavefront-uniform value pinned in a scalar register (the compiler would
+// otherwise rematerialize it in vector registers).
+__device__ __forceinline__ float to_sgpr(float x) {
+    float r;
+    asm volatile("v_readfirstlane_b32 %0, %1" : "=s"(r) : "v"(x));
+    return r;
+}
 
-__host__ __device__ inline StageLayout stage_layout(int32_t tb, int32_t n_leaf) {
-    StageLayout L;
-    L.nodes = 0;
-    L.vals = (uint32_t)tb * n_leaf * 16u;
-    L.boxes = L.vals + (((uint32_t)tb * n_leaf * 4u + 15u) & ~15u);
-    L.stride = L.boxes + (uint32_t)tb * n_leaf * 16u;
-    return L;
+constexpr int kRowGroup = 8;   // rows whose (KV, batch) hull is tested as one
+
+// Adds the leaves of NT consecutive staged trees (records of R.bytes bytes,
+// the first at `tree`) to the J row sums of a wavefront, in tree order.
+// hull[g] = (min KV, max KV, min batch, max batch) over rows g*8 .. g*8+7;
+// kv4 holds the rows' (KV, batch) pairs, two per 16 bytes.  A lane keeps the
+// leaves its last walk reached and the intersection of their boxes.  A group
+// whose hull lies inside that box on every lane needs only its adds; other
+// groups test row by row and walk the trees again for lanes whose row left
+// the box.
+template <int NF, int J, int NT>
+__device__ __forceinline__ void eval_trees(const unsigned char* tree, const RecordLayout& R, int32_t n_leaf,
+                                           int32_t depth, const float4* kv4,
+                                           const float (&hull)[J / kRowGroup][4], float xf, float xe,
+                                           double (&acc)[J]) {
+    static_assert(J % kRowGroup == 0, "whole row groups");
+    // the pairs are re-read from LDS for each group that needs them rather
+    // than held in registers across the tree loop
+    asm volatile("" ::: "memory");
+    const int32_t n_int = n_leaf - 1;
+    float4 box = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);   // empty: first row walks
+    double v[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) v[t] = 0.0;
+#pragma unroll
+    for (int gi = 0; gi < J / kRowGroup; ++gi) {
+        const uint64_t inside = __builtin_amdgcn_fcmpf(hull[gi][0], box.x, 3) &   // min KV >= kv_lo
+                                __builtin_amdgcn_fcmpf(hull[gi][1], box.y, 4) &   // max KV < kv_hi
+                                __builtin_amdgcn_fcmpf(hull[gi][2], box.z, 3) &
+                                __builtin_amdgcn_fcmpf(hull[gi][3], box.w, 4);
+        const bool test_rows = inside != __builtin_amdgcn_read_exec();   // wavefront-uniform
+        float4 q = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+        for (int i = 0; i < kRowGroup; ++i) {
+            if (test_rows) {
+                if ((i & 1) == 0) {
+                    // two rows per read; the barrier keeps the compiler from
+                    // hoisting all reads of the group (registers)
+                    asm volatile("" ::: "memory");
+                    q = kv4[gi * (kRowGroup / 2) + i / 2];
+                }
+                const float kv = (i & 1) ? q.z : q.x;
+                const float bs = (i & 1) ? q.w : q.y;
+                if (!in_box(box, kv, bs)) {
+                    int32_t k[NT];
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) k[t] = 0;
+                    for (int32_t level = 0; level < depth; ++level) {
+#pragma unroll
+                        for (int t = 0; t < NT; ++t) {
+                            const float4 nd = ((const float4*)(tree + t * R.bytes))[k[t]];
+                            k[t] = 2 * k[t] + child_step(go_left<NF>(nd, xf, kv, bs, xe));
+                        }
+                    }
+                    box = make_float4(-INFINITY, INFINITY, -INFINITY, INFINITY);
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+                        const int32_t l = k[t] - n_int;
+                        const unsigned char* rec = tree + t * R.bytes;
+                        v[t] = (double)((const float*)(rec + R.vals))[l];
+                        const float4 lb = ((const float4*)(rec + R.boxes))[l];
+                        box.x = lb.x > box.x ? lb.x : box.x;
+                        box.y = lb.y < box.y ? lb.y : box.y;
+                        box.z = lb.z > box.z ? lb.z : box.z;
+                        box.w = lb.w < box.w ? lb.w : box.w;
+                    }
+                }
+            }
+            double& a = acc[gi * kRowGroup + i];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) a += v[t];
+            // consume the sum here so the adds are not sunk past later walks
+            // (that would keep leaf values live)
+            asm volatile("" ::"v"(a));
+        }
+    }
 }
 
 template <int NF, int J>
-__global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const uint4* __restrict__ nodes4,
-                                                                      const float* __restrict__ leaves,
-                                                                      const float4* __restrict__ boxes,
+__global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const uint4* __restrict__ records,
                                                                       int32_t n_trees, int32_t depth,
                                                                       int32_t tb, float base, GridParams P) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const int32_t n_int = (1 << depth) - 1;
     const int32_t n_leaf = 1 << depth;
-    const StageLayout L = stage_layout(tb, n_leaf);
+    const RecordLayout R = record_layout(depth);
+    const uint32_t rec_words = R.bytes / 16u;
+    const uint32_t buf_bytes = (uint32_t)tb * R.bytes;
 
     const int wave = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -207,24 +280,18 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
     float xe = (NF == 4) ? P.engine[g.s] : 0.0f;
     xf = (xf == xf) ? xf : INFINITY;
     xe = (xe == xe) ? xe : INFINITY;
-    // the J (KV, batch) pairs of this wavefront are the same for every lane:
-    // keep them in scalar registers
-    float skv[J], sbs[J];
-    {
-        const int32_t j = g.j0 + min(lane % J, g.nj - 1);
-        const float kvl = (float)P.kv[g.s * H + j], bsl = (float)P.batch[g.s * H + j];
-#pragma unroll
-        for (int jj = 0; jj < J; ++jj) {
-            skv[jj] = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(kvl), jj));
-            sbs[jj] = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(bsl), jj));
-        }
+    // the J (KV, batch) pairs of this wavefront are the same for every lane;
+    // they sit in LDS after the two tree buffers and are read as broadcasts
+    float2* kvb = (float2*)(smem + 2 * buf_bytes) + wave * J;
+    if (lane < J) {
+        const int32_t j = g.j0 + min(lane, g.nj - 1);
+        kvb[lane] = make_float2((float)P.kv[g.s * H + j], (float)P.batch[g.s * H + j]);
     }
 
-    // staging: block b holds trees [b*tb, b*tb + cnt), copied as 16-byte words
-    // from the three global arrays (the host pads them so whole words exist).
-    // Each thread moves up to kStageRegs words: one load per word straight
-    // into its own register, so the loads stay in flight while the current
-    // block is evaluated.
+    // staging: block b is trees [b*tb, b*tb + cnt), one contiguous range of
+    // 16-byte words in global memory and in LDS.  Each thread moves up to
+    // kStageRegs words: one load per word straight into its own register, so
+    // the loads stay in flight while the current block is evaluated.
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
     static_assert(kStageRegs == 4 || kStageRegs == 8, "staging code below moves four or eight words");
     uint4 rw0 = make_uint4(0, 0, 0, 0), rw1 = rw0, rw2 = rw0, rw3 = rw0;
@@ -233,27 +300,18 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
 #pragma unroll
     for (int jj = 0; jj < J; ++jj) acc[jj] = (double)base;
 
-#define TL_STAGE_WORDS(b)                                                      \
-    const int32_t cnt_ = min(tb, n_trees - (b) * tb);                          \
-    const int32_t wn = cnt_ * n_leaf;                                          \
-    const int32_t wv = (cnt_ * n_leaf * 4 + 15) / 16;                          \
-    const int32_t wt = wn + wv + cnt_ * n_leaf;
+#define TL_BLOCK_WORDS(b) ((uint32_t)min(tb, n_trees - (b) * tb) * rec_words)
 #define TL_FETCH_WORD(r, reg)                                                  \
     {                                                                          \
         /* unconditional (threads past the block re-read word 0), so the   */ \
-        /* four loads issue back to back without waits between them        */ \
-        const int32_t i0 = (int32_t)threadIdx.x + (r) * kLdsThreads;           \
-        const int32_t i = i0 < wt ? i0 : 0;                                    \
-        const uint4* src = i < wn ? sn : (i < wn + wv ? sv : sb);              \
-        reg = src[i];                                                          \
+        /* loads issue back to back without waits between them             */ \
+        const uint32_t i0 = threadIdx.x + (r) * kLdsThreads;                   \
+        reg = src[i0 < wt ? i0 : 0];                                           \
     }
 #define TL_FETCH(b)                                                            \
     {                                                                          \
-        TL_STAGE_WORDS(b)                                                      \
-        const int64_t t0 = (int64_t)(b) * tb;                                  \
-        const uint4* sn = nodes4 + t0 * n_leaf;                                \
-        const uint4* sv = (const uint4*)(leaves + t0 * n_leaf) - wn;           \
-        const uint4* sb = (const uint4*)(boxes + t0 * n_leaf) - (wn + wv);     \
+        const uint32_t wt = TL_BLOCK_WORDS(b);                                 \
+        const uint4* src = records + (int64_t)(b) * tb * rec_words;            \
         TL_FETCH_WORD(0, rw0) TL_FETCH_WORD(1, rw1)                            \
         TL_FETCH_WORD(2, rw2) TL_FETCH_WORD(3, rw3)                            \
         if (kStageRegs == 8) {                                                 \
@@ -263,17 +321,13 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
     }
 #define TL_STORE_WORD(r, reg)                                                  \
     {                                                                          \
-        const int32_t i = (int32_t)threadIdx.x + (r) * kLdsThreads;            \
-        uint4* dst = i < wn ? dn : (i < wn + wv ? dv : db);                    \
+        const uint32_t i = threadIdx.x + (r) * kLdsThreads;                    \
         if (i < wt) dst[i] = reg;                                              \
     }
 #define TL_STORE(b, buf)                                                       \
     {                                                                          \
-        TL_STAGE_WORDS(b)                                                      \
-        unsigned char* bp = smem + (buf) * L.stride;                           \
-        uint4* dn = (uint4*)(bp + L.nodes);                                    \
-        uint4* dv = (uint4*)(bp + L.vals) - wn;                                \
-        uint4* db = (uint4*)(bp + L.boxes) - (wn + wv);                        \
+        const uint32_t wt = TL_BLOCK_WORDS(b);                                 \
+        uint4* dst = (uint4*)(smem + (buf) * buf_bytes);                       \
         TL_STORE_WORD(0, rw0) TL_STORE_WORD(1, rw1)                            \
         TL_STORE_WORD(2, rw2) TL_STORE_WORD(3, rw3)                            \
         if (kStageRegs == 8) {                                                 \
@@ -291,68 +345,39 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
         TL_STORE(0, 0)
     }
     __syncthreads();
+    // per row group, the (KV, batch) hull of its rows (wavefront-uniform)
+    const float4* kvb4 = (const float4*)kvb;
+    float hull[J / kRowGroup][4];
+#pragma unroll
+    for (int gi = 0; gi < J / kRowGroup; ++gi) {
+        float klo = INFINITY, khi = -INFINITY, blo = INFINITY, bhi = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < kRowGroup; ++i) {
+            const float2 p = kvb[gi * kRowGroup + i];
+            klo = fminf(klo, p.x);
+            khi = fmaxf(khi, p.x);
+            blo = fminf(blo, p.y);
+            bhi = fmaxf(bhi, p.y);
+        }
+        hull[gi][0] = to_sgpr(klo);
+        hull[gi][1] = to_sgpr(khi);
+        hull[gi][2] = to_sgpr(blo);
+        hull[gi][3] = to_sgpr(bhi);
+    }
     for (int32_t b = 0; b < n_blocks; ++b) {
         const int cur = b & 1;
         if (b + 1 < n_blocks) TL_FETCH(b + 1)
         if (g.valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
-            const unsigned char* bp = smem + cur * L.stride;
-            const float4* nb = (const float4*)(bp + L.nodes);
-            const float* vb = (const float*)(bp + L.vals);
-            const float4* bb = (const float4*)(bp + L.boxes);
-            // Trees are taken two at a time: when either tree's leaf must be
-            // found again, both are walked in one pass, so the two chains of
-            // dependent LDS reads overlap.  A lane still inside its box walks
-            // back to the same leaf, so no per-tree selection is needed.
+            const unsigned char* bp = smem + cur * buf_bytes;
+            // Trees are taken two at a time and a lane keeps the intersection
+            // of the two leaf boxes: a row inside it reaches both leaves
+            // again.  When a row leaves it, both trees are walked in one pass,
+            // so the two chains of dependent LDS reads overlap.
             int32_t tt = 0;
-            for (; tt + 1 < cnt; tt += 2) {
-                const float4* na = nb + tt * n_leaf;
-                const float4* nc = na + n_leaf;
-                float4 ba = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY), bc = ba;
-                double va = 0.0, vc = 0.0;
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj) {
-                    const float kvj = skv[jj], bsj = sbs[jj];
-                    const bool hit = in_box(ba, kvj, bsj) & in_box(bc, kvj, bsj);
-                    if (!hit) {
-                        int32_t ka = 0, kc = 0;
-                        for (int32_t level = 0; level < depth; ++level) {
-                            const float4 da = na[ka], dc = nc[kc];
-                            ka = 2 * ka + child_step(go_left<NF>(da, xf, kvj, bsj, xe));
-                            kc = 2 * kc + child_step(go_left<NF>(dc, xf, kvj, bsj, xe));
-                        }
-                        const int32_t la = tt * n_leaf + ka - n_int, lc = la + n_leaf + kc - ka;
-                        va = (double)vb[la];
-                        vc = (double)vb[lc];
-                        ba = bb[la];
-                        bc = bb[lc];
-                    }
-                    acc[jj] += va;
-                    acc[jj] += vc;
-                    // consume the sum here so the adds are not sunk to the end
-                    // of the loop (that would keep J leaf-value pairs live)
-                    asm volatile("" ::"v"(acc[jj]));
-                }
-            }
-            for (; tt < cnt; ++tt) {
-                const float4* na = nb + tt * n_leaf;
-                float4 ba = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
-                double va = 0.0;
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj) {
-                    const float kvj = skv[jj], bsj = sbs[jj];
-                    if (!in_box(ba, kvj, bsj)) {
-                        int32_t ka = 0;
-                        for (int32_t level = 0; level < depth; ++level)
-                            ka = 2 * ka + child_step(go_left<NF>(na[ka], xf, kvj, bsj, xe));
-                        const int32_t la = tt * n_leaf + ka - n_int;
-                        va = (double)vb[la];
-                        ba = bb[la];
-                    }
-                    acc[jj] += va;
-                    asm volatile("" ::"v"(acc[jj]));
-                }
-            }
+            for (; tt + 1 < cnt; tt += 2)
+                eval_trees<NF, J, 2>(bp + tt * R.bytes, R, n_leaf, depth, kvb4, hull, xf, xe, acc);
+            if (tt < cnt) eval_trees<NF, J, 1>(bp + tt * R.bytes, R, n_leaf, depth, kvb4, hull, xf, xe, acc);
         }
         if (b + 1 < n_blocks) TL_STORE(b + 1, cur ^ 1)
         __syncthreads();
@@ -361,7 +386,7 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
 #undef TL_STORE_WORD
 #undef TL_FETCH
 #undef TL_FETCH_WORD
-#undef TL_STAGE_WORDS
+#undef TL_BLOCK_WORDS
     if (active) {
         float* o = P.out + ((int64_t)g.s * F + g.f) * H + g.j0;
 #pragma unroll
@@ -448,23 +473,21 @@ hipError_t launch_nf(const ForestDev& f, const float* rows, int64_t n_rows, floa
     return hipGetLastError();
 }
 
-// Trees per staged block for the LDS kernel: two blocks must fit the LDS
-// budget and one block the staging registers; the value segments of a block
-// must be whole 16-byte words.  0 = the LDS kernel cannot run.
+// Trees per staged block for the LDS kernel: two blocks and the wavefronts'
+// (KV, batch) pairs must fit the LDS budget, and one block the staging
+// registers.  0 = the LDS kernel cannot run.
 int32_t lds_trees_per_block(const ForestDev& f, size_t* lds_bytes) {
-    if (f.depth > kMaxLdsDepth || !f.kvb_box || !f.nodes4) return 0;
-    const int32_t n_leaf = 1 << f.depth;
+    if (!f.records || f.depth > kMaxRecordDepth) return 0;
+    const size_t rec = record_layout(f.depth).bytes;
+    const size_t head = (size_t)kLdsWaves * kLdsJ * sizeof(float2);
     const size_t budget = (size_t)TL_LDS_BUDGET_KIB * 1024;
     auto fits = [&](int32_t tb) {
-        const StageLayout L = stage_layout(tb, n_leaf);
-        const size_t words = (size_t)tb * n_leaf * 36 / 16 + 2;
-        return 2 * (size_t)L.stride <= budget && words <= (size_t)kStageRegs * kLdsThreads;
+        return 2 * (size_t)tb * rec + head <= budget && (size_t)tb * rec / 16 <= (size_t)kStageRegs * kLdsThreads;
     };
-    const int32_t step = n_leaf >= 4 ? 1 : 4 / n_leaf;   // whole 16-byte words per block
     int32_t tb = 64;
-    while (tb > step && !fits(tb)) tb -= step;
+    while (tb > 1 && !fits(tb)) --tb;
     if (!fits(tb)) return 0;
-    *lds_bytes = 2 * (size_t)stage_layout(tb, n_leaf).stride;
+    *lds_bytes = 2 * (size_t)tb * rec + head;
     return tb;
 }
 
@@ -477,8 +500,8 @@ hipError_t launch_grid_lds(const ForestDev& f, const GridParams& g, int32_t tb, 
     const int64_t n_fg = (g.F + kWave - 1) / kWave;
     const int64_t items = g.S * n_fg * n_chunks;
     const int64_t blocks = (items + kLdsWaves - 1) / kLdsWaves;
-    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kLdsThreads), lds, stream, f.nodes4, f.leaves,
-                       f.kvb_box, f.n_trees, f.depth, tb, f.base_score, g);
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kLdsThreads), lds, stream, f.records, f.n_trees,
+                       f.depth, tb, f.base_score, g);
     return hipGetLastError();
 }
 

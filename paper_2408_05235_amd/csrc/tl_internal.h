@@ -61,12 +61,36 @@ struct ForestDev {
     // same leaf.  Empty (lo = +inf) for leaves no row can reach.  Present when
     // n_features >= 3, else NULL.
     const float4* kvb_box;  // [T][2^d]
-    // Per node one threshold per feature, (f0, f1, f2, f3): the node's own
-    // feature carries its threshold, the others NaN; a NaN threshold is
-    // stored as -inf (both send every row to 2k+2).  A row goes to 2k+1 iff
-    // !(x_c >= t_c) for every feature c.  Present when n_features >= 3.
-    const uint4* nodes4;    // [T][2^d]
+    // Tree records of the LDS-staged grid kernel, one per tree, back to back
+    // (layout: record_layout).  Present when n_features >= 3 and the depth
+    // is at most kMaxRecordDepth, else NULL.
+    const uint4* records;
 };
+
+constexpr int kMaxRecordDepth = 11;
+
+// One tree as the LDS-staged grid kernel reads it (byte ranges, each
+// starting on a 16-byte boundary):
+//   [0, vals)       nodes: one threshold per feature (f0, f1, f2, f3); the
+//                   node's own feature carries its threshold, the others
+//                   NaN; a NaN threshold is stored as -inf (both send every
+//                   row to 2k+2).  A row goes to 2k+1 iff !(x_c >= t_c) for
+//                   every feature c.  2^d entries, the last one padding.
+//   [vals, boxes)   leaf values, fp32, 2^d entries (padded to whole words)
+//   [boxes, bytes)  leaf boxes as in kvb_box, 2^d entries
+// A block of consecutive trees is one contiguous byte range, staged as is.
+struct RecordLayout {
+    uint32_t vals, boxes, bytes;
+};
+
+__host__ __device__ inline RecordLayout record_layout(int32_t depth) {
+    const uint32_t n_leaf = 1u << depth;
+    RecordLayout r;
+    r.vals = 16u * n_leaf;
+    r.boxes = r.vals + ((4u * n_leaf + 15u) & ~15u);
+    r.bytes = r.boxes + 16u * n_leaf;
+    return r;
+}
 
 struct GridParams {
     int64_t S;
