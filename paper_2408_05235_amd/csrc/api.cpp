@@ -122,21 +122,21 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     if (n_features >= 3) {
         leaf_boxes(n_trees, depth, feature, threshold, boxes);
         if (depth <= tl::kMaxRecordDepth) {
-            // per tree: nodes with one threshold per feature (the tested one,
-            // NaN -> -inf, which sends every row the same way; NaN elsewhere),
-            // leaf values, leaf boxes
+            // per tree: nodes (threshold, then byte-permute selectors that
+            // pick the tested feature: sel1 frequency / KV, sel2 batch /
+            // engine size, sel3 between the two), leaf values, leaf boxes
+            constexpr uint32_t kLow = 0x03020100u, kHigh = 0x07060504u;
             const tl::RecordLayout R = tl::record_layout(depth);
             records.assign((size_t)n_trees * R.bytes + 64, 0);
             for (int64_t t = 0; t < n_trees; ++t) {
                 unsigned char* rec = records.data() + (size_t)t * R.bytes;
-                float4* nd = (float4*)rec;
-                for (int64_t k = 0; k < n_leaf; ++k) {
-                    float v[4] = {NAN, NAN, NAN, NAN};
-                    if (k < n_int) {
-                        const int64_t i = t * n_int + k;
-                        v[feature[i]] = std::isnan(threshold[i]) ? -INFINITY : threshold[i];
-                    }
-                    nd[k] = make_float4(v[0], v[1], v[2], v[3]);
+                uint4* nd = (uint4*)rec;
+                for (int64_t k = 0; k < n_int; ++k) {
+                    const int64_t i = t * n_int + k;
+                    const int fi = feature[i];
+                    uint32_t bits;
+                    std::memcpy(&bits, &threshold[i], 4);
+                    nd[k] = make_uint4(bits, fi == 1 ? kHigh : kLow, fi == 3 ? kHigh : kLow, fi >= 2 ? kHigh : kLow);
                 }
                 std::memcpy(rec + R.vals, leaf + t * n_leaf, (size_t)n_leaf * 4);
                 std::memcpy(rec + R.boxes, boxes.data() + t * n_leaf, (size_t)n_leaf * 16);

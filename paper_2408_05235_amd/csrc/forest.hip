@@ -21,9 +21,9 @@
 //       that are staged in LDS, double-buffered: the next block is fetched
 //       into registers while the current one is evaluated.  A tree is one
 //       record (nodes, leaf values, leaf boxes), so a block is one contiguous
-//       copy.  Tree walks read LDS only.  Nodes hold one threshold per
-//       feature (NaN for the features they do not test) so a step is four
-//       compares and no feature selection.  Trees are taken in pairs that
+//       copy.  Tree walks read LDS only.  A node step picks the tested
+//       feature with byte permutes and compares once, all in vector
+//       registers (no lane-mask round trip).  Trees are taken in pairs that
 //       share one box test and one walk pass, and rows in groups of eight
 //       whose (KV, batch) hull is tested before any single row.
 //   forest_grid_global_kernel  (deeper trees) The same per-lane scheme with
@@ -145,24 +145,16 @@ __device__ __forceinline__ bool in_box(const float4& b, float kv, float bs) {
     return (kv >= b.x) & (kv < b.y) & (bs >= b.z) & (bs < b.w);
 }
 
-// Lane mask of the lanes that go to 2k+1 at a node holding one threshold per
-// feature: the node's own feature carries its threshold, the others NaN,
-// which no "not >=" test (compare predicate 12: unordered or less than) can
-// fail.  The tests run as wavefront lane masks.
+// The value of the feature a record node tests, picked with byte permutes:
+// node = (threshold, sel1, sel2, sel3); sel1 picks frequency or KV, sel2
+// batch or engine size, sel3 between the two picks (v_perm_b32: selector
+// 0x03020100 keeps the second operand, 0x07060504 takes the first).
 template <int NF>
-__device__ __forceinline__ uint64_t go_left(const float4& nd, float xf, float kv, float bs, float xe) {
-    uint64_t m = __builtin_amdgcn_fcmpf(xf, nd.x, 12) & __builtin_amdgcn_fcmpf(kv, nd.y, 12) &
-                 __builtin_amdgcn_fcmpf(bs, nd.z, 12);
-    if (NF == 4) m &= __builtin_amdgcn_fcmpf(xe, nd.w, 12);
-    return m;
-}
-
-// 1 for lanes whose bit is set in the wavefront lane mask m (go to 2k+1),
-// 2 otherwise: one v_cndmask on the mask instead of extracting the lane's bit.
-__device__ __forceinline__ int32_t child_step(uint64_t m) {
-    int32_t step;
-    asm("v_cndmask_b32_e64 %0, 2, 1, %1" : "=v"(step) : "s"(m));
-    return step;
+__device__ __forceinline__ float node_feature(const uint4& nd, float xf, float kv, float bs, float xe) {
+    const uint32_t x01 = __builtin_amdgcn_perm(__float_as_uint(kv), __float_as_uint(xf), nd.y);
+    const uint32_t x23 = NF == 4 ? __builtin_amdgcn_perm(__float_as_uint(xe), __float_as_uint(bs), nd.z)
+                                 : __float_as_uint(bs);
+    return __uint_as_float(__builtin_amdgcn_perm(x23, x01, nd.w));
 }
 
 constexpr int kLdsWaves = TL_LDS_WAVES;  // wavefronts per workgroup
@@ -230,8 +222,9 @@ __device__ __forceinline__ void eval_trees(const unsigned char* tree, const Reco
                     for (int32_t level = 0; level < depth; ++level) {
 #pragma unroll
                         for (int t = 0; t < NT; ++t) {
-                            const float4 nd = ((const float4*)(tree + t * R.bytes))[k[t]];
-                            k[t] = 2 * k[t] + child_step(go_left<NF>(nd, xf, kv, bs, xe));
+                            const uint4 nd = ((const uint4*)(tree + t * R.bytes))[k[t]];
+                            const bool left = node_feature<NF>(nd, xf, kv, bs, xe) < __uint_as_float(nd.x);
+                            k[t] = 2 * k[t] + (left ? 1 : 2);
                         }
                     }
                     box = make_float4(-INFINITY, INFINITY, -INFINITY, INFINITY);
@@ -274,12 +267,10 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
     const GridItem g = grid_item(P, item, J);
     const int32_t F = P.F, H = P.H;
     const bool active = g.valid && g.f < F;
-    // A NaN input takes every right turn at its own nodes, as +inf does; +inf
-    // also passes the "not >=" tests of the other features' NaN thresholds.
-    float xf = P.freqs[g.f < F ? g.f : F - 1];
-    float xe = (NF == 4) ? P.engine[g.s] : 0.0f;
-    xf = (xf == xf) ? xf : INFINITY;
-    xe = (xe == xe) ? xe : INFINITY;
+    // (a NaN frequency or engine size fails every "x < threshold" test and
+    // takes every right turn, as in a plain walk)
+    const float xf = P.freqs[g.f < F ? g.f : F - 1];
+    const float xe = (NF == 4) ? P.engine[g.s] : 0.0f;
     // the J (KV, batch) pairs of this wavefront are the same for every lane;
     // they sit in LDS after the two tree buffers and are read as broadcasts
     float2* kvb = (float2*)(smem + 2 * buf_bytes) + wave * J;

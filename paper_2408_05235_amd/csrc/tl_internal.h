@@ -71,11 +71,10 @@ constexpr int kMaxRecordDepth = 11;
 
 // One tree as the LDS-staged grid kernel reads it (byte ranges, each
 // starting on a 16-byte boundary):
-//   [0, vals)       nodes: one threshold per feature (f0, f1, f2, f3); the
-//                   node's own feature carries its threshold, the others
-//                   NaN; a NaN threshold is stored as -inf (both send every
-//                   row to 2k+2).  A row goes to 2k+1 iff !(x_c >= t_c) for
-//                   every feature c.  2^d entries, the last one padding.
+//   [0, vals)       nodes (threshold, sel1, sel2, sel3): byte-permute
+//                   selectors that pick the tested feature c out of
+//                   (frequency, KV, batch, engine size); a row goes to 2k+1
+//                   iff x_c < threshold.  2^d entries, the last one padding.
 //   [vals, boxes)   leaf values, fp32, 2^d entries (padded to whole words)
 //   [boxes, bytes)  leaf boxes as in kvb_box, 2^d entries
 // A block of consecutive trees is one contiguous byte range, staged as is.
