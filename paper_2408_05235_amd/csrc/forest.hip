@@ -160,7 +160,7 @@ __device__ __forceinline__ float node_feature(const uint4& nd, float xf, float k
 constexpr int kLdsWaves = TL_LDS_WAVES;  // wavefronts per workgroup
 constexpr int kLdsThreads = kLdsWaves * kWave;
 #ifndef TL_STAGE_REGS
-#define TL_STAGE_REGS (8 * 16 / TL_LDS_WAVES)
+#define TL_STAGE_REGS (6 * 16 / TL_LDS_WAVES)
 #endif
 constexpr int kStageRegs = TL_STAGE_REGS;  // staged 16-byte words per thread per block
 
@@ -174,28 +174,61 @@ __device__ __forceinline__ float to_sgpr(float x) {
 
 constexpr int kRowGroup = 8;   // rows whose (KV, batch) hull is tested as one
 
-// Adds the leaves of NT consecutive staged trees (records of R.bytes bytes,
-// the first at `tree`) to the J row sums of a wavefront, in tree order.
-// hull[g] = (min KV, max KV, min batch, max batch) over rows g*8 .. g*8+7;
-// kv4 holds the rows' (KV, batch) pairs, two per 16 bytes.  A lane keeps the
-// leaves its last walk reached and the intersection of their boxes.  A group
-// whose hull lies inside that box on every lane needs only its adds; other
-// groups test row by row and walk the trees again for lanes whose row left
-// the box.
+// Walks NT consecutive staged trees (records R.bytes apart, the first at
+// `tree`) from the root for one row; k[t] = leaf index of tree t.  The walks
+// of two trees interleave, so their chains of dependent LDS reads overlap.
+template <int NF, int NT>
+__device__ __forceinline__ void walk(const unsigned char* tree, uint32_t rec_bytes, int32_t depth, float xf,
+                                     float kv, float bs, float xe, int32_t (&k)[NT]) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) k[t] = 0;
+    for (int32_t level = 0; level < depth; ++level) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const uint4 nd = ((const uint4*)(tree + t * rec_bytes))[k[t]];
+            const bool left = node_feature<NF>(nd, xf, kv, bs, xe) < __uint_as_float(nd.x);
+            k[t] = 2 * k[t] + (left ? 1 : 2);
+        }
+    }
+    const int32_t n_int = (1 << depth) - 1;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) k[t] -= n_int;
+}
+
+__device__ __forceinline__ float4 box_meet(const float4& a, const float4& b) {
+    return make_float4(a.x > b.x ? a.x : b.x, a.y < b.y ? a.y : b.y, a.z > b.z ? a.z : b.z, a.w < b.w ? a.w : b.w);
+}
+
+// Adds the leaves of NT (1 or 2) consecutive staged trees (records R.bytes
+// apart, the first at `tree`) to the J row sums of a wavefront, in tree
+// order.  hull[g] = (min KV, max KV, min batch, max batch) over rows
+// g*8 .. g*8+7; kv4 holds the rows' (KV, batch) pairs, two per 16 bytes.
+// A lane keeps the leaves its walks reached and the intersection of their
+// boxes.  A group whose hull lies inside that box on every lane needs only
+// its adds; other groups test row by row.  A lane whose row leaves the
+// intersection re-reads both leaf boxes and walks only the trees whose own
+// box it left (both in one pass when the wavefront needs both).
 template <int NF, int J, int NT>
-__device__ __forceinline__ void eval_trees(const unsigned char* tree, const RecordLayout& R, int32_t n_leaf,
-                                           int32_t depth, const float4* kv4,
-                                           const float (&hull)[J / kRowGroup][4], float xf, float xe,
-                                           double (&acc)[J]) {
+__device__ __forceinline__ void eval_trees(const unsigned char* tree, const RecordLayout& R, int32_t depth,
+                                           const float4* kv4, const float (&hull)[J / kRowGroup][4], float xf,
+                                           float xe, double (&acc)[J]) {
     static_assert(J % kRowGroup == 0, "whole row groups");
+    static_assert(NT == 1 || NT == 2, "one tree or a pair");
     // the pairs are re-read from LDS for each group that needs them rather
     // than held in registers across the tree loop
     asm volatile("" ::: "memory");
-    const int32_t n_int = n_leaf - 1;
+    const float* vals0 = (const float*)(tree + R.vals);
+    const float4* boxes0 = (const float4*)(tree + R.boxes);
+    const float* vals1 = (const float*)(tree + R.bytes + R.vals);
+    const float4* boxes1 = (const float4*)(tree + R.bytes + R.boxes);
     float4 box = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);   // empty: first row walks
+    int32_t leaf[NT];
     double v[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) v[t] = 0.0;
+    for (int t = 0; t < NT; ++t) {
+        leaf[t] = 0;
+        v[t] = 0.0;
+    }
 #pragma unroll
     for (int gi = 0; gi < J / kRowGroup; ++gi) {
         const uint64_t inside = __builtin_amdgcn_fcmpf(hull[gi][0], box.x, 3) &   // min KV >= kv_lo
@@ -216,28 +249,41 @@ __device__ __forceinline__ void eval_trees(const unsigned char* tree, const Reco
                 const float kv = (i & 1) ? q.z : q.x;
                 const float bs = (i & 1) ? q.w : q.y;
                 if (!in_box(box, kv, bs)) {
-                    int32_t k[NT];
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) k[t] = 0;
-                    for (int32_t level = 0; level < depth; ++level) {
-#pragma unroll
-                        for (int t = 0; t < NT; ++t) {
-                            const uint4 nd = ((const uint4*)(tree + t * R.bytes))[k[t]];
-                            const bool left = node_feature<NF>(nd, xf, kv, bs, xe) < __uint_as_float(nd.x);
-                            k[t] = 2 * k[t] + (left ? 1 : 2);
+                    if (NT == 1) {
+                        int32_t k[1];
+                        walk<NF, 1>(tree, R.bytes, depth, xf, kv, bs, xe, k);
+                        leaf[0] = k[0];
+                    } else if (gi == 0 && i == 0) {
+                        int32_t k[2];       // first row: both trees, every lane
+                        walk<NF, 2>(tree, R.bytes, depth, xf, kv, bs, xe, k);
+                        leaf[0] = k[0];
+                        leaf[NT - 1] = k[1];
+                    } else {
+                        const bool n0 = !in_box(boxes0[leaf[0]], kv, bs);
+                        const bool n1 = !in_box(boxes1[leaf[NT - 1]], kv, bs);
+                        if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
+                            int32_t k[2];
+                            walk<NF, 2>(tree, R.bytes, depth, xf, kv, bs, xe, k);
+                            leaf[0] = k[0];
+                            leaf[NT - 1] = k[1];
+                        } else {
+                            if (n0) {
+                                int32_t k[1];
+                                walk<NF, 1>(tree, R.bytes, depth, xf, kv, bs, xe, k);
+                                leaf[0] = k[0];
+                            }
+                            if (n1) {
+                                int32_t k[1];
+                                walk<NF, 1>(tree + R.bytes, R.bytes, depth, xf, kv, bs, xe, k);
+                                leaf[NT - 1] = k[0];
+                            }
                         }
                     }
-                    box = make_float4(-INFINITY, INFINITY, -INFINITY, INFINITY);
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) {
-                        const int32_t l = k[t] - n_int;
-                        const unsigned char* rec = tree + t * R.bytes;
-                        v[t] = (double)((const float*)(rec + R.vals))[l];
-                        const float4 lb = ((const float4*)(rec + R.boxes))[l];
-                        box.x = lb.x > box.x ? lb.x : box.x;
-                        box.y = lb.y < box.y ? lb.y : box.y;
-                        box.z = lb.z > box.z ? lb.z : box.z;
-                        box.w = lb.w < box.w ? lb.w : box.w;
+                    v[0] = (double)vals0[leaf[0]];
+                    box = boxes0[leaf[0]];
+                    if (NT == 2) {
+                        v[NT - 1] = (double)vals1[leaf[NT - 1]];
+                        box = box_meet(box, boxes1[leaf[NT - 1]]);
                     }
                 }
             }
@@ -284,7 +330,7 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
     // kStageRegs words: one load per word straight into its own register, so
     // the loads stay in flight while the current block is evaluated.
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
-    static_assert(kStageRegs == 4 || kStageRegs == 8, "staging code below moves four or eight words");
+    static_assert(kStageRegs >= 1 && kStageRegs <= 8, "staging code below moves up to eight words");
     uint4 rw0 = make_uint4(0, 0, 0, 0), rw1 = rw0, rw2 = rw0, rw3 = rw0;
     uint4 rw4 = rw0, rw5 = rw0, rw6 = rw0, rw7 = rw0;
     double acc[J];
@@ -293,7 +339,7 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
 
 #define TL_BLOCK_WORDS(b) ((uint32_t)min(tb, n_trees - (b) * tb) * rec_words)
 #define TL_FETCH_WORD(r, reg)                                                  \
-    {                                                                          \
+    if ((r) < kStageRegs) {                                                    \
         /* unconditional (threads past the block re-read word 0), so the   */ \
         /* loads issue back to back without waits between them             */ \
         const uint32_t i0 = threadIdx.x + (r) * kLdsThreads;                   \
@@ -305,13 +351,11 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
         const uint4* src = records + (int64_t)(b) * tb * rec_words;            \
         TL_FETCH_WORD(0, rw0) TL_FETCH_WORD(1, rw1)                            \
         TL_FETCH_WORD(2, rw2) TL_FETCH_WORD(3, rw3)                            \
-        if (kStageRegs == 8) {                                                 \
-            TL_FETCH_WORD(4, rw4) TL_FETCH_WORD(5, rw5)                        \
-            TL_FETCH_WORD(6, rw6) TL_FETCH_WORD(7, rw7)                        \
-        }                                                                      \
+        TL_FETCH_WORD(4, rw4) TL_FETCH_WORD(5, rw5)                            \
+        TL_FETCH_WORD(6, rw6) TL_FETCH_WORD(7, rw7)                            \
     }
 #define TL_STORE_WORD(r, reg)                                                  \
-    {                                                                          \
+    if ((r) < kStageRegs) {                                                    \
         const uint32_t i = threadIdx.x + (r) * kLdsThreads;                    \
         if (i < wt) dst[i] = reg;                                              \
     }
@@ -321,10 +365,8 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
         uint4* dst = (uint4*)(smem + (buf) * buf_bytes);                       \
         TL_STORE_WORD(0, rw0) TL_STORE_WORD(1, rw1)                            \
         TL_STORE_WORD(2, rw2) TL_STORE_WORD(3, rw3)                            \
-        if (kStageRegs == 8) {                                                 \
-            TL_STORE_WORD(4, rw4) TL_STORE_WORD(5, rw5)                        \
-            TL_STORE_WORD(6, rw6) TL_STORE_WORD(7, rw7)                        \
-        }                                                                      \
+        TL_STORE_WORD(4, rw4) TL_STORE_WORD(5, rw5)                            \
+        TL_STORE_WORD(6, rw6) TL_STORE_WORD(7, rw7)                            \
     }
 
     // Make the lane's frequency / engine size complete here, before any
@@ -367,8 +409,8 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
             // so the two chains of dependent LDS reads overlap.
             int32_t tt = 0;
             for (; tt + 1 < cnt; tt += 2)
-                eval_trees<NF, J, 2>(bp + tt * R.bytes, R, n_leaf, depth, kvb4, hull, xf, xe, acc);
-            if (tt < cnt) eval_trees<NF, J, 1>(bp + tt * R.bytes, R, n_leaf, depth, kvb4, hull, xf, xe, acc);
+                eval_trees<NF, J, 2>(bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
+            if (tt < cnt) eval_trees<NF, J, 1>(bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
         }
         if (b + 1 < n_blocks) TL_STORE(b + 1, cur ^ 1)
         __syncthreads();
