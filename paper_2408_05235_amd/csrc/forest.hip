@@ -174,25 +174,45 @@ __device__ __forceinline__ float to_sgpr(float x) {
 
 constexpr int kRowGroup = 8;   // rows whose (KV, batch) hull is tested as one
 
-// Walks NT consecutive staged trees (records R.bytes apart, the first at
-// `tree`) from the root for one row; k[t] = leaf index of tree t.  The walks
-// of two trees interleave, so their chains of dependent LDS reads overlap.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
+
+// LDS byte address of a location in the kernel's dynamic LDS.
+__device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const unsigned char*)p;
+}
+
+// Walks NT consecutive staged trees (records rec_bytes apart, the first at
+// LDS byte address `tree`) from the root for one row; k[t] = leaf index of
+// tree t.  The walks of two trees interleave, so their chains of dependent
+// LDS reads overlap.
 template <int NF, int NT>
-__device__ __forceinline__ void walk(const unsigned char* tree, uint32_t rec_bytes, int32_t depth, float xf,
-                                     float kv, float bs, float xe, int32_t (&k)[NT]) {
+__device__ __forceinline__ void walk(uint32_t tree, uint32_t rec_bytes, int32_t depth, float xf, float kv, float bs,
+                                     float xe, int32_t (&k)[NT]) {
+    // the loop carries node byte addresses: child 2k+1 of the node at
+    // a = root + 16 k sits at 2 a + (16 - root), child 2k+2 16 bytes later
+    uint32_t a[NT], cl[NT], cr[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) k[t] = 0;
+    for (int t = 0; t < NT; ++t) {
+        a[t] = tree + t * rec_bytes;
+        cl[t] = 16u - a[t];
+        cr[t] = 32u - a[t];
+        // opaque to the optimizer, which would otherwise rewrite the select
+        // of the two offsets as an add after the compare
+        asm volatile("" : "+v"(cl[t]), "+v"(cr[t]));
+    }
     for (int32_t level = 0; level < depth; ++level) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            const uint4 nd = ((const uint4*)(tree + t * rec_bytes))[k[t]];
+            const u32x4 w = *(lds_u32x4*)(uintptr_t)a[t];
+            const uint4 nd = make_uint4(w.x, w.y, w.z, w.w);
             const bool left = node_feature<NF>(nd, xf, kv, bs, xe) < __uint_as_float(nd.x);
-            k[t] = 2 * k[t] + (left ? 1 : 2);
+            a[t] = 2u * a[t] + (left ? cl[t] : cr[t]);
         }
     }
     const int32_t n_int = (1 << depth) - 1;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) k[t] -= n_int;
+    for (int t = 0; t < NT; ++t) k[t] = (int32_t)((a[t] - (tree + t * rec_bytes)) >> 4) - n_int;
 }
 
 __device__ __forceinline__ float4 box_meet(const float4& a, const float4& b) {
@@ -209,7 +229,8 @@ __device__ __forceinline__ float4 box_meet(const float4& a, const float4& b) {
 // intersection re-reads both leaf boxes and walks only the trees whose own
 // box it left (both in one pass when the wavefront needs both).
 template <int NF, int J, int NT>
-__device__ __forceinline__ void eval_trees(const unsigned char* tree, const RecordLayout& R, int32_t depth,
+__device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tree_off, const RecordLayout& R,
+                                           int32_t depth,
                                            const float4* kv4, const float (&hull)[J / kRowGroup][4], float xf,
                                            float xe, double (&acc)[J]) {
     static_assert(J % kRowGroup == 0, "whole row groups");
@@ -217,6 +238,8 @@ __device__ __forceinline__ void eval_trees(const unsigned char* tree, const Reco
     // the pairs are re-read from LDS for each group that needs them rather
     // than held in registers across the tree loop
     asm volatile("" ::: "memory");
+    const unsigned char* tree = lds + tree_off;
+    const uint32_t tree_addr = lds_addr(tree);
     const float* vals0 = (const float*)(tree + R.vals);
     const float4* boxes0 = (const float4*)(tree + R.boxes);
     const float* vals1 = (const float*)(tree + R.bytes + R.vals);
@@ -251,11 +274,11 @@ __device__ __forceinline__ void eval_trees(const unsigned char* tree, const Reco
                 if (!in_box(box, kv, bs)) {
                     if (NT == 1) {
                         int32_t k[1];
-                        walk<NF, 1>(tree, R.bytes, depth, xf, kv, bs, xe, k);
+                        walk<NF, 1>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
                         leaf[0] = k[0];
                     } else if (gi == 0 && i == 0) {
                         int32_t k[2];       // first row: both trees, every lane
-                        walk<NF, 2>(tree, R.bytes, depth, xf, kv, bs, xe, k);
+                        walk<NF, 2>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
                         leaf[0] = k[0];
                         leaf[NT - 1] = k[1];
                     } else {
@@ -263,18 +286,18 @@ __device__ __forceinline__ void eval_trees(const unsigned char* tree, const Reco
                         const bool n1 = !in_box(boxes1[leaf[NT - 1]], kv, bs);
                         if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
                             int32_t k[2];
-                            walk<NF, 2>(tree, R.bytes, depth, xf, kv, bs, xe, k);
+                            walk<NF, 2>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
                             leaf[0] = k[0];
                             leaf[NT - 1] = k[1];
                         } else {
                             if (n0) {
                                 int32_t k[1];
-                                walk<NF, 1>(tree, R.bytes, depth, xf, kv, bs, xe, k);
+                                walk<NF, 1>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
                                 leaf[0] = k[0];
                             }
                             if (n1) {
                                 int32_t k[1];
-                                walk<NF, 1>(tree + R.bytes, R.bytes, depth, xf, kv, bs, xe, k);
+                                walk<NF, 1>(tree_addr + R.bytes, R.bytes, depth, xf, kv, bs, xe, k);
                                 leaf[NT - 1] = k[0];
                             }
                         }
@@ -402,15 +425,15 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
         if (b + 1 < n_blocks) TL_FETCH(b + 1)
         if (g.valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
-            const unsigned char* bp = smem + cur * buf_bytes;
+            const uint32_t bp = cur * buf_bytes;
             // Trees are taken two at a time and a lane keeps the intersection
             // of the two leaf boxes: a row inside it reaches both leaves
             // again.  When a row leaves it, both trees are walked in one pass,
             // so the two chains of dependent LDS reads overlap.
             int32_t tt = 0;
             for (; tt + 1 < cnt; tt += 2)
-                eval_trees<NF, J, 2>(bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
-            if (tt < cnt) eval_trees<NF, J, 1>(bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
+                eval_trees<NF, J, 2>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
+            if (tt < cnt) eval_trees<NF, J, 1>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
         }
         if (b + 1 < n_blocks) TL_STORE(b + 1, cur ^ 1)
         __syncthreads();
