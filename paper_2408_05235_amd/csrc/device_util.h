@@ -66,28 +66,31 @@ __device__ __forceinline__ int32_t wave_incl_max(int32_t v) {
     return v;
 }
 
+// Butterfly reductions: every lane ends with the same value, which is
+// returned through a lane read so the compiler treats it as wave-uniform.
 __device__ __forceinline__ int32_t wave_max(int32_t v) {
 #pragma unroll
     for (int d = kWave / 2; d >= 1; d >>= 1) v = max(v, __shfl_xor(v, d));
-    return v;
+    return __builtin_amdgcn_readfirstlane(v);
 }
 
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 #pragma unroll
     for (int d = kWave / 2; d >= 1; d >>= 1) v += __shfl_xor(v, d);
-    return v;
+    return ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int32_t)(v >> 32)) << 32) |
+           (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)(uint32_t)v);
 }
 
 __device__ __forceinline__ int32_t wave_sum(int32_t v) {
 #pragma unroll
     for (int d = kWave / 2; d >= 1; d >>= 1) v += __shfl_xor(v, d);
-    return v;
+    return __builtin_amdgcn_readfirstlane(v);
 }
 
 __device__ __forceinline__ uint32_t wave_or(uint32_t v) {
 #pragma unroll
     for (int d = kWave / 2; d >= 1; d >>= 1) v |= __shfl_xor(v, d);
-    return v;
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)v);
 }
 
 }  // namespace tl

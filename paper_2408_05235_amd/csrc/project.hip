@@ -191,30 +191,21 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     const int32_t bcap = has_bcap ? P.batch_cap[s] : 0;
     if (last_over >= 0 || (has_bcap && n_in > bcap)) fl |= TL_FLAG_OVERCOMMIT;
 
-    // FIFO admission of queued requests
+    // FIFO admission of queued requests.  One wave does it; every value the
+    // loop carries (iteration j, batch count, the head's fields, check
+    // outcomes) is wave-uniform and kept in scalar registers.  LDS accesses
+    // of one wave are processed in order, so lane 0's updates of DA are seen
+    // by the later reads of every lane.
     int32_t* DA = CD;   // admitted-batch difference array
     if (has_queue) {
         for (int32_t t = lane; t < H; t += kWave) DA[t] = 0;
         __syncthreads();
-        int32_t j = 0, run = 0;
-        int64_t cb = lo;
+        int32_t j = 0;
+        int32_t run = 0;    // admitted requests active at j (kept only under a batch cap)
+        int64_t cb = lo - kWave;
         int32_t q_arr = 0, q_c = 0, q_len = 0, q_lost = 0;
         uint64_t q_dl = kNoDeadline;
         uint64_t mask = 0;
-        {
-            const int64_t i = cb + lane;
-            bool q = false;
-            if (i < hi) {
-                q_arr = P.arr[i];
-                const int32_t p = P.prompt[i], g = P.gen[i];
-                q_len = P.rem[i];
-                q = entry_ok(p, g, q_len, q_arr) && q_arr >= 0;
-                q_c = p + g;
-                q_lost = P.lost ? P.lost[i] : 0;
-                q_dl = P.deadline ? P.deadline[i] : kNoDeadline;
-            }
-            mask = __ballot(q);
-        }
         for (;;) {
             while (mask == 0) {
                 cb += kWave;
@@ -233,21 +224,24 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 mask = __ballot(q);
             }
             if (mask == 0) break;
+            // the head of the queue (uniform lane: lane reads, no LDS shuffle)
             const int hl = __ffsll((unsigned long long)mask) - 1;
-            const int32_t h_arr = __shfl(q_arr, hl);
-            const int32_t h_c = __shfl(q_c, hl);
-            const int32_t h_len = __shfl(q_len, hl);
-            const int32_t h_lost = __shfl(q_lost, hl);
-            const uint64_t h_dl = __shfl(q_dl, hl);
-            int32_t target = max(max(h_arr, j), last_over + 1);
+            const int32_t h_arr = __builtin_amdgcn_readlane(q_arr, hl);
+            const int32_t h_c = __builtin_amdgcn_readlane(q_c, hl);
+            const int32_t h_len = __builtin_amdgcn_readlane(q_len, hl);
+            const int32_t h_lost = __builtin_amdgcn_readlane(q_lost, hl);
+            const uint64_t h_dl =
+                ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int32_t)(q_dl >> 32), hl) << 32) |
+                (uint32_t)__builtin_amdgcn_readlane((int32_t)(uint32_t)q_dl, hl);
+            const int32_t target = max(max(h_arr, j), last_over + 1);
             if (h_arr >= H || target >= H) break;
-            if (target > j) {
-                run += sum_range(DA, j, target);
-                j = target;
-            }
+            if (has_bcap && target > j) run += sum_range(DA, j, target);
+            j = target;
             bool admitted = false;
             for (;;) {
-                bool ok = !has_bcap || (BI[j] + run < bcap);
+                bool ok = true;
+                if (has_bcap) ok = __builtin_amdgcn_readfirstlane(BI[j] + run) < bcap;
+                int32_t t_bad = -1;
                 if (ok) {
                     const int32_t lim = (int32_t)min((int64_t)j + h_len, (int64_t)H);
                     for (int32_t t0 = j; t0 < lim; t0 += kWave) {
@@ -255,13 +249,31 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                         bool badt = false;
                         if (t < lim)
                             badt = KV[t] + (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN) > cap;
-                        if (__ballot(badt)) { ok = false; break; }
+                        const uint64_t m = __ballot(badt);
+                        if (m) {
+                            t_bad = t0 + __ffsll((unsigned long long)m) - 1;
+                            break;
+                        }
                     }
+                    ok = t_bad < 0;
                 }
                 if (ok) { admitted = true; break; }
-                if (j + 1 >= H) break;
-                run += DA[j + 1];
-                ++j;
+                // Next start to try.  If iteration t_bad overflowed, every
+                // start j2 in (j, t_bad] whose own contribution there,
+                // ceil((c + t_bad - j2) / N), exceeds room = cap - KV[t_bad]
+                // fails the same way: j2 < c + t_bad - N * room (all of
+                // them when room < 0).  Skipping those gives the same
+                // admission iteration.
+                int32_t nj = j + 1;
+                if (t_bad >= 0) {
+                    const int32_t room = cap - __builtin_amdgcn_readfirstlane(KV[t_bad]);
+                    int64_t first = (int64_t)t_bad + 1;
+                    if (room >= 0) first = min(first, (int64_t)h_c + t_bad - (int64_t)N * room);
+                    nj = (int32_t)max((int64_t)nj, first);
+                }
+                if (nj >= H) break;
+                if (has_bcap) run += sum_range(DA, j, nj);
+                j = nj;
             }
             if (!admitted) break;
             const int64_t e = (int64_t)j + h_len;
@@ -276,7 +288,6 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 if (e <= H && !h_lost && h_dl != kNoDeadline)
                     atomicMin((unsigned long long*)&outDL[e - 1], (unsigned long long)h_dl);
             }
-            __syncthreads();
             run += 1;
             n_end = max(n_end, lim);
             mask &= mask - 1;
