@@ -172,7 +172,7 @@ __device__ __forceinline__ float to_sgpr(float x) {
     return r;
 }
 
-constexpr int kRowGroup = 8;   // rows whose (KV, batch) hull is tested as one
+constexpr int kRowGroup = 4;   // rows whose (KV, batch) hull is tested as one
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
