@@ -13,12 +13,15 @@
 // where comb_diff gets +1 at j0 and -1 at the first comb point >= e.  The
 // batch curve is the prefix sum of +1 at 0 / -1 at e.
 //
-// Queued requests are admitted iteration by iteration in FIFO order by the
-// same wave: the head's KV contribution over its in-horizon lifetime is
-// checked against the capacity with all 64 lanes, then added into the LDS
-// KV curve.  Admissions only happen after the last iteration at which the
-// in-flight batch alone exceeds the capacity, which makes the lifetime check
-// equal to checking the whole projected vector from the current iteration on.
+// Queued requests are admitted in FIFO order by the same wave, each at the
+// first iteration from its arrival (and from the previous admission) where
+// its KV contribution over its in-horizon lifetime fits under the capacity.
+// Admissions only happen after the last iteration at which the in-flight
+// batch alone exceeds the capacity, which makes the lifetime check equal to
+// checking the whole projected vector from the current iteration on.
+// Without a batch cap, up to 64 requests are tried at once at their FIFO
+// targets with one check of their summed contribution; when that fails the
+// batch shrinks, down to one request at a time.
 #include "device_util.h"
 #include "tl_internal.h"
 
@@ -33,7 +36,7 @@ __device__ __forceinline__ bool entry_ok(int32_t p, int32_t g, int32_t r, int32_
 
 // sum of DA[t] for t in (j, j2], j2 < H; every lane returns the same value
 __device__ __forceinline__ int32_t sum_range(const int32_t* DA, int32_t j, int32_t j2) {
-    if (j2 == j + 1) return DA[j2];
+    if (j2 == j + 1) return __builtin_amdgcn_readfirstlane(DA[j2]);
     int32_t acc = 0;
     for (int32_t t0 = j + 1; t0 <= j2; t0 += kWave) {
         int32_t t = t0 + lane_id();
@@ -158,12 +161,14 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     }
     __syncthreads();
 
-    // scans: comb (stride N) then KV and batch prefix sums; last over-capacity iteration
+    // scans: comb (stride N) then the KV prefix sum; last over-capacity
+    // iteration.  The batch curve stays a difference array: admissions add
+    // their +1 / -1 to it and the output takes its prefix sum.
     const int32_t cap = P.kv_cap[s];
     int32_t last_over = -1;
     {
         const int32_t lane_mod = lane % N;
-        int32_t carry_kv = 0, carry_b = 0;
+        int32_t carry_kv = 0;
         for (int32_t t0 = 0; t0 < H; t0 += kWave) {
             const int32_t t = t0 + lane;
             const bool in = t < H;
@@ -175,13 +180,10 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
             const int32_t prev = t0 + lane_mod - N;
             if (prev >= 0 && in) c += CD[prev];
             if (in) CD[t] = c;
-            int32_t y = wave_incl_scan((in ? KV[t] : 0) + c) + carry_kv;
-            carry_kv = __shfl(y, kWave - 1);
-            int32_t b = wave_incl_scan(in ? BI[t] : 0) + carry_b;
-            carry_b = __shfl(b, kWave - 1);
+            const int32_t y = wave_incl_scan((in ? KV[t] : 0) + c) + carry_kv;
+            carry_kv = __builtin_amdgcn_readlane(y, kWave - 1);
             if (in) {
                 KV[t] = y;
-                BI[t] = b;
                 if (y > cap) last_over = t;
             }
         }
@@ -192,16 +194,22 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     if (last_over >= 0 || (has_bcap && n_in > bcap)) fl |= TL_FLAG_OVERCOMMIT;
 
     // FIFO admission of queued requests.  One wave does it; every value the
-    // loop carries (iteration j, batch count, the head's fields, check
+    // loop carries (iteration j, batch size, the head's fields, check
     // outcomes) is wave-uniform and kept in scalar registers.  LDS accesses
-    // of one wave are processed in order, so lane 0's updates of DA are seen
-    // by the later reads of every lane.
-    int32_t* DA = CD;   // admitted-batch difference array
+    // of one wave are processed in order, so one lane's updates are seen by
+    // the later reads of every lane.
+    int32_t* BD = BI;   // batch differences: in-flight requests, then admitted ones
+    int32_t* W = CD;    // scratch curve of batched admission, kept zero between batches
     if (has_queue) {
-        for (int32_t t = lane; t < H; t += kWave) DA[t] = 0;
+        __syncthreads();
+        for (int32_t t = lane; t < H; t += kWave) W[t] = 0;
         __syncthreads();
         int32_t j = 0;
-        int32_t run = 0;    // admitted requests active at j (kept only under a batch cap)
+        int32_t run = 0;    // batch size at j (prefix of BD; kept only under a batch cap)
+        if (has_bcap) run = __builtin_amdgcn_readfirstlane(BD[0]);
+        int32_t bsz = kWave;   // requests tried as one batch (no batch cap)
+        int32_t seq_left = 0;  // one-at-a-time admissions before the next batch try
+        int32_t backoff = 1;   // ... after the next run of failed batches
         int64_t cb = lo - kWave;
         int32_t q_arr = 0, q_c = 0, q_len = 0, q_lost = 0;
         uint64_t q_dl = kNoDeadline;
@@ -224,7 +232,83 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 mask = __ballot(q);
             }
             if (mask == 0) break;
-            // the head of the queue (uniform lane: lane reads, no LDS shuffle)
+
+            if (!has_bcap && bsz > 1 && seq_left == 0) {
+                // Batched admission of the next bsz queued requests, each at
+                // its FIFO target: the running maximum of the arrivals, from
+                // max(j, last_over + 1).  Their summed contribution is added
+                // to the KV curve and checked once.  If the sum fits
+                // everywhere, so does every request's own check at its target
+                // (each sees the KV of the requests before it, which is no
+                // more than the sum): these are exactly the admissions the
+                // one-at-a-time loop makes.  Otherwise retry with fewer.
+                const int32_t lo_j = max(j, last_over + 1);
+                const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+                    (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+                const bool mem = ((mask >> lane) & 1) && (int32_t)below < bsz;
+                const int32_t a = wave_incl_max(mem ? max(q_arr, lo_j) : -1);
+                const uint64_t memm = __ballot(mem);
+                const uint64_t over = __ballot(mem && a >= H);
+                const uint64_t take = over ? (memm & ((over & (~over + 1)) - 1)) : memm;
+                if (take == 0) break;   // the head cannot start within the horizon
+                int32_t r_end = 0;
+                for (uint64_t mm = take; mm; mm &= mm - 1) {
+                    const int m = __ffsll((unsigned long long)mm) - 1;
+                    const int32_t am = __builtin_amdgcn_readlane(a, m);
+                    const int32_t cm = __builtin_amdgcn_readlane(q_c, m);
+                    const int32_t lm = __builtin_amdgcn_readlane(q_len, m);
+                    const int32_t lim = (int32_t)min((int64_t)am + lm, (int64_t)H);
+                    r_end = max(r_end, lim);
+                    // LDS adds without a returned value: no wait per chunk
+                    for (int32_t t0 = am; t0 < lim; t0 += kWave) {
+                        const int32_t t = t0 + lane;
+                        if (t < lim) atomicAdd(&W[t], (int32_t)ceil_div_u32((uint32_t)(cm + t - am), divN));
+                    }
+                }
+                const int32_t a_first = __builtin_amdgcn_readlane(a, __ffsll((unsigned long long)take) - 1);
+                bool bad = false;
+                for (int32_t t0 = a_first; t0 < r_end; t0 += kWave) {
+                    const int32_t t = t0 + lane;
+                    if (t < r_end && KV[t] + W[t] > cap) bad = true;
+                }
+                const bool fits = __ballot(bad) == 0;
+                for (int32_t t0 = a_first; t0 < r_end; t0 += kWave) {
+                    const int32_t t = t0 + lane;
+                    if (t < r_end) {
+                        if (fits) KV[t] += W[t];
+                        W[t] = 0;
+                    }
+                }
+                if (!fits) {
+                    // shrink the batch; once down to single requests, admit
+                    // a growing number of them one at a time before batching
+                    // again (the capacity binds)
+                    bsz >>= 2;
+                    if (bsz < 2) {
+                        bsz = 2;
+                        seq_left = backoff;
+                        backoff = min(2 * backoff, 256);
+                    }
+                    continue;
+                }
+                if ((take >> lane) & 1) {
+                    const int64_t e = (int64_t)a + q_len;
+                    atomicAdd(&BD[a], 1);
+                    if (e < H) atomicAdd(&BD[e], -1);
+                    if (e <= H && !q_lost && q_dl != kNoDeadline)
+                        atomicMin((unsigned long long*)&outDL[e - 1], (unsigned long long)q_dl);
+                }
+                n_end = max(n_end, r_end);
+                j = __builtin_amdgcn_readlane(a, 63 - __clzll((long long)take));
+                mask &= ~take;
+                bsz = min(kWave, 2 * bsz);
+                backoff = 1;
+                if (over) break;
+                continue;
+            }
+
+            // One request at a time (under a batch cap, or after batches
+            // failed).  The head of the queue: uniform lane, lane reads.
             const int hl = __ffsll((unsigned long long)mask) - 1;
             const int32_t h_arr = __builtin_amdgcn_readlane(q_arr, hl);
             const int32_t h_c = __builtin_amdgcn_readlane(q_c, hl);
@@ -235,12 +319,11 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 (uint32_t)__builtin_amdgcn_readlane((int32_t)(uint32_t)q_dl, hl);
             const int32_t target = max(max(h_arr, j), last_over + 1);
             if (h_arr >= H || target >= H) break;
-            if (has_bcap && target > j) run += sum_range(DA, j, target);
+            if (has_bcap && target > j) run += sum_range(BD, j, target);
             j = target;
             bool admitted = false;
             for (;;) {
-                bool ok = true;
-                if (has_bcap) ok = __builtin_amdgcn_readfirstlane(BI[j] + run) < bcap;
+                bool ok = !has_bcap || run < bcap;
                 int32_t t_bad = -1;
                 if (ok) {
                     const int32_t lim = (int32_t)min((int64_t)j + h_len, (int64_t)H);
@@ -272,7 +355,7 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                     nj = (int32_t)max((int64_t)nj, first);
                 }
                 if (nj >= H) break;
-                if (has_bcap) run += sum_range(DA, j, nj);
+                if (has_bcap) run += sum_range(BD, j, nj);
                 j = nj;
             }
             if (!admitted) break;
@@ -283,30 +366,29 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 if (t < lim) KV[t] += (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN);
             }
             if (lane == 0) {
-                DA[j] += 1;
-                if (e < H) DA[e] -= 1;
+                BD[j] += 1;
+                if (e < H) BD[e] -= 1;
                 if (e <= H && !h_lost && h_dl != kNoDeadline)
                     atomicMin((unsigned long long*)&outDL[e - 1], (unsigned long long)h_dl);
             }
             run += 1;
             n_end = max(n_end, lim);
             mask &= mask - 1;
+            if (seq_left > 0) --seq_left;
         }
     }
     __syncthreads();
 
-    // outputs: curves, optional feature rows, scalars
+    // outputs: curves (batch = prefix sum of BD), optional feature rows, scalars
     {
-        int32_t carry_a = 0;
+        int32_t carry_b = 0;
         const float eng = (P.rows && P.nf == 4) ? P.engine[s] : 0.0f;
         for (int32_t t0 = 0; t0 < H; t0 += kWave) {
             const int32_t t = t0 + lane;
             const bool in = t < H;
-            int32_t da = (has_queue && in) ? DA[t] : 0;
-            da = wave_incl_scan(da) + carry_a;
-            carry_a = __shfl(da, kWave - 1);
+            const int32_t b = wave_incl_scan(in ? BD[t] : 0) + carry_b;
+            carry_b = __builtin_amdgcn_readlane(b, kWave - 1);
             if (!in) continue;
-            const int32_t b = BI[t] + da;
             const int32_t k = KV[t];
             outB[t] = b;
             outKV[t] = k;
