@@ -162,6 +162,42 @@ def test_project_overcommit_and_caps(gpu):
     assert_projection_equal(gpu_project(inp), o, "overcommit")
 
 
+@pytest.mark.parametrize("bcap,seed", [(False, 11), (True, 12), (False, 13)])
+def test_project_long_queues(gpu, bcap, seed):
+    """Hundreds of queued requests per scenario (several 64-request windows),
+    capacities from slack to binding, some arrival orders unsorted: the
+    batched and the one-at-a-time admission paths both run and must give the
+    oracle's admissions."""
+    rng = np.random.default_rng(seed)
+    S, H, N = 48, 600, 16
+    counts = rng.integers(150, 400, S)
+    off = np.zeros(S + 1, np.int64)
+    np.cumsum(counts, out=off[1:])
+    R = int(off[-1])
+    prompt = rng.integers(16, 2000, R).astype(np.int32)
+    gen = np.zeros(R, np.int32)
+    rem = np.clip(rng.lognormal(4.0, 1.0, R), 1, 3 * H).astype(np.int32)
+    arr = np.full(R, -1, np.int32)
+    for s in range(S):
+        lo, hi = off[s], off[s + 1]
+        nin = int(rng.integers(0, 30))
+        gen[lo:lo + nin] = rng.integers(0, 200, nin)
+        a = np.sort(rng.integers(0, H + 20, hi - lo - nin)).astype(np.int32)
+        if s % 7 == 3:
+            rng.shuffle(a)
+        arr[lo + nin:hi] = a
+    cap = rng.integers(300, 6000, S).astype(np.int32)
+    inp = dict(n_scenarios=S, horizon=H, block_tokens=N, req_offset=off, prompt=prompt, generated=gen,
+               remaining=rem, arrival=arr, deadline_ns=rng.integers(1, 10 ** 9, R).astype(np.uint64),
+               lost=(rng.random(R) < 0.01).astype(np.uint8), kv_capacity=cap,
+               batch_cap=rng.integers(5, 60, S).astype(np.int32) if bcap else None)
+    o = oracle.project(inp, return_admit=True)
+    adm = o["admit_iter"]
+    late = (adm > arr) & (arr >= 0)
+    assert late.sum() > 100 and ((adm >= 0) & (adm == arr)).sum() > 1000   # both regimes occur
+    assert_projection_equal(gpu_project(inp), o, f"long queues bcap={bcap}")
+
+
 def test_project_size_guard(gpu):
     H, N = 16, 1
     big = 1 << 30
