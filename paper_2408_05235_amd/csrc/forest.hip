@@ -113,6 +113,9 @@ __global__ __launch_bounds__(256) void forest_rows_kernel(const uint2* __restric
 #ifndef TL_LDS_BUDGET_KIB
 #define TL_LDS_BUDGET_KIB 152
 #endif
+#ifndef TL_LDS_WAVES_PER_SIMD
+#define TL_LDS_WAVES_PER_SIMD 4
+#endif
 constexpr int kLdsJ = TL_LDS_J;          // future iterations per wavefront (LDS kernel)
 constexpr int kGlobalJ = 32;             // future iterations per wavefront (global kernel)
 
@@ -172,7 +175,10 @@ __device__ __forceinline__ float to_sgpr(float x) {
     return r;
 }
 
-constexpr int kRowGroup = 4;   // rows whose (KV, batch) hull is tested as one
+#ifndef TL_ROW_GROUP
+#define TL_ROW_GROUP 4
+#endif
+constexpr int kRowGroup = TL_ROW_GROUP;   // rows whose (KV, batch) hull is tested as one
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
@@ -321,7 +327,7 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
 }
 
 template <int NF, int J>
-__global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const uint4* __restrict__ records,
+__global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_grid_lds_kernel(const uint4* __restrict__ records,
                                                                       int32_t n_trees, int32_t depth,
                                                                       int32_t tb, float base, GridParams P) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -353,9 +359,9 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
     // kStageRegs words: one load per word straight into its own register, so
     // the loads stay in flight while the current block is evaluated.
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
-    static_assert(kStageRegs >= 1 && kStageRegs <= 8, "staging code below moves up to eight words");
+    static_assert(kStageRegs >= 1 && kStageRegs <= 12, "staging code below moves up to twelve words");
     uint4 rw0 = make_uint4(0, 0, 0, 0), rw1 = rw0, rw2 = rw0, rw3 = rw0;
-    uint4 rw4 = rw0, rw5 = rw0, rw6 = rw0, rw7 = rw0;
+    uint4 rw4 = rw0, rw5 = rw0, rw6 = rw0, rw7 = rw0, rw8 = rw0, rw9 = rw0, rw10 = rw0, rw11 = rw0;
     double acc[J];
 #pragma unroll
     for (int jj = 0; jj < J; ++jj) acc[jj] = (double)base;
@@ -376,6 +382,8 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
         TL_FETCH_WORD(2, rw2) TL_FETCH_WORD(3, rw3)                            \
         TL_FETCH_WORD(4, rw4) TL_FETCH_WORD(5, rw5)                            \
         TL_FETCH_WORD(6, rw6) TL_FETCH_WORD(7, rw7)                            \
+        TL_FETCH_WORD(8, rw8) TL_FETCH_WORD(9, rw9)                            \
+        TL_FETCH_WORD(10, rw10) TL_FETCH_WORD(11, rw11)                        \
     }
 #define TL_STORE_WORD(r, reg)                                                  \
     if ((r) < kStageRegs) {                                                    \
@@ -390,6 +398,8 @@ __global__ __launch_bounds__(kLdsThreads, 4) void forest_grid_lds_kernel(const u
         TL_STORE_WORD(2, rw2) TL_STORE_WORD(3, rw3)                            \
         TL_STORE_WORD(4, rw4) TL_STORE_WORD(5, rw5)                            \
         TL_STORE_WORD(6, rw6) TL_STORE_WORD(7, rw7)                            \
+        TL_STORE_WORD(8, rw8) TL_STORE_WORD(9, rw9)                            \
+        TL_STORE_WORD(10, rw10) TL_STORE_WORD(11, rw11)                        \
     }
 
     // Make the lane's frequency / engine size complete here, before any
