@@ -126,16 +126,21 @@ struct GridItem {
     int32_t f, j0, nj;
 };
 
+// Items are numbered scenario-fastest: the wavefronts of one workgroup take
+// the same iteration chunk (and frequency group) of consecutive scenarios.
+// How many walks a chunk needs follows how fast KV and batch change there,
+// which depends mostly on the chunk's place in the horizon; workgroups whose
+// wavefronts do similar work lose less time at their block barriers.
 __device__ __forceinline__ GridItem grid_item(const GridParams& P, int64_t item, int J) {
     const int32_t n_chunks = (P.H + J - 1) / J;
     const int32_t n_fg = (P.F + kWave - 1) / kWave;
     GridItem g;
     g.valid = item < P.S * n_fg * n_chunks;
     const int64_t it = g.valid ? item : 0;
-    const int32_t chunk = (int32_t)(it % n_chunks);
-    const int64_t rest = it / n_chunks;
+    g.s = it % P.S;
+    const int64_t rest = it / P.S;
     g.f = (int32_t)(rest % n_fg) * kWave + lane_id();
-    g.s = rest / n_fg;
+    const int32_t chunk = (int32_t)(rest / n_fg);
     g.j0 = chunk * J;
     g.nj = min(J, P.H - g.j0);
     return g;
