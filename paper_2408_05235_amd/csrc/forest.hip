@@ -172,12 +172,15 @@ constexpr int kLdsThreads = kLdsWaves * kWave;
 #endif
 constexpr int kStageRegs = TL_STAGE_REGS;  // staged 16-byte words per thread per block
 
-// A wavefront-uniform value pinned in a scalar register (the compiler would
-// otherwise rematerialize it in vector registers).
+// A wavefront-uniform value read into a scalar register: the compiler's lane
+// read, with the empty asm statements hiding how x was computed and pinning
+// the result to the scalar register file (the compiler would otherwise
+// rematerialize it in vector registers).
 __device__ __forceinline__ float to_sgpr(float x) {
-    float r;
-    asm volatile("v_readfirstlane_b32 %0, %1" : "=s"(r) : "v"(x));
-    return r;
+    asm volatile("" : "+v"(x));
+    int32_t r = __builtin_amdgcn_readfirstlane(__float_as_int(x));
+    asm volatile("" : "+s"(r));
+    return __int_as_float(r);
 }
 
 #ifndef TL_ROW_GROUP
