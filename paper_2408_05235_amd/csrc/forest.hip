@@ -24,8 +24,10 @@
 //       copy.  Tree walks read LDS only.  A node step picks the tested
 //       feature with byte permutes and compares once, all in vector
 //       registers (no lane-mask round trip).  Trees are taken in pairs that
-//       share one box test and one walk pass, and rows in groups of eight
-//       whose (KV, batch) hull is tested before any single row.
+//       share one box test (a row that leaves it walks only the tree whose
+//       own box it left), and rows in groups of four whose (KV, batch) hull
+//       is tested before any single row.  The wavefronts of a workgroup take
+//       the same iteration chunk of consecutive scenarios.
 //   forest_grid_global_kernel  (deeper trees) The same per-lane scheme with
 //       nodes, leaves and boxes read from global memory, one row at a time.
 //
