@@ -2,6 +2,7 @@
 // forest upload, kernel dispatch and error reporting.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -20,6 +21,7 @@ struct tl_forest {
     void* leaves_mem;
     void* box_mem;
     void* records_mem;
+    void* cuts_mem;   // [kMaxCuts] KV cuts, then [kMaxCuts] batch cuts
 };
 
 namespace {
@@ -59,6 +61,18 @@ void leaf_boxes(int32_t n_trees, int32_t depth, const uint8_t* feature, const fl
                                                   : make_float4(lo[0], hi[0], lo[1], hi[1]);
         }
     }
+}
+
+// Up to kMaxCuts quantiles of the finite thresholds of one feature, ascending.
+std::vector<float> threshold_cuts(int64_t n_nodes, const uint8_t* feature, const float* threshold, int fi) {
+    std::vector<float> t;
+    for (int64_t i = 0; i < n_nodes; ++i)
+        if (feature[i] == fi && std::isfinite(threshold[i])) t.push_back(threshold[i]);
+    std::sort(t.begin(), t.end());
+    if ((int64_t)t.size() <= tl::kMaxCuts) return t;
+    std::vector<float> c(tl::kMaxCuts);
+    for (int64_t i = 0; i < tl::kMaxCuts; ++i) c[(size_t)i] = t[(size_t)(i * (int64_t)t.size() / tl::kMaxCuts)];
+    return c;
 }
 
 tl_status fail(tl_status st, const char* fmt, ...) {
@@ -144,6 +158,11 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
         }
         boxes.resize(cells + 4, make_float4(0, 0, 0, 0));
     }
+    std::vector<float> cuts_kv, cuts_bs;
+    if (n_features >= 3 && n_int > 0) {
+        cuts_kv = threshold_cuts(n_trees * n_int, feature, threshold, 1);
+        cuts_bs = threshold_cuts(n_trees * n_int, feature, threshold, 2);
+    }
 
     tl_forest* f = new (std::nothrow) tl_forest();
     if (!f) return fail(TL_ENOMEM, "tl_forest_create: host allocation failed");
@@ -155,13 +174,17 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     if (e != hipSuccess) { (void)hipFree(f->nodes_mem); delete f; return from_hip(e, "tl_forest_create: hipMalloc(leaves)"); }
     f->box_mem = nullptr;
     f->records_mem = nullptr;
+    f->cuts_mem = nullptr;
+    const size_t cut_bytes = 2 * (size_t)tl::kMaxCuts * sizeof(float);
     if (!boxes.empty()) e = hipMalloc(&f->box_mem, boxes.size() * sizeof(float4));
     if (e == hipSuccess && !records.empty()) e = hipMalloc(&f->records_mem, records.size());
+    if (e == hipSuccess && !cuts_kv.empty() && !cuts_bs.empty()) e = hipMalloc(&f->cuts_mem, cut_bytes);
     if (e != hipSuccess) {
         (void)hipFree(f->nodes_mem);
         (void)hipFree(f->leaves_mem);
         if (f->box_mem) (void)hipFree(f->box_mem);
         if (f->records_mem) (void)hipFree(f->records_mem);
+        if (f->cuts_mem) (void)hipFree(f->cuts_mem);
         delete f;
         return from_hip(e, "tl_forest_create: hipMalloc");
     }
@@ -172,11 +195,18 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
         e = hipMemcpy(f->box_mem, boxes.data(), boxes.size() * sizeof(float4), hipMemcpyHostToDevice);
     if (e == hipSuccess && f->records_mem)
         e = hipMemcpy(f->records_mem, records.data(), records.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess && f->cuts_mem) {
+        std::vector<float> cuts(2 * (size_t)tl::kMaxCuts, 0.0f);
+        std::copy(cuts_kv.begin(), cuts_kv.end(), cuts.begin());
+        std::copy(cuts_bs.begin(), cuts_bs.end(), cuts.begin() + tl::kMaxCuts);
+        e = hipMemcpy(f->cuts_mem, cuts.data(), cut_bytes, hipMemcpyHostToDevice);
+    }
     if (e != hipSuccess) {
         (void)hipFree(f->nodes_mem);
         (void)hipFree(f->leaves_mem);
         if (f->box_mem) (void)hipFree(f->box_mem);
         if (f->records_mem) (void)hipFree(f->records_mem);
+        if (f->cuts_mem) (void)hipFree(f->cuts_mem);
         delete f;
         return from_hip(e, "tl_forest_create: hipMemcpy");
     }
@@ -188,6 +218,10 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     f->dev.leaves = (const float*)f->leaves_mem;
     f->dev.kvb_box = (const float4*)f->box_mem;
     f->dev.records = (const uint4*)f->records_mem;
+    f->dev.cuts_kv = f->cuts_mem ? (const float*)f->cuts_mem : nullptr;
+    f->dev.cuts_bs = f->cuts_mem ? (const float*)f->cuts_mem + tl::kMaxCuts : nullptr;
+    f->dev.n_cuts_kv = f->cuts_mem ? (int32_t)cuts_kv.size() : 0;
+    f->dev.n_cuts_bs = f->cuts_mem ? (int32_t)cuts_bs.size() : 0;
     *out = f;
     return ok();
 }
@@ -199,6 +233,7 @@ void tl_forest_destroy(tl_forest* f) {
     (void)hipFree(f->leaves_mem);
     if (f->box_mem) (void)hipFree(f->box_mem);
     if (f->records_mem) (void)hipFree(f->records_mem);
+    if (f->cuts_mem) (void)hipFree(f->cuts_mem);
     delete f;
 }
 

@@ -39,6 +39,8 @@
 //
 // forest_rows_kernel evaluates arbitrary rows: each thread walks RPT
 // consecutive rows through every tree.
+#include <hipcub/hipcub.hpp>
+
 #include "device_util.h"
 #include "tl_internal.h"
 
@@ -130,22 +132,76 @@ struct GridItem {
 
 // Items are numbered scenario-fastest: the wavefronts of one workgroup take
 // the same iteration chunk (and frequency group) of consecutive scenarios.
-// How many walks a chunk needs follows how fast KV and batch change there,
-// which depends mostly on the chunk's place in the horizon; workgroups whose
-// wavefronts do similar work lose less time at their block barriers.
+// How many walks a chunk needs follows how fast KV and batch change there;
+// workgroups whose wavefronts do similar work lose less time at their block
+// barriers.  With a work order (P.order), item i of a frequency group takes
+// the (scenario, chunk) pair order[i] instead: pairs sorted by estimated
+// cost, most expensive first.
 __device__ __forceinline__ GridItem grid_item(const GridParams& P, int64_t item, int J) {
     const int32_t n_chunks = (P.H + J - 1) / J;
     const int32_t n_fg = (P.F + kWave - 1) / kWave;
     GridItem g;
     g.valid = item < P.S * n_fg * n_chunks;
     const int64_t it = g.valid ? item : 0;
-    g.s = it % P.S;
-    const int64_t rest = it / P.S;
-    g.f = (int32_t)(rest % n_fg) * kWave + lane_id();
-    const int32_t chunk = (int32_t)(rest / n_fg);
+    const int64_t n_pairs = P.S * n_chunks;
+    int32_t chunk;
+    if (P.order) {
+        const uint32_t code = P.order[it % n_pairs];
+        g.s = code / (uint32_t)n_chunks;
+        chunk = (int32_t)(code % (uint32_t)n_chunks);
+        g.f = (int32_t)(it / n_pairs) * kWave + lane_id();
+    } else {
+        g.s = it % P.S;
+        const int64_t rest = it / P.S;
+        g.f = (int32_t)(rest % n_fg) * kWave + lane_id();
+        chunk = (int32_t)(rest / n_fg);
+    }
     g.j0 = chunk * J;
     g.nj = min(J, P.H - g.j0);
     return g;
+}
+
+// Estimated cost of each (scenario, chunk) pair of the grid: how many KV and
+// batch threshold cuts its rows cross from one row to the next (each crossing
+// may change a leaf, i.e. cost a walk).  One thread per pair; the cuts sit in
+// LDS.  Writes cost[i] and the pair code i = s * n_chunks + chunk.
+constexpr int kCostThreads = 256;
+
+__global__ __launch_bounds__(kCostThreads) void grid_cost_kernel(const float* __restrict__ cuts_kv, int32_t n_kv,
+                                                                 const float* __restrict__ cuts_bs, int32_t n_bs,
+                                                                 const int32_t* __restrict__ kv,
+                                                                 const int32_t* __restrict__ batch, int64_t S,
+                                                                 int32_t H, int32_t J, uint32_t* __restrict__ cost,
+                                                                 uint32_t* __restrict__ code) {
+    __shared__ float ck[kMaxCuts], cb[kMaxCuts];
+    for (int32_t i = threadIdx.x; i < n_kv; i += kCostThreads) ck[i] = cuts_kv[i];
+    for (int32_t i = threadIdx.x; i < n_bs; i += kCostThreads) cb[i] = cuts_bs[i];
+    __syncthreads();
+    const int32_t n_chunks = (H + J - 1) / J;
+    const int64_t i = (int64_t)blockIdx.x * kCostThreads + threadIdx.x;
+    if (i >= S * n_chunks) return;
+    const int64_t s = i / n_chunks;
+    const int32_t j0 = (int32_t)(i % n_chunks) * J, j1 = min(j0 + J, H);
+    // number of cuts <= x
+    auto rank = [](const float* c, int32_t n, float x) {
+        int32_t lo = 0, hi = n;
+        while (lo < hi) {
+            const int32_t mid = (lo + hi) >> 1;
+            if (c[mid] <= x) lo = mid + 1;
+            else hi = mid;
+        }
+        return lo;
+    };
+    int32_t rk = rank(ck, n_kv, (float)kv[s * H + j0]), rb = rank(cb, n_bs, (float)batch[s * H + j0]);
+    uint32_t c = 0;
+    for (int32_t j = j0 + 1; j < j1; ++j) {
+        const int32_t nk = rank(ck, n_kv, (float)kv[s * H + j]), nb = rank(cb, n_bs, (float)batch[s * H + j]);
+        c += (uint32_t)(abs(nk - rk) + abs(nb - rb));
+        rk = nk;
+        rb = nb;
+    }
+    cost[i] = c;
+    code[i] = (uint32_t)i;
 }
 
 // ---------------------------------------------------------------- LDS-staged
@@ -595,12 +651,57 @@ hipError_t launch_grid_global(const ForestDev& f, const GridParams& g, hipStream
 }  // namespace
 
 
-hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, hipStream_t stream) {
+// Work order for the LDS kernel: (scenario, chunk) pairs by estimated cost,
+// most expensive first, so a workgroup's wavefronts do similar work and the
+// longest ones start first.  Scratch comes from the stream-ordered pool and
+// is released on the stream.  Returns false (no order) when it does not
+// apply; errors are returned through *err.
+bool order_grid(const ForestDev& f, GridParams& g, hipStream_t stream, void** scratch, hipError_t* err) {
+    *err = hipSuccess;
+    const int64_t n_chunks = (g.H + kLdsJ - 1) / kLdsJ;
+    const int64_t n = g.S * n_chunks;
+    if (!f.cuts_kv || !f.cuts_bs || n < 2 * kLdsWaves || n >= (int64_t)1 << 31) return false;
+    size_t temp = 0;
+    *err = hipcub::DeviceRadixSort::SortPairsDescending(nullptr, temp, (const uint32_t*)nullptr, (uint32_t*)nullptr,
+                                                        (const uint32_t*)nullptr, (uint32_t*)nullptr, (int)n, 0, 32,
+                                                        stream);
+    if (*err != hipSuccess) return false;
+    const size_t arr = ((size_t)n * sizeof(uint32_t) + 255) & ~(size_t)255;
+    *err = hipMallocAsync(scratch, 4 * arr + temp, stream);
+    if (*err != hipSuccess) return false;
+    unsigned char* base = (unsigned char*)*scratch;
+    uint32_t* cost = (uint32_t*)base;
+    uint32_t* code = (uint32_t*)(base + arr);
+    uint32_t* cost_sorted = (uint32_t*)(base + 2 * arr);
+    uint32_t* order = (uint32_t*)(base + 3 * arr);
+    hipLaunchKernelGGL(grid_cost_kernel, dim3((unsigned)((n + kCostThreads - 1) / kCostThreads)), dim3(kCostThreads), 0,
+                       stream, f.cuts_kv, f.n_cuts_kv, f.cuts_bs, f.n_cuts_bs, g.kv, g.batch, g.S, g.H, kLdsJ, cost,
+                       code);
+    *err = hipGetLastError();
+    if (*err == hipSuccess)
+        *err = hipcub::DeviceRadixSort::SortPairsDescending(base + 4 * arr, temp, cost, cost_sorted, code, order,
+                                                            (int)n, 0, 32, stream);
+    if (*err != hipSuccess) return false;
+    g.order = order;
+    return true;
+}
+
+hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g_in, hipStream_t stream) {
+    GridParams g = g_in;
+    g.order = nullptr;
     size_t lds = 0;
     const int32_t tb = lds_trees_per_block(f, &lds);
-    if (tb > 0)
-        return f.n_features == 4 ? launch_grid_lds<4>(f, g, tb, lds, stream) : launch_grid_lds<3>(f, g, tb, lds, stream);
-    return f.n_features == 4 ? launch_grid_global<4>(f, g, stream) : launch_grid_global<3>(f, g, stream);
+    if (tb <= 0) return f.n_features == 4 ? launch_grid_global<4>(f, g, stream) : launch_grid_global<3>(f, g, stream);
+    void* scratch = nullptr;
+    hipError_t e = hipSuccess;
+    order_grid(f, g, stream, &scratch, &e);
+    if (e == hipSuccess)
+        e = f.n_features == 4 ? launch_grid_lds<4>(f, g, tb, lds, stream) : launch_grid_lds<3>(f, g, tb, lds, stream);
+    if (scratch) {
+        const hipError_t e2 = hipFreeAsync(scratch, stream);
+        if (e == hipSuccess) e = e2;
+    }
+    return e;
 }
 
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,

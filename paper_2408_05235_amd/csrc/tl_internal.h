@@ -65,7 +65,17 @@ struct ForestDev {
     // (layout: record_layout).  Present when n_features >= 3 and the depth
     // is at most kMaxRecordDepth, else NULL.
     const uint4* records;
+    // Quantiles of the forest's KV (feature 1) and batch (feature 2)
+    // thresholds, ascending, at most kMaxCuts each (NULL / 0 when
+    // n_features < 3).  Between two rows, the number of cuts crossed by KV
+    // and batch estimates how many tree decisions change: the cost model
+    // for ordering the grid kernel's work.
+    const float* cuts_kv;
+    const float* cuts_bs;
+    int32_t n_cuts_kv, n_cuts_bs;
 };
+
+constexpr int32_t kMaxCuts = 4096;
 
 constexpr int kMaxRecordDepth = 11;
 
@@ -100,6 +110,9 @@ struct GridParams {
     const int32_t* batch;   // [S][H]
     const float* engine;    // [S] (4 features) or NULL
     float* out;             // [S][F][H]
+    // optional work order: entry i is the (scenario, chunk) pair s * n_chunks
+    // + chunk that the i-th item (of each frequency group) evaluates
+    const uint32_t* order;
 };
 
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
