@@ -193,6 +193,10 @@ tl_status tl_forest_predict(const tl_forest* forest, const float* rows, int64_t 
  * ignored otherwise; out [S][F][H] fp32.  The forest must have 3 or 4
  * features in the order (frequency, KV, batch[, engine size]).
  * 1 <= F <= TL_MAX_FREQS, 1 <= H <= TL_MAX_HORIZON.
+ * Work is ordered by an estimate of its cost (results do not depend on the
+ * order); the ordering takes about 16 bytes per (scenario, 32-iteration
+ * chunk) of device scratch from the stream-ordered allocator, released on
+ * the stream when the call's work is done.  TL_ENOMEM if that fails.
  * ---------------------------------------------------------------------- */
 tl_status tl_forest_predict_grid(const tl_forest* forest, int64_t n_scenarios, int32_t n_freqs,
                                  int32_t horizon, const float* freqs_mhz, const int32_t* kv,
