@@ -21,6 +21,11 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 
 
 def _short(name):
+    if "rocprim" in name:
+        # library sort kernels: keep the stage name of the config
+        import re
+        m = re.search(r"wrapped_([a-z_]+?)_config", name)
+        return "rocprim " + (m.group(1) if m else "kernel") + " (radix sort of the work order)"
     return name.replace("tl::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
 
 
