@@ -5,8 +5,11 @@ every (scenario, frequency, iteration) row, and frequency selection, for one
 batch of synthetic scenarios already resident in HBM.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c3] [--no-cpu-baseline]
+                    [--cpu-procs C]
 
-Prints one JSON line.
+Prints one JSON line: whole-step throughput, per-stage HIP-event times (mean,
+median, min over the K timed steps), the forest kernel's roofline record and
+the oracle's CPU baseline (one thread, and C single-threaded processes).
 """
 import argparse
 import hashlib
@@ -59,37 +62,93 @@ def traffic_record(cfg_name):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(inp, budget_s=12.0, max_scen=64):
+def _host_info():
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return dict(cpu_model=model, nproc=os.cpu_count(), affinity=len(os.sched_getaffinity(0)))
+
+
+def _oracle_scenarios(sub_inputs, budget_s):
+    """Run the oracle on whole scenarios, one after another, until the budget
+    is spent; returns (scenarios done, rows done, seconds)."""
     import oracle
-    from paper_2408_05235_amd import synth
-    S = inp["n_scenarios"]
-    order = [0, S - 1] + list(np.random.default_rng(0).permutation(S))
-    seen, done, rows, t_used = set(), [], 0, 0.0
-    F, H = inp["n_freqs"], inp["horizon"]
-    for s in order:
-        if s in seen:
-            continue
-        seen.add(s)
-        sub = synth.subset(inp, [s])
+    done, rows, t_used = 0, 0, 0.0
+    for sub in sub_inputs:
         t0 = time.perf_counter()
         oracle.end_to_end(sub)
         t_used += time.perf_counter() - t0
-        done.append(int(s))
-        rows += F * H
-        if t_used >= budget_s or len(done) >= max_scen:
+        done += 1
+        rows += sub["n_freqs"] * sub["horizon"]
+        if t_used >= budget_s:
             break
-    return dict(value=rows / t_used, unit="rows/s", cores=1, kind="oracle",
-                sample=f"{len(done)} of {S} scenarios (all stages, single thread), {t_used:.1f} s",
-                scenarios_per_s=len(done) / t_used)
+    return done, rows, t_used
+
+
+def cpu_baseline(inp, budget_s=12.0, max_scen=64, procs=0):
+    """The oracle timed on whole scenarios of the workload (s = 0, s = S-1,
+    then a seeded random order) for about `budget_s` seconds on one thread;
+    with `procs` > 1 also as that many single-threaded processes, each on its
+    own scenarios, for the same budget (rows of all processes / longest one)."""
+    from paper_2408_05235_amd import synth
+    S = inp["n_scenarios"]
+    order = list(dict.fromkeys([0, S - 1] + list(np.random.default_rng(0).permutation(S))))
+    done, rows, t_used = 0, 0, 0.0
+    F, H = inp["n_freqs"], inp["horizon"]
+    for s in order[:max_scen]:
+        d, r, t = _oracle_scenarios([synth.subset(inp, [s])], budget_s)
+        done, rows, t_used = done + d, rows + r, t_used + t
+        if t_used >= budget_s:
+            break
+    out = dict(value=rows / t_used, unit="rows/s", cores=1, kind="oracle",
+               sample=f"{done} of {S} scenarios (all stages, single thread), {t_used:.1f} s",
+               scenarios_per_s=done / t_used, **_host_info())
+    if procs > 1 and S >= 2 * procs:
+        import multiprocessing as mp
+        per = max(2, (max_scen * 2) // procs)
+        jobs = [[synth.subset(inp, [s]) for s in order[w::procs][:per]] for w in range(procs)]
+        t0 = time.perf_counter()
+        with mp.get_context("spawn").Pool(procs) as pool:
+            res = pool.starmap(_oracle_scenarios, [(j, budget_s) for j in jobs])
+        wall = time.perf_counter() - t0
+        n = sum(r[0] for r in res)
+        tot_rows = sum(r[1] for r in res)
+        t_max = max(r[2] for r in res)
+        out["sharded"] = dict(value=tot_rows / t_max, unit="rows/s", cores=procs, kind="oracle",
+                              sample=f"{n} of {S} scenarios in {procs} single-threaded processes, "
+                                     f"longest {t_max:.1f} s of oracle time ({wall:.1f} s wall with start-up)")
+    return out
+
+
+def _clock_record():
+    """Clock state as rocm-smi reports it (clocks are left at their defaults)."""
+    import subprocess
+    try:
+        r = subprocess.run(["rocm-smi", "--showperflevel", "--showclocks", "--json"],
+                           capture_output=True, text=True, timeout=20)
+        rec = json.loads(r.stdout)
+        card = next(iter(rec.values()))
+        keep = {k: v for k, v in card.items() if "perf" in k.lower() or "sclk" in k.lower()
+                or "mclk" in k.lower() or "fclk" in k.lower()}
+        return keep or card
+    except Exception as e:  # noqa: BLE001 - a missing tool only loses this record
+        return {"error": f"{type(e).__name__}: {e}"[:200]}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="c3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-procs", type=int, default=min(16, len(os.sched_getaffinity(0))),
+                    help="processes for the sharded oracle run (0 or 1: single thread only)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy a buffer of this size once (a known-size "
                          "kernel for scaling hardware byte counters)")
@@ -99,14 +158,23 @@ def main():
               "(scenarios are independent: shard them across GPUs, one process each)", file=sys.stderr)
         sys.exit(2)
 
-    import torch
-
-    from paper_2408_05235_amd import api, configs, synth
+    from paper_2408_05235_amd import configs, synth
 
     cfg = configs.get_config(args.config)
     t0 = time.perf_counter()
     inp = synth.make_inputs(cfg)
     log(f"inputs {cfg['name']}: {time.perf_counter() - t0:.1f}s, {int(inp['req_offset'][-1])} requests")
+    # host-side work that starts other processes runs before the GPU is touched
+    cpu_base = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        cpu_base = cpu_baseline(inp, procs=args.cpu_procs)
+    clocks = _clock_record()
+
+    import torch
+
+    from paper_2408_05235_amd import api
+
     torch.cuda.set_device(0)
     dev_in = api.upload(inp, "cuda:0")
     forest = api.Forest.from_dict(inp["forest"])
@@ -137,6 +205,7 @@ def main():
     log(f"timed {args.steps} steps in {wall:.2f}s")
 
     st = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] for e in ev])  # ms
+    step_ev = np.array([e[0].elapsed_time(e[3]) for e in ev])
     stage_ms = st.mean(axis=0)
     step_ms = wall * 1e3 / args.steps
     byt = algorithmic_bytes(inp, F, rows)
@@ -170,6 +239,12 @@ def main():
         "scenarios_per_s": S / (step_ms / 1e3),
         "hbm_frac_end_to_end": tot_bytes / (step_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
         "stages_ms": {"project": stage_ms[0], "predict": stage_ms[1], "select": stage_ms[2]},
+        "stages_ms_median": dict(zip(("project", "predict", "select"), np.median(st, axis=0).tolist())),
+        "stages_ms_min": dict(zip(("project", "predict", "select"), st.min(axis=0).tolist())),
+        "step_ms_events": {"median": float(np.median(step_ev)), "min": float(step_ev.min())},
+        "gpu": {"name": torch.cuda.get_device_properties(0).name,
+                "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,
+                "clocks": clocks},
         "stage_hbm_gbs": {k: byt[k] / (v / 1e3) / 1e9 for k, v in
                           zip(("project", "predict", "select"), stage_ms)},
         "forest_rows_per_s": rows / forest_s,
@@ -188,9 +263,8 @@ def main():
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = n * 4
         del src, dst
-    if not args.no_cpu_baseline:
-        log("cpu baseline (oracle) ...")
-        out["cpu_baseline"] = cpu_baseline(inp)
+    if cpu_base is not None:
+        out["cpu_baseline"] = cpu_base
     forest.close()
     print(json.dumps(out), flush=True)
 

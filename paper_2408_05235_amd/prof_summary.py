@@ -4,10 +4,20 @@
     python -m paper_2408_05235_amd.prof_summary traffic <fetch_counter_collection.csv> \
         <write_counter_collection.csv> <kernel substring> <copy bytes> <out.json> <command>
 
+    python -m paper_2408_05235_amd.prof_summary counters <out.md> <kernel substring> <command> \
+        <counter_collection.csv> [<counter_collection.csv> ...]
+
 `traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of one kernel into
 bytes per launch, each scaled by what the same counter reads for the last
 copy dispatch of the run, a copy of known size (the counters' byte formulas
 need not match the request sizes a kernel uses).
+
+`counters` averages every counter of the given runs over the dispatches of one
+kernel and derives the rates kept beside the kernel statistics: LDS bank
+conflict cycles per cycle of indexed LDS activity, and per LDS instruction.
+L2 hit rate from TCC_HIT and TCC_MISS (rocprofv3 has no L2CacheHit for gfx950).
+Derived counters that rocprofv3 computes itself (VALUBusy, VALUUtilization,
+both percentages) are reported as it gives them.
 """
 from __future__ import annotations
 
@@ -74,11 +84,51 @@ def traffic(fetch_csv, write_csv, kernel, copy_bytes, out_json, command):
     return rec
 
 
+def counters(out_md, kernel, command, csv_paths):
+    vals = {}
+    names = set()
+    for path in csv_paths:
+        for r in csv.DictReader(open(path)):
+            if kernel not in r["Kernel_Name"]:
+                continue
+            names.add(r["Kernel_Name"])
+            key = (r["Counter_Name"], path, int(r["Dispatch_Id"]))
+            vals[key] = vals.get(key, 0.0) + float(r["Counter_Value"])
+    if not vals:
+        raise SystemExit(f"no dispatch of {kernel} in {csv_paths}")
+    per = {}
+    for (c, _, _), v in vals.items():
+        per.setdefault(c, []).append(v)
+    avg = {c: sum(v) / len(v) for c, v in per.items()}
+    n_disp = {c: len(v) for c, v in per.items()}
+    lines = [f"# rocprofv3 counters of {_short(sorted(names)[0])}", "", "Command:", "", "```", command, "```", "",
+             "| counter | dispatches | average per dispatch |", "|---|---|---|"]
+    for c in sorted(avg):
+        lines.append(f"| {c} | {n_disp[c]} | {avg[c]:.6g} |")
+    derived = []
+    if "SQ_LDS_BANK_CONFLICT" in avg and avg.get("SQ_LDS_IDX_ACTIVE"):
+        derived.append(("LDS bank-conflict cycles / indexed-LDS-active cycles",
+                        avg["SQ_LDS_BANK_CONFLICT"] / avg["SQ_LDS_IDX_ACTIVE"]))
+    if "SQ_LDS_BANK_CONFLICT" in avg and avg.get("SQ_INSTS_LDS"):
+        derived.append(("LDS bank-conflict cycles per LDS instruction",
+                        avg["SQ_LDS_BANK_CONFLICT"] / avg["SQ_INSTS_LDS"]))
+    if avg.get("TCC_HIT_sum", 0) + avg.get("TCC_MISS_sum", 0) > 0:
+        derived.append(("L2 hit rate, % (TCC_HIT / (TCC_HIT + TCC_MISS))",
+                        100.0 * avg["TCC_HIT_sum"] / (avg["TCC_HIT_sum"] + avg["TCC_MISS_sum"])))
+    if derived:
+        lines += ["", "| derived | value |", "|---|---|"]
+        lines += [f"| {k} | {v:.4g} |" for k, v in derived]
+    open(out_md, "w").write("\n".join(lines) + "\n")
+    return avg, derived
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "stats":
         kernel_stats(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5] if len(sys.argv) > 5 else "")
     elif sys.argv[1] == "traffic":
         print(json.dumps(traffic(sys.argv[2], sys.argv[3], sys.argv[4], int(sys.argv[5]), sys.argv[6],
                                  sys.argv[7]), indent=1))
+    elif sys.argv[1] == "counters":
+        print(counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5:]))
     else:
         raise SystemExit(__doc__)
