@@ -8,7 +8,8 @@ code with the HIP library and never imports it.
 Functions follow the paper: ``project`` (Sec. 4.2, Eq. 1-2, admission check 1
 of Sec. 4.3.2), ``rows`` and ``forest_predict`` (Sec. 4.3.1), ``select`` and
 ``select_binary`` (Sec. 4.3.2 checks 2-3, Eq. 3-4, Sec. 4.5), ``latency_ns``
-(T' = 1/T in ns) and ``end_to_end`` (all three stages).
+(T' = 1/T in ns), ``end_to_end`` (all three stages) and ``admit`` (the
+admission control of Sec. 4.3.2 for one new query per scenario).
 """
 from __future__ import annotations
 
@@ -24,6 +25,7 @@ _LIB_PATH = os.path.join(_HERE, "libtl_oracle.so")
 
 FLAG_BAD_REQUEST, FLAG_LOST, FLAG_OVERCOMMIT, FLAG_OVERFLOW, FLAG_UNSORTED = 1, 2, 4, 8, 16
 STATUS_OK, STATUS_INFEASIBLE, STATUS_LOST, STATUS_INVALID = 0, 1, 2, 3
+ADMIT_OK, ADMIT_LOST, QUEUE_CAPACITY, QUEUE_TBT, QUEUE_E2E, ADMIT_INVALID = 0, 1, 2, 3, 4, 5
 NO_DEADLINE = np.uint64(0xFFFFFFFFFFFFFFFF)
 LAT_SATURATED = 1 << 40
 
@@ -177,3 +179,96 @@ def end_to_end(inp):
     ips = forest_predict(inp["forest"], x)
     idx, st = select(ips, proj["deadline_at"], proj["n_iters"], inp["tbt_slo_ns"], proj["flags"])
     return dict(proj, ips=ips, freq_idx=idx, status=st)
+
+
+def _append_candidate(inp, s, p, L):
+    """Scenario s of ``inp`` with the new query appended as a request that
+    starts now: prompt p, nothing generated, L iterations, no deadline (its
+    own deadline is checked apart), not lost."""
+    lo, hi = int(inp["req_offset"][s]), int(inp["req_offset"][s + 1])
+    out = dict(n_scenarios=1, horizon=inp["horizon"], block_tokens=inp["block_tokens"],
+               req_offset=np.array([0, hi - lo + 1], np.int64))
+    for k, v, t in (("prompt", p, np.int32), ("generated", 0, np.int32), ("remaining", L, np.int32),
+                    ("arrival", -1, np.int32)):
+        out[k] = np.append(np.asarray(inp[k][lo:hi], t), t(v))
+    if inp.get("deadline_ns") is not None:
+        out["deadline_ns"] = np.append(np.asarray(inp["deadline_ns"][lo:hi], np.uint64), NO_DEADLINE)
+    if inp.get("lost") is not None:
+        out["lost"] = np.append(np.asarray(inp["lost"][lo:hi], np.uint8), np.uint8(0))
+    out["kv_capacity"] = np.asarray(inp["kv_capacity"][s:s + 1], np.int32)
+    if inp.get("batch_cap") is not None:
+        out["batch_cap"] = np.asarray(inp["batch_cap"][s:s + 1], np.int32)
+    return out
+
+
+def admit(inp, cand_prompt, cand_len, cand_deadline_ns, max_freq_mhz, forest=None):
+    """Admission control for one new query per scenario (Sec. 4.3.2).
+
+    The query joins the scenario's virtual scoreboard as a request that starts
+    now (prompt ``cand_prompt[s]``, nothing generated, active for the
+    ``cand_len[s]`` iterations [0, L)).  On the projection with it (Eq. 1-2):
+      1. KV: some projected KV value exceeds the capacity, or the batch that
+         runs now exceeds the batch cap -> QUEUE_CAPACITY;
+      2. TBT: with M queried at the maximum frequency, T' = 1/T per iteration
+         (``latency_ns``) and T_R[l] = T'[0] + ... + T'[l-1] (Eq. 3), the mean
+         T' over the n projected iterations exceeds the SLO, T_R[n] > sigma*n
+         -> QUEUE_TBT;
+      3. E2E (Eq. 4): a scheduled request that is not lost and ends inside the
+         horizon at e misses T_R[e] < deadline -> QUEUE_E2E; if only the new
+         query's own deadline fails (checked when L <= H) -> ADMIT_LOST
+         (scheduled, marked lost);
+    otherwise ADMIT_OK.  A malformed query (prompt < 0 or > 2^30, L < 1) or a
+    scenario the projection cannot size -> ADMIT_INVALID.
+    Returns decision[S], ips[S][H] at the maximum frequency (zeros where not
+    evaluated) and the projection with the query."""
+    forest = inp["forest"] if forest is None else forest
+    S, H = int(inp["n_scenarios"]), int(inp["horizon"])
+    nf = int(forest["n_features"])
+    dec = np.zeros(S, np.uint32)
+    ips_all = np.zeros((S, H), np.float32)
+    proj_all = dict(batch=np.zeros((S, H), np.int32), kv=np.zeros((S, H), np.int32),
+                    deadline_at=np.full((S, H), NO_DEADLINE, np.uint64),
+                    n_iters=np.zeros(S, np.int32), flags=np.zeros(S, np.uint32))
+    for s in range(S):
+        p, L = int(cand_prompt[s]), int(cand_len[s])
+        d_own = np.uint64(cand_deadline_ns[s]) if cand_deadline_ns is not None else NO_DEADLINE
+        if p < 0 or p > (1 << 30) or L < 1:
+            dec[s] = ADMIT_INVALID
+            continue
+        board = _append_candidate(inp, s, p, L)
+        proj = project(board)
+        for k in proj_all:
+            proj_all[k][s] = proj[k][0]
+        if proj["flags"][0] & FLAG_OVERFLOW:
+            dec[s] = ADMIT_INVALID
+            continue
+        # check 1: the projected KV vector against the capacity
+        kv = proj["kv"][0]
+        bcap = board.get("batch_cap")
+        if int(kv.max()) > int(board["kv_capacity"][0]) or (bcap is not None and
+                                                          int(proj["batch"][0][0]) > int(bcap[0])):
+            dec[s] = QUEUE_CAPACITY
+            continue
+        # check 2: M at the maximum frequency on every projected iteration
+        eng = None if nf == 3 else np.asarray(inp["engine_size"][s:s + 1], np.float32)
+        x = rows(np.array([max_freq_mhz], np.float32), proj["batch"], proj["kv"], eng, nf)
+        ips = forest_predict(forest, x)[0, 0]
+        ips_all[s] = ips
+        n = int(proj["n_iters"][0])
+        t_r = [0]
+        for j in range(n):
+            t_r.append(t_r[-1] + latency_ns(ips[j]))
+        sigma = int(inp["tbt_slo_ns"][s])
+        if n > 0 and t_r[n] > sigma * n:
+            dec[s] = QUEUE_TBT
+            continue
+        # check 3: Eq. 4 for the scheduled requests, then the new one
+        dl = proj["deadline_at"][0]
+        if any(dl[j] != NO_DEADLINE and not t_r[j + 1] < int(dl[j]) for j in range(n)):
+            dec[s] = QUEUE_E2E
+            continue
+        if d_own != NO_DEADLINE and L <= H and not t_r[L] < int(d_own):
+            dec[s] = ADMIT_LOST
+            continue
+        dec[s] = ADMIT_OK
+    return dict(proj_all, decision=dec, ips=ips_all)

@@ -553,3 +553,132 @@ def test_selection_special_cases():
     dl[:, 3] = 4
     idx, stt = oracle.select(ips, dl, n, tbt, np.zeros(S, np.uint32))
     assert stt.tolist() == [1, 0, 1, 1]
+
+
+# ------------------------------------------ admission control (Sec. 4.3.2)
+
+def _admit_board(g, case):
+    sigma = case["sigma_ns"]
+    inp = goldens.scoreboard(g, deadline_ns=[sigma * r for r in g["remaining"]], lost=case.get("lost"))
+    if "kv_capacity" in case:
+        inp["kv_capacity"] = np.array([case["kv_capacity"]], np.int32)
+    if "batch_cap" in case:
+        inp["batch_cap"] = np.array([case["batch_cap"]], np.int32)
+    inp["tbt_slo_ns"] = np.array([sigma], np.uint64)
+    return inp
+
+
+def test_golden_admission():
+    g = goldens.load("admit_two_stumps.json")
+    forest = goldens.forest(g)
+    for case in g["cases"]:
+        inp = _admit_board(g, case)
+        d = case["cand_deadline"]
+        out = oracle.admit(inp, [case["cand_prompt"]], [case["cand_len"]],
+                           None if d is None else np.array([d], np.uint64), g["max_freq_mhz"], forest)
+        assert int(out["decision"][0]) == case["decision"], case["note"]
+        ex = g["expect_by_len"].get(str(case["cand_len"]))
+        if ex is not None and case["decision"] != oracle.QUEUE_CAPACITY:
+            assert out["kv"][0].tolist() == ex["kv"]
+            assert out["batch"][0].tolist() == ex["batch"]
+            assert out["ips"][0].tolist() == ex["ips"]
+
+
+def _random_admission(rng, queued):
+    H = int(rng.integers(4, 40))
+    N = int(rng.integers(1, 9))
+    R = int(rng.integers(0, 12))
+    inp = _inflight_board(rng, R, H, N, pmax=40, gmax=10, rmax=H + 6)
+    if queued and R:
+        q = rng.random(R) < 0.3
+        inp["arrival"] = np.where(q, np.sort(rng.integers(0, H, R)), -1).astype(np.int32)
+        inp["generated"] = np.where(q, 0, inp["generated"]).astype(np.int32)
+    p = int(rng.integers(0, 40))
+    L = int(rng.integers(1, H + 8))
+    sigma = int(rng.integers(5_000_000, 40_000_000))
+    inp["deadline_ns"] = (inp["remaining"] * sigma * rng.uniform(0.6, 1.6, R)).astype(np.uint64) + np.uint64(1)
+    inp["lost"] = (rng.random(R) < 0.1).astype(np.uint8)
+    kvmax = int(oracle.project(inp)["kv"].max()) if H else 0
+    margin = (p + L) // N + 2 if rng.random() < 0.75 else 0
+    inp["kv_capacity"] = np.array([kvmax + margin + int(rng.integers(-2, 4))], np.int32)
+    if rng.random() < 0.3:
+        inp["batch_cap"] = np.array([R + int(rng.integers(0, 3))], np.int32)
+    inp["tbt_slo_ns"] = np.array([sigma], np.uint64)
+    T, d = int(rng.integers(1, 5)), int(rng.integers(1, 4))
+    forest = dict(n_trees=T, depth=d, n_features=3, base_score=np.float32(30.0),
+                  feature=rng.integers(0, 3, (T, (1 << d) - 1)).astype(np.uint8),
+                  threshold=np.stack([rng.choice([1100.0, 1500.0, 1900.0, 50.0, 200.0, 2.0, 5.0, 9.0],
+                                                 (1 << d) - 1) for _ in range(T)]).astype(np.float32),
+                  leaf=rng.uniform(-20, 40, (T, 1 << d)).astype(np.float32))
+    dc = np.uint64(1 + sigma * L * rng.uniform(0.6, 1.6)) if rng.random() < 0.8 else NONE
+    return inp, forest, p, L, dc
+
+
+def _controller_feasible(inp, forest, p, L, dc, fmax):
+    """Check 2 and 3 by the controller's own selection (Sec. 4.5) on the board
+    with the query appended, at the single frequency fmax."""
+    R = int(inp["req_offset"][-1])
+    b = dict(inp)
+    b["req_offset"] = np.array([0, R + 1], np.int64)
+    for k, v in (("prompt", p), ("generated", 0), ("remaining", L), ("arrival", -1)):
+        b[k] = np.append(inp[k], np.int32(v)).astype(np.int32)
+    b["deadline_ns"] = np.append(inp["deadline_ns"], np.uint64(dc)).astype(np.uint64)
+    b["lost"] = np.append(inp["lost"], np.uint8(0)).astype(np.uint8)
+    proj = oracle.project(b)
+    x = oracle.rows(np.array([fmax], np.float32), proj["batch"], proj["kv"], None, 3)
+    ips = oracle.forest_predict(forest, x)
+    _, stt = oracle.select(ips, proj["deadline_at"], proj["n_iters"], inp["tbt_slo_ns"], None)
+    return int(stt[0]) == oracle.STATUS_OK, proj
+
+
+@pytest.mark.parametrize("queued", [False, True])
+def test_admission_agrees_with_controller_and_brute_force(queued):
+    """Checks 2-3 of the admission decision equal the controller's
+    feasibility at the maximum frequency (with and without the query's own
+    deadline); check 1 equals a brute-force maximum of Eq. 1 over the
+    requests running now."""
+    rng = np.random.default_rng(40 + queued)
+    seen = set()
+    fmax = 2000.0
+    for _ in range(150):
+        inp, forest, p, L, dc = _random_admission(rng, queued)
+        dec = int(oracle.admit(inp, [p], [L], np.array([dc], np.uint64), fmax, forest)["decision"][0])
+        seen.add(dec)
+        with_own, proj = _controller_feasible(inp, forest, p, L, dc, fmax)
+        without_own, _ = _controller_feasible(inp, forest, p, L, NONE, fmax)
+        H, N = int(inp["horizon"]), int(inp["block_tokens"])
+        running = [(int(a) + int(g), int(r)) for a, g, r, ar in
+                   zip(inp["prompt"], inp["generated"], inp["remaining"], inp["arrival"]) if ar == -1]
+        running.append((p, L))
+        kv_now = [sum(-(-(c + j) // N) for c, r in running if j < r) for j in range(H)]
+        over = max(kv_now) > int(inp["kv_capacity"][0])
+        bcap = inp.get("batch_cap")
+        over_b = bcap is not None and len(running) > int(bcap[0])
+        if dec == oracle.QUEUE_CAPACITY:
+            assert over or over_b
+            continue
+        assert not over and not over_b
+        if dec == oracle.ADMIT_OK:
+            assert with_own and without_own
+        elif dec == oracle.ADMIT_LOST:
+            assert without_own and not with_own and L <= H
+        else:
+            assert dec in (oracle.QUEUE_TBT, oracle.QUEUE_E2E) and not without_own
+    assert {oracle.ADMIT_OK, oracle.QUEUE_CAPACITY} <= seen and len(seen) >= 4, seen
+
+
+def test_admission_monotone_in_slo_and_own_deadline():
+    rng = np.random.default_rng(77)
+    fmax = 2000.0
+    changed = 0
+    for _ in range(120):
+        inp, forest, p, L, dc = _random_admission(rng, False)
+        d0 = int(oracle.admit(inp, [p], [L], np.array([dc], np.uint64), fmax, forest)["decision"][0])
+        loose = dict(inp, tbt_slo_ns=inp["tbt_slo_ns"] * np.uint64(2))
+        d1 = int(oracle.admit(loose, [p], [L], np.array([dc], np.uint64), fmax, forest)["decision"][0])
+        # a looser TBT SLO (deadlines unchanged) only lifts a TBT queueing
+        assert d1 == d0 or d0 == oracle.QUEUE_TBT
+        changed += d1 != d0
+        later = NONE if dc == NONE else np.uint64(int(dc) + 50_000_000)
+        d2 = int(oracle.admit(inp, [p], [L], np.array([later], np.uint64), fmax, forest)["decision"][0])
+        assert d2 == d0 or (d0 == oracle.ADMIT_LOST and d2 == oracle.ADMIT_OK)
