@@ -14,6 +14,8 @@
  *                     lowest frequency whose predicted per-iteration times
  *                     pass the TBT check and the E2E deadlines (Sec. 4.3.2,
  *                     checks 2 and 3, Eq. 3-4).
+ * and, from the same stages, tl_admit: the admission control of Sec. 4.3.2
+ * for one new query per scenario.
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers (memory of the device that is current on
@@ -69,12 +71,28 @@ typedef enum tl_status {
                                    could overflow; outputs are zero / no deadline  */
 #define TL_FLAG_UNSORTED   16u  /* queued entries are not in non-decreasing arrival
                                    order; the queue is still served in array order */
+#define TL_FLAG_BAD_CANDIDATE 32u /* tl_admit only: the new query is malformed
+                                   (prompt < 0 or > 2^30, length < 1) and was left
+                                   out of the projection */
 
 /* Per-scenario status written by tl_select_freq. */
 #define TL_STATUS_OK         0u  /* freq_idx is the lowest feasible index           */
 #define TL_STATUS_INFEASIBLE 1u  /* no frequency passes; freq_idx = F-1            */
 #define TL_STATUS_LOST       2u  /* a lost request forces the maximum; freq_idx = F-1 */
 #define TL_STATUS_INVALID    3u  /* scenario flagged TL_FLAG_OVERFLOW; freq_idx = F-1 */
+
+/* Per-scenario decision written by tl_admit (Sec. 4.3.2). */
+#define TL_ADMIT_OK             0u  /* checks 1-3 pass: schedule the query            */
+#define TL_ADMIT_LOST           1u  /* only its own deadline fails: schedule it and
+                                       mark it lost                                   */
+#define TL_ADMIT_QUEUE_CAPACITY 2u  /* check 1: a projected KV value exceeds the
+                                       capacity, or the batch running now exceeds
+                                       the batch cap -> queue                         */
+#define TL_ADMIT_QUEUE_TBT      3u  /* check 2: mean TBT at the maximum frequency
+                                       exceeds the SLO -> queue                       */
+#define TL_ADMIT_QUEUE_E2E      4u  /* check 3: a scheduled request would miss its
+                                       deadline (Eq. 4) -> queue                      */
+#define TL_ADMIT_INVALID        5u  /* malformed query or scenario not projected     */
 
 /* Per-iteration time that stands for "no progress" (IPS <= 0, NaN, or
  * 1e9/IPS >= 2^40 ns). */
@@ -221,6 +239,52 @@ tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs,
                          const uint64_t* deadline_at, const int32_t* n_iters,
                          const uint64_t* tbt_slo_ns, const uint32_t* proj_flags,
                          int32_t* freq_idx, uint32_t* status, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Admission control (Sec. 4.3.2) for one new query per scenario, as a batch
+ * of what-ifs: the projection of tl_project on the scenario's scoreboard with
+ * the query appended as a request that starts now (prompt cand_prompt[s],
+ * nothing generated, active for the cand_len[s] iterations [0, L); queued and
+ * arriving entries keep their FIFO admission behind it), the model at
+ * max_freq_mhz on every projected iteration, and the paper's three checks in
+ * order (the first failure decides):
+ *   1. some projected KV value exceeds kv_capacity, or the batch running now
+ *      exceeds batch_cap                         -> TL_ADMIT_QUEUE_CAPACITY
+ *   2. with n = n_iters[s] and T_R as in tl_select_freq (Eq. 3),
+ *      T_R[n] > tbt_slo_ns[s] * n (mean TBT)     -> TL_ADMIT_QUEUE_TBT
+ *   3. T_R[e] < deadline fails for a scheduled, non-lost request ending at
+ *      e <= H (Eq. 4)                            -> TL_ADMIT_QUEUE_E2E
+ *      else, when L <= H and cand_deadline_ns[s] is set, T_R[L] <
+ *      cand_deadline_ns[s] fails                 -> TL_ADMIT_LOST
+ *   otherwise                                    -> TL_ADMIT_OK
+ * A malformed query (flag TL_FLAG_BAD_CANDIDATE) or a scenario flagged
+ * TL_FLAG_OVERFLOW gives TL_ADMIT_INVALID.
+ *
+ * `proj` describes the scoreboards and receives the projection with the query
+ * (batch, kv, deadline_at without the query's deadline, n_iters, flags);
+ * its rows, n_freqs, freqs_mhz and n_features are ignored.  engine_size [S]
+ * is read for 4-feature forests.  ips [S][H] receives M at max_freq_mhz (rows
+ * of scenarios flagged TL_FLAG_OVERFLOW hold M on the zero curves).  All
+ * arrays are device arrays of the caller; the call allocates nothing.
+ * Errors as for tl_project, plus a NULL forest, ips, decision, tbt_slo_ns,
+ * cand_prompt or cand_len, or a forest without 3 or 4 features: TL_EINVAL.
+ * ---------------------------------------------------------------------- */
+typedef struct tl_admit_args {
+    uint32_t struct_size;              /* sizeof(tl_admit_args) */
+    uint32_t reserved;
+    tl_project_args proj;              /* scoreboards; projection outputs */
+    const tl_forest* forest;
+    float max_freq_mhz;                /* the maximum available frequency */
+    const float* engine_size;          /* [S], 4-feature forests */
+    const uint64_t* tbt_slo_ns;        /* [S] */
+    const int32_t* cand_prompt;        /* [S] prompt tokens of the new query */
+    const int32_t* cand_len;           /* [S] its predicted length, >= 1 */
+    const uint64_t* cand_deadline_ns;  /* [S] t_dead - t_cur; NULL or TL_NO_DEADLINE = none */
+    float* ips;                        /* out [S][H] */
+    uint32_t* decision;                /* out [S], TL_ADMIT_* */
+} tl_admit_args;
+
+tl_status tl_admit(const tl_admit_args* args, void* stream);
 
 #ifdef __cplusplus
 }

@@ -16,11 +16,13 @@ i32, i64, u32, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_f
 
 TL_OK, TL_EINVAL, TL_ENOMEM, TL_EDEVICE, TL_EUNSUPPORTED = 0, 1, 2, 3, 4
 FLAG_BAD_REQUEST, FLAG_LOST, FLAG_OVERCOMMIT, FLAG_OVERFLOW, FLAG_UNSORTED = 1, 2, 4, 8, 16
+FLAG_BAD_CANDIDATE = 32
 STATUS_OK, STATUS_INFEASIBLE, STATUS_LOST, STATUS_INVALID = 0, 1, 2, 3
+ADMIT_OK, ADMIT_LOST, ADMIT_QUEUE_CAPACITY, ADMIT_QUEUE_TBT, ADMIT_QUEUE_E2E, ADMIT_INVALID = 0, 1, 2, 3, 4, 5
 MAX_HORIZON, MAX_BLOCK_TOKENS, MAX_FREQS, MAX_FEATURES, MAX_DEPTH = 8192, 65536, 4096, 4, 14
 
 EXPORTED = ("tl_abi_version", "tl_last_error", "tl_forest_create", "tl_forest_destroy",
-            "tl_project", "tl_forest_predict", "tl_forest_predict_grid", "tl_select_freq")
+            "tl_project", "tl_forest_predict", "tl_forest_predict_grid", "tl_select_freq", "tl_admit")
 
 
 class ProjectArgs(ctypes.Structure):
@@ -31,6 +33,14 @@ class ProjectArgs(ctypes.Structure):
         ("arrival_iter", P), ("deadline_ns", P), ("lost", P), ("kv_capacity", P),
         ("batch_cap", P), ("batch", P), ("kv", P), ("deadline_at", P), ("n_iters", P),
         ("flags", P), ("freqs_mhz", P), ("engine_size", P), ("rows", P),
+    ]
+
+
+class AdmitArgs(ctypes.Structure):
+    _fields_ = [
+        ("struct_size", u32), ("reserved", u32), ("proj", ProjectArgs), ("forest", P),
+        ("max_freq_mhz", f32), ("engine_size", P), ("tbt_slo_ns", P), ("cand_prompt", P),
+        ("cand_len", P), ("cand_deadline_ns", P), ("ips", P), ("decision", P),
     ]
 
 
@@ -70,6 +80,8 @@ def lib():
     L.tl_forest_predict_grid.restype = ctypes.c_int
     L.tl_select_freq.argtypes = [P, i64, i32, i32, P, P, P, P, P, P, P]
     L.tl_select_freq.restype = ctypes.c_int
+    L.tl_admit.argtypes = [ctypes.POINTER(AdmitArgs), P]
+    L.tl_admit.restype = ctypes.c_int
     _lib = L
     return L
 

@@ -42,13 +42,10 @@ def _opt(t, dtype, name, shape=None):
     return None if t is None else _need(t, dtype, name, shape)
 
 
-def tl_project(req_offset, prompt_len, generated, remaining, arrival_iter, kv_capacity,
-               horizon, block_tokens, deadline_ns=None, lost=None, batch_cap=None,
-               freqs_mhz=None, engine_size=None, n_features=3, want_rows=True, out=None):
-    """Stage 1 (tl_project).  Returns a dict of device tensors:
-    batch, kv [S,H] int32; deadline_at [S,H] int64 (uint64 bits); n_iters [S]
-    int32; flags [S] int32 (uint32 bits); rows [S,F,H,n_features] fp32 when
-    ``want_rows`` and ``freqs_mhz`` is given."""
+def _project_args(req_offset, prompt_len, generated, remaining, arrival_iter, kv_capacity,
+                  horizon, block_tokens, deadline_ns, lost, batch_cap, out):
+    """Checked tl_project_args for the scoreboards, with the curve outputs
+    (taken from ``out`` or allocated).  Returns (args, outputs)."""
     _need(req_offset, torch.int64, "req_offset")
     S = req_offset.numel() - 1
     R = prompt_len.numel()
@@ -61,35 +58,21 @@ def tl_project(req_offset, prompt_len, generated, remaining, arrival_iter, kv_ca
     _opt(batch_cap, torch.int32, "batch_cap", (S,))
     H = int(horizon)
     dev = req_offset.device
-    rows_on = bool(want_rows and freqs_mhz is not None)
-    F = int(freqs_mhz.numel()) if rows_on else 0
-    if rows_on:
-        _need(freqs_mhz, torch.float32, "freqs_mhz", (F,))
-        if n_features == 4:
-            _need(engine_size, torch.float32, "engine_size", (S,))
     o = out or {}
-    batch = o.get("batch") if o.get("batch") is not None else torch.empty((S, H), dtype=torch.int32, device=dev)
-    kv = o.get("kv") if o.get("kv") is not None else torch.empty((S, H), dtype=torch.int32, device=dev)
-    dl = o.get("deadline_at") if o.get("deadline_at") is not None else torch.empty((S, H), dtype=torch.int64, device=dev)
-    n_iters = o.get("n_iters") if o.get("n_iters") is not None else torch.empty(S, dtype=torch.int32, device=dev)
-    flags = o.get("flags") if o.get("flags") is not None else torch.empty(S, dtype=torch.int32, device=dev)
-    rows = None
-    if rows_on:
-        rows = o.get("rows") if o.get("rows") is not None else torch.empty((S, F, H, n_features), dtype=torch.float32, device=dev)
-        _need(rows, torch.float32, "rows", (S, F, H, n_features))
-    _need(batch, torch.int32, "batch", (S, H))
-    _need(kv, torch.int32, "kv", (S, H))
-    _need(dl, torch.int64, "deadline_at", (S, H))
-    _need(n_iters, torch.int32, "n_iters", (S,))
-    _need(flags, torch.int32, "flags", (S,))
+
+    def buf(name, shape, dtype):
+        t = o.get(name) if o.get(name) is not None else torch.empty(shape, dtype=dtype, device=dev)
+        return _need(t, dtype, name, shape)
+
+    res = dict(batch=buf("batch", (S, H), torch.int32), kv=buf("kv", (S, H), torch.int32),
+               deadline_at=buf("deadline_at", (S, H), torch.int64), n_iters=buf("n_iters", (S,), torch.int32),
+               flags=buf("flags", (S,), torch.int32))
     a = _lib.ProjectArgs()
     a.struct_size = ctypes.sizeof(_lib.ProjectArgs)
     a.horizon = H
     a.n_scenarios = S
     a.n_requests = R
     a.block_tokens = int(block_tokens)
-    a.n_freqs = F
-    a.n_features = int(n_features) if rows_on else 0
     a.req_offset = _p(req_offset)
     a.prompt_len = _p(prompt_len)
     a.generated = _p(generated)
@@ -99,14 +82,72 @@ def tl_project(req_offset, prompt_len, generated, remaining, arrival_iter, kv_ca
     a.lost = _p(lost)
     a.kv_capacity = _p(kv_capacity)
     a.batch_cap = _p(batch_cap)
-    a.batch, a.kv, a.deadline_at, a.n_iters, a.flags = _p(batch), _p(kv), _p(dl), _p(n_iters), _p(flags)
-    a.freqs_mhz = _p(freqs_mhz) if rows_on else None
-    a.engine_size = _p(engine_size) if rows_on else None
-    a.rows = _p(rows)
-    check(lib().tl_project(ctypes.byref(a), _stream()))
-    res = dict(batch=batch, kv=kv, deadline_at=dl, n_iters=n_iters, flags=flags)
+    a.batch, a.kv, a.deadline_at = _p(res["batch"]), _p(res["kv"]), _p(res["deadline_at"])
+    a.n_iters, a.flags = _p(res["n_iters"]), _p(res["flags"])
+    return a, res
+
+
+def tl_project(req_offset, prompt_len, generated, remaining, arrival_iter, kv_capacity,
+               horizon, block_tokens, deadline_ns=None, lost=None, batch_cap=None,
+               freqs_mhz=None, engine_size=None, n_features=3, want_rows=True, out=None):
+    """Stage 1 (tl_project).  Returns a dict of device tensors:
+    batch, kv [S,H] int32; deadline_at [S,H] int64 (uint64 bits); n_iters [S]
+    int32; flags [S] int32 (uint32 bits); rows [S,F,H,n_features] fp32 when
+    ``want_rows`` and ``freqs_mhz`` is given."""
+    a, res = _project_args(req_offset, prompt_len, generated, remaining, arrival_iter, kv_capacity,
+                           horizon, block_tokens, deadline_ns, lost, batch_cap, out)
+    S, H = int(a.n_scenarios), int(a.horizon)
+    rows_on = bool(want_rows and freqs_mhz is not None)
     if rows_on:
+        F = int(freqs_mhz.numel())
+        _need(freqs_mhz, torch.float32, "freqs_mhz", (F,))
+        if n_features == 4:
+            _need(engine_size, torch.float32, "engine_size", (S,))
+        o = out or {}
+        rows = o.get("rows")
+        if rows is None:
+            rows = torch.empty((S, F, H, n_features), dtype=torch.float32, device=req_offset.device)
+        _need(rows, torch.float32, "rows", (S, F, H, n_features))
+        a.n_freqs, a.n_features = F, int(n_features)
+        a.freqs_mhz, a.engine_size, a.rows = _p(freqs_mhz), _p(engine_size), _p(rows)
         res["rows"] = rows
+    check(lib().tl_project(ctypes.byref(a), _stream()))
+    return res
+
+
+def tl_admit(forest, max_freq_mhz, tbt_slo_ns, cand_prompt, cand_len, req_offset, prompt_len, generated,
+             remaining, arrival_iter, kv_capacity, horizon, block_tokens, deadline_ns=None, lost=None,
+             batch_cap=None, engine_size=None, cand_deadline_ns=None, out=None):
+    """Admission control (tl_admit) for one new query per scenario.  Returns
+    the projection with the query (batch, kv, deadline_at, n_iters, flags as
+    in tl_project), ips [S,H] fp32 at max_freq_mhz and decision [S] int32
+    (TL_ADMIT_* codes)."""
+    a, res = _project_args(req_offset, prompt_len, generated, remaining, arrival_iter, kv_capacity,
+                           horizon, block_tokens, deadline_ns, lost, batch_cap, out)
+    S, H = int(a.n_scenarios), int(a.horizon)
+    dev = req_offset.device
+    _need(tbt_slo_ns, torch.int64, "tbt_slo_ns", (S,))
+    _need(cand_prompt, torch.int32, "cand_prompt", (S,))
+    _need(cand_len, torch.int32, "cand_len", (S,))
+    _opt(cand_deadline_ns, torch.int64, "cand_deadline_ns", (S,))
+    if forest.n_features == 4:
+        _need(engine_size, torch.float32, "engine_size", (S,))
+    o = out or {}
+    ips = o.get("ips") if o.get("ips") is not None else torch.empty((S, H), dtype=torch.float32, device=dev)
+    dec = o.get("decision") if o.get("decision") is not None else torch.empty(S, dtype=torch.int32, device=dev)
+    _need(ips, torch.float32, "ips", (S, H))
+    _need(dec, torch.int32, "decision", (S,))
+    b = _lib.AdmitArgs()
+    b.struct_size = ctypes.sizeof(_lib.AdmitArgs)
+    b.proj = a
+    b.forest = forest._h
+    b.max_freq_mhz = float(max_freq_mhz)
+    b.engine_size = _p(engine_size) if forest.n_features == 4 else None
+    b.tbt_slo_ns = _p(tbt_slo_ns)
+    b.cand_prompt, b.cand_len, b.cand_deadline_ns = _p(cand_prompt), _p(cand_len), _p(cand_deadline_ns)
+    b.ips, b.decision = _p(ips), _p(dec)
+    check(lib().tl_admit(ctypes.byref(b), _stream()))
+    res.update(ips=ips, decision=dec)
     return res
 
 
@@ -207,6 +248,7 @@ def tl_select_freq(ips, deadline_at, n_iters, tbt_slo_ns, proj_flags=None, out=N
 # short names
 project = tl_project
 select_freq = tl_select_freq
+admit = tl_admit
 
 
 def upload(inp, device="cuda"):

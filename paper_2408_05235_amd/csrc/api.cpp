@@ -237,61 +237,126 @@ void tl_forest_destroy(tl_forest* f) {
     delete f;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Host checks of a projection request and its translation to kernel
+// parameters; `who` prefixes messages.  Rows are only looked at when
+// `with_rows` (tl_admit ignores them).
+tl_status project_params(const tl_project_args* a, const char* who, bool with_rows, tl::ProjectParams* p) {
+    if (a->struct_size < sizeof(tl_project_args))
+        return fail(TL_EINVAL, "%s: struct_size %u < %zu", who, a->struct_size, sizeof(tl_project_args));
+    if (a->n_scenarios < 0 || a->n_scenarios > 0x7fffffffll)
+        return fail(TL_EINVAL, "%s: n_scenarios %lld outside [0, 2^31-1]", who, (long long)a->n_scenarios);
+    if (a->horizon < 1 || a->horizon > TL_MAX_HORIZON)
+        return fail(TL_EINVAL, "%s: horizon %d outside [1, %d]", who, a->horizon, TL_MAX_HORIZON);
+    if (a->block_tokens < 1 || a->block_tokens > TL_MAX_BLOCK_TOKENS)
+        return fail(TL_EINVAL, "%s: block_tokens %d outside [1, %d]", who, a->block_tokens, TL_MAX_BLOCK_TOKENS);
+    if (a->n_requests < 0) return fail(TL_EINVAL, "%s: n_requests < 0", who);
+    if (!a->req_offset || !a->kv_capacity || !a->batch || !a->kv || !a->deadline_at || !a->n_iters || !a->flags)
+        return fail(TL_EINVAL, "%s: NULL required pointer", who);
+    if (a->n_requests > 0 && (!a->prompt_len || !a->generated || !a->remaining || !a->arrival_iter))
+        return fail(TL_EINVAL, "%s: NULL request array", who);
+    const bool rows = with_rows && a->rows;
+    if (rows) {
+        if (a->n_freqs < 1 || a->n_freqs > TL_MAX_FREQS)
+            return fail(TL_EINVAL, "%s: n_freqs %d outside [1, %d]", who, a->n_freqs, TL_MAX_FREQS);
+        if (a->n_features != 3 && a->n_features != 4)
+            return fail(TL_EINVAL, "%s: n_features %d is not 3 or 4", who, a->n_features);
+        if (!a->freqs_mhz) return fail(TL_EINVAL, "%s: rows requested without freqs_mhz", who);
+        if (a->n_features == 4 && !a->engine_size) return fail(TL_EINVAL, "%s: 4 features need engine_size", who);
+        if (a->n_features == 4 && ((uintptr_t)a->rows & 15u))
+            return fail(TL_EINVAL, "%s: rows must be 16-byte aligned for 4 features", who);
+    }
+    *p = tl::ProjectParams{};
+    p->n_scenarios = a->n_scenarios;
+    p->n_requests = a->n_requests;
+    p->H = a->horizon;
+    p->N = a->block_tokens;
+    const tl::DivU32 dv = tl::make_divu32((uint32_t)a->block_tokens);
+    p->div_m = dv.m;
+    p->div_l = dv.l;
+    p->off = a->req_offset;
+    p->prompt = a->prompt_len;
+    p->gen = a->generated;
+    p->rem = a->remaining;
+    p->arr = a->arrival_iter;
+    p->deadline = a->deadline_ns;
+    p->lost = a->lost;
+    p->kv_cap = a->kv_capacity;
+    p->batch_cap = a->batch_cap;
+    p->batch = a->batch;
+    p->kv = a->kv;
+    p->deadline_at = a->deadline_at;
+    p->n_iters = a->n_iters;
+    p->flags = a->flags;
+    p->rows = rows ? a->rows : nullptr;
+    p->F = rows ? a->n_freqs : 0;
+    p->nf = rows ? a->n_features : 0;
+    p->freqs = rows ? a->freqs_mhz : nullptr;
+    p->engine = rows ? a->engine_size : nullptr;
+    p->cand_prompt = nullptr;
+    p->cand_len = nullptr;
+    return TL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 tl_status tl_project(const tl_project_args* a, void* stream) {
     if (!a) return fail(TL_EINVAL, "tl_project: args is NULL");
-    if (a->struct_size < sizeof(tl_project_args))
-        return fail(TL_EINVAL, "tl_project: struct_size %u < %zu", a->struct_size, sizeof(tl_project_args));
-    if (a->n_scenarios < 0 || a->n_scenarios > 0x7fffffffll)
-        return fail(TL_EINVAL, "tl_project: n_scenarios %lld outside [0, 2^31-1]", (long long)a->n_scenarios);
-    if (a->horizon < 1 || a->horizon > TL_MAX_HORIZON)
-        return fail(TL_EINVAL, "tl_project: horizon %d outside [1, %d]", a->horizon, TL_MAX_HORIZON);
-    if (a->block_tokens < 1 || a->block_tokens > TL_MAX_BLOCK_TOKENS)
-        return fail(TL_EINVAL, "tl_project: block_tokens %d outside [1, %d]", a->block_tokens, TL_MAX_BLOCK_TOKENS);
-    if (a->n_requests < 0) return fail(TL_EINVAL, "tl_project: n_requests < 0");
-    if (!a->req_offset || !a->kv_capacity || !a->batch || !a->kv || !a->deadline_at || !a->n_iters || !a->flags)
-        return fail(TL_EINVAL, "tl_project: NULL required pointer");
-    if (a->n_requests > 0 && (!a->prompt_len || !a->generated || !a->remaining || !a->arrival_iter))
-        return fail(TL_EINVAL, "tl_project: NULL request array");
-    if (a->rows) {
-        if (a->n_freqs < 1 || a->n_freqs > TL_MAX_FREQS)
-            return fail(TL_EINVAL, "tl_project: n_freqs %d outside [1, %d]", a->n_freqs, TL_MAX_FREQS);
-        if (a->n_features != 3 && a->n_features != 4)
-            return fail(TL_EINVAL, "tl_project: n_features %d is not 3 or 4", a->n_features);
-        if (!a->freqs_mhz) return fail(TL_EINVAL, "tl_project: rows requested without freqs_mhz");
-        if (a->n_features == 4 && !a->engine_size)
-            return fail(TL_EINVAL, "tl_project: 4 features need engine_size");
-        if (a->n_features == 4 && ((uintptr_t)a->rows & 15u))
-            return fail(TL_EINVAL, "tl_project: rows must be 16-byte aligned for 4 features");
-    }
+    tl::ProjectParams p;
+    const tl_status st = project_params(a, "tl_project", true, &p);
+    if (st != TL_OK) return st;
     if (a->n_scenarios == 0) return ok();
-    tl::ProjectParams p{};
-    p.n_scenarios = a->n_scenarios;
-    p.n_requests = a->n_requests;
-    p.H = a->horizon;
-    p.N = a->block_tokens;
-    const tl::DivU32 dv = tl::make_divu32((uint32_t)a->block_tokens);
-    p.div_m = dv.m;
-    p.div_l = dv.l;
-    p.off = a->req_offset;
-    p.prompt = a->prompt_len;
-    p.gen = a->generated;
-    p.rem = a->remaining;
-    p.arr = a->arrival_iter;
-    p.deadline = a->deadline_ns;
-    p.lost = a->lost;
-    p.kv_cap = a->kv_capacity;
-    p.batch_cap = a->batch_cap;
-    p.batch = a->batch;
-    p.kv = a->kv;
-    p.deadline_at = a->deadline_at;
-    p.n_iters = a->n_iters;
-    p.flags = a->flags;
-    p.rows = a->rows;
-    p.F = a->rows ? a->n_freqs : 0;
-    p.nf = a->rows ? a->n_features : 0;
-    p.freqs = a->freqs_mhz;
-    p.engine = a->engine_size;
     return from_hip(tl::launch_project(p, (hipStream_t)stream), "tl_project: launch");
+}
+
+tl_status tl_admit(const tl_admit_args* a, void* stream) {
+    if (!a) return fail(TL_EINVAL, "tl_admit: args is NULL");
+    if (a->struct_size < sizeof(tl_admit_args))
+        return fail(TL_EINVAL, "tl_admit: struct_size %u < %zu", a->struct_size, sizeof(tl_admit_args));
+    tl::ProjectParams p;
+    const tl_status st = project_params(&a->proj, "tl_admit", false, &p);
+    if (st != TL_OK) return st;
+    const tl_forest* f = a->forest;
+    if (!f) return fail(TL_EINVAL, "tl_admit: forest is NULL");
+    if (f->dev.n_features != 3 && f->dev.n_features != 4)
+        return fail(TL_EINVAL, "tl_admit: the forest has %d features, admission needs 3 or 4", f->dev.n_features);
+    if (f->dev.n_features == 4 && !a->engine_size) return fail(TL_EINVAL, "tl_admit: 4 features need engine_size");
+    if (!a->tbt_slo_ns || !a->cand_prompt || !a->cand_len || !a->ips || !a->decision)
+        return fail(TL_EINVAL, "tl_admit: NULL required pointer");
+    const int64_t S = a->proj.n_scenarios;
+    if (S == 0) return ok();
+    const hipStream_t st_h = (hipStream_t)stream;
+    p.cand_prompt = a->cand_prompt;
+    p.cand_len = a->cand_len;
+    hipError_t e = tl::launch_project(p, st_h);
+    if (e != hipSuccess) return from_hip(e, "tl_admit: projection launch");
+    tl::ColumnParams c{};
+    c.S = S;
+    c.H = a->proj.horizon;
+    c.kv = a->proj.kv;
+    c.batch = a->proj.batch;
+    c.freq = a->max_freq_mhz;
+    c.engine = a->engine_size;
+    c.out = a->ips;
+    e = tl::launch_forest_column(f->dev, c, st_h);
+    if (e != hipSuccess) return from_hip(e, "tl_admit: model launch");
+    tl::AdmitParams d{};
+    d.ips = a->ips;
+    d.S = S;
+    d.H = a->proj.horizon;
+    d.deadline_at = a->proj.deadline_at;
+    d.n_iters = a->proj.n_iters;
+    d.tbt_slo_ns = a->tbt_slo_ns;
+    d.proj_flags = a->proj.flags;
+    d.cand_len = a->cand_len;
+    d.cand_deadline = a->cand_deadline_ns;
+    d.decision = a->decision;
+    return from_hip(tl::launch_admit(d, st_h), "tl_admit: decision launch");
 }
 
 tl_status tl_forest_predict(const tl_forest* f, const float* rows, int64_t n_rows, float* out, void* stream) {

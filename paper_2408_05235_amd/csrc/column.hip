@@ -1,0 +1,212 @@
+// The model M (Sec. 4.3.1) at one frequency per scenario on the projection
+// grid: out[s][j] = M(f_s, KV[s][j], B[s][j] [, E_s]).  This is the query of
+// the admission checks (Sec. 4.3.2 check 2 asks M at the maximum frequency
+// for every projected iteration) and of one probe of a search over
+// frequencies (Sec. 4.5).
+//
+// A wavefront takes 64 consecutive iterations of one scenario, one row per
+// lane; the rows differ, so every lane walks every tree (the grid kernel's
+// leaf reuse needs many frequencies on the same row sequence).  Sixteen
+// wavefronts of a workgroup share double-buffered blocks of tree records in
+// LDS, loaded into registers while the current block is evaluated and stored
+// after it.  The walks of up to four trees interleave, so their chains of
+// dependent LDS reads overlap.  Leaves are accumulated in fp64 in tree order
+// and rounded once, as everywhere in the library.
+//
+// Forests too deep for LDS records are walked from global memory.
+#include <algorithm>
+
+#include "device_util.h"
+#include "tl_internal.h"
+#include "forest_walk.h"
+
+namespace tl {
+namespace {
+
+constexpr int kColWaves = 16;
+constexpr int kColThreads = kColWaves * kWave;
+constexpr int kColStage = 8;                       // staged 16-byte words per thread per block
+constexpr size_t kColLdsBudget = 152 * 1024;
+
+struct ColumnItem {
+    int64_t s;
+    int32_t j;          // this lane's iteration
+    bool valid;         // the wavefront has a scenario
+    bool row;           // this lane's row is inside the horizon
+};
+
+__device__ __forceinline__ ColumnItem column_item(const ColumnParams& P, int64_t item) {
+    const int32_t n_cols = (P.H + kWave - 1) / kWave;
+    ColumnItem c;
+    c.valid = item < P.S * n_cols;
+    c.s = c.valid ? item / n_cols : 0;
+    const int32_t j = (int32_t)(item % n_cols) * kWave + lane_id();
+    c.row = c.valid && j < P.H;
+    c.j = min(j, P.H - 1);
+    return c;
+}
+
+__device__ __forceinline__ float column_freq(const ColumnParams& P, int64_t s) {
+    return P.fidx ? P.freqs[P.fidx[s]] : P.freq;
+}
+
+template <int NF, int NT>
+__device__ __forceinline__ void add_leaves(const unsigned char* smem, uint32_t tree, const RecordLayout& R,
+                                           int32_t depth, float xf, float kv, float bs, float xe, double& acc) {
+    int32_t k[NT];
+    walk<NF, NT>(lds_addr(smem) + tree, R.bytes, depth, xf, kv, bs, xe, k);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc += (double)((const float*)(smem + tree + t * R.bytes + R.vals))[k[t]];
+}
+
+template <int NF>
+__global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const uint4* __restrict__ records,
+                                                                       int32_t n_trees, int32_t depth, int32_t tb,
+                                                                       float base, ColumnParams P) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const RecordLayout R = record_layout(depth);
+    const uint32_t rec_words = R.bytes / 16u;
+    const uint32_t buf_bytes = (uint32_t)tb * R.bytes;
+    const int wave = threadIdx.x / kWave;
+    const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kColWaves + wave);
+    const ColumnItem c = column_item(P, item);
+    const float xf = column_freq(P, c.s);
+    const float xe = NF == 4 ? P.engine[c.s] : 0.0f;
+    const float kv = (float)P.kv[c.s * P.H + c.j];
+    const float bs = (float)P.batch[c.s * P.H + c.j];
+    double acc = (double)base;
+
+    const int32_t n_blocks = (n_trees + tb - 1) / tb;
+    // block b: trees [b*tb, b*tb + cnt), one contiguous range of words; each
+    // thread moves word threadIdx.x + r * kColThreads through register st<r>
+    static_assert(kColStage == 8, "staging below names eight registers");
+    uint4 st0 = make_uint4(0, 0, 0, 0), st1 = st0, st2 = st0, st3 = st0, st4 = st0, st5 = st0, st6 = st0, st7 = st0;
+#define TL_COL_FETCH_WORD(r, reg)                                              \
+    {                                                                          \
+        const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
+        reg = src[i < words ? i : 0];                                          \
+    }
+#define TL_COL_FETCH(b)                                                        \
+    {                                                                          \
+        const uint32_t words = (uint32_t)min(tb, n_trees - (b) * tb) * rec_words; \
+        const uint4* src = records + (int64_t)(b) * tb * rec_words;            \
+        TL_COL_FETCH_WORD(0, st0) TL_COL_FETCH_WORD(1, st1)                    \
+        TL_COL_FETCH_WORD(2, st2) TL_COL_FETCH_WORD(3, st3)                    \
+        TL_COL_FETCH_WORD(4, st4) TL_COL_FETCH_WORD(5, st5)                    \
+        TL_COL_FETCH_WORD(6, st6) TL_COL_FETCH_WORD(7, st7)                    \
+    }
+#define TL_COL_STORE_WORD(r, reg)                                              \
+    {                                                                          \
+        const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
+        if (i < words) dst[i] = reg;                                           \
+    }
+#define TL_COL_STORE(b, buf)                                                   \
+    {                                                                          \
+        const uint32_t words = (uint32_t)min(tb, n_trees - (b) * tb) * rec_words; \
+        uint4* dst = (uint4*)(smem + (buf) * buf_bytes);                       \
+        TL_COL_STORE_WORD(0, st0) TL_COL_STORE_WORD(1, st1)                    \
+        TL_COL_STORE_WORD(2, st2) TL_COL_STORE_WORD(3, st3)                    \
+        TL_COL_STORE_WORD(4, st4) TL_COL_STORE_WORD(5, st5)                    \
+        TL_COL_STORE_WORD(6, st6) TL_COL_STORE_WORD(7, st7)                    \
+    }
+    // the row is complete before any staging load is in flight
+    asm volatile("" ::"v"(xf), "v"(xe), "v"(kv), "v"(bs));
+    if (n_blocks > 0) {
+        TL_COL_FETCH(0)
+        TL_COL_STORE(0, 0)
+    }
+    __syncthreads();
+    for (int32_t b = 0; b < n_blocks; ++b) {
+        const int cur = b & 1;
+        if (b + 1 < n_blocks) TL_COL_FETCH(b + 1)
+        if (c.valid) {
+            const int32_t cnt = min(tb, n_trees - b * tb);
+            const uint32_t base_off = cur * buf_bytes;
+            int32_t t = 0;
+            for (; t + 4 <= cnt; t += 4) add_leaves<NF, 4>(smem, base_off + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
+            if (t + 2 <= cnt) {
+                add_leaves<NF, 2>(smem, base_off + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
+                t += 2;
+            }
+            if (t < cnt) add_leaves<NF, 1>(smem, base_off + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
+        }
+        if (b + 1 < n_blocks) TL_COL_STORE(b + 1, cur ^ 1)
+        __syncthreads();
+    }
+#undef TL_COL_STORE
+#undef TL_COL_STORE_WORD
+#undef TL_COL_FETCH
+#undef TL_COL_FETCH_WORD
+    if (c.row) P.out[c.s * P.H + c.j] = (float)acc;
+}
+
+// Global-memory walks for forests without LDS records.
+template <int NF>
+__global__ __launch_bounds__(256) void forest_column_global_kernel(const uint2* __restrict__ nodes,
+                                                                  const float* __restrict__ leaves,
+                                                                  int32_t n_trees, int32_t depth, float base,
+                                                                  ColumnParams P) {
+    const int64_t item = (int64_t)blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
+    const ColumnItem c = column_item(P, item);
+    if (!c.row) return;
+    float x[4];
+    x[0] = column_freq(P, c.s);
+    x[1] = (float)P.kv[c.s * P.H + c.j];
+    x[2] = (float)P.batch[c.s * P.H + c.j];
+    x[3] = NF == 4 ? P.engine[c.s] : 0.0f;
+    const int64_t stride = (int64_t)1 << depth;
+    const int32_t n_int = (1 << depth) - 1;
+    double acc = (double)base;
+    for (int32_t t = 0; t < n_trees; ++t) {
+        const uint2* nd = nodes + t * stride;
+        int32_t k = 0;
+        for (int32_t level = 0; level < depth; ++level) {
+            const uint2 w = nd[k];
+            const float v = x[w.y & 3u];
+            k = 2 * k + (v < __uint_as_float(w.x) ? 1 : 2);
+        }
+        acc += (double)leaves[t * stride + (k - n_int)];
+    }
+    P.out[c.s * P.H + c.j] = (float)acc;
+}
+
+// Trees per staged block: double buffers within the LDS budget, and no more
+// words per block than the staging registers of one workgroup hold.
+int32_t column_trees_per_block(const ForestDev& f, size_t* lds) {
+    if (!f.records || f.n_trees == 0) return 0;
+    const RecordLayout R = record_layout(f.depth);
+    const int64_t by_lds = (int64_t)(kColLdsBudget / (2 * (size_t)R.bytes));
+    const int64_t by_regs = (int64_t)kColStage * kColThreads / (R.bytes / 16);
+    const int32_t tb = (int32_t)std::min<int64_t>(std::min<int64_t>(by_lds, by_regs), f.n_trees);
+    *lds = (size_t)2 * tb * R.bytes;
+    return tb;
+}
+
+template <int NF>
+hipError_t launch_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream) {
+    const int64_t n_cols = (c.H + kWave - 1) / kWave;
+    const int64_t items = c.S * n_cols;
+    size_t lds = 0;
+    const int32_t tb = column_trees_per_block(f, &lds);
+    if (tb > 0) {
+        const auto kern = forest_column_lds_kernel<NF>;
+        const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 (int)lds);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(kern, dim3((unsigned)((items + kColWaves - 1) / kColWaves)), dim3(kColThreads), lds,
+                           stream, f.records, f.n_trees, f.depth, tb, f.base_score, c);
+    } else {
+        hipLaunchKernelGGL(forest_column_global_kernel<NF>, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, stream,
+                           f.nodes, f.leaves, f.n_trees, f.depth, f.base_score, c);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream) {
+    if (c.S == 0) return hipSuccess;
+    return f.n_features == 4 ? launch_column<4>(f, c, stream) : launch_column<3>(f, c, stream);
+}
+
+}  // namespace tl

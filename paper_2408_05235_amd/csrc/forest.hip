@@ -43,6 +43,7 @@
 
 #include "device_util.h"
 #include "tl_internal.h"
+#include "forest_walk.h"
 
 namespace tl {
 namespace {
@@ -211,18 +212,6 @@ __device__ __forceinline__ bool in_box(const float4& b, float kv, float bs) {
     return (kv >= b.x) & (kv < b.y) & (bs >= b.z) & (bs < b.w);
 }
 
-// The value of the feature a record node tests, picked with byte permutes:
-// node = (threshold, sel1, sel2, sel3); sel1 picks frequency or KV, sel2
-// batch or engine size, sel3 between the two picks (v_perm_b32: selector
-// 0x03020100 keeps the second operand, 0x07060504 takes the first).
-template <int NF>
-__device__ __forceinline__ float node_feature(const uint4& nd, float xf, float kv, float bs, float xe) {
-    const uint32_t x01 = __builtin_amdgcn_perm(__float_as_uint(kv), __float_as_uint(xf), nd.y);
-    const uint32_t x23 = NF == 4 ? __builtin_amdgcn_perm(__float_as_uint(xe), __float_as_uint(bs), nd.z)
-                                 : __float_as_uint(bs);
-    return __uint_as_float(__builtin_amdgcn_perm(x23, x01, nd.w));
-}
-
 constexpr int kLdsWaves = TL_LDS_WAVES;  // wavefronts per workgroup
 constexpr int kLdsThreads = kLdsWaves * kWave;
 #ifndef TL_STAGE_REGS
@@ -245,47 +234,6 @@ __device__ __forceinline__ float to_sgpr(float x) {
 #define TL_ROW_GROUP 4
 #endif
 constexpr int kRowGroup = TL_ROW_GROUP;   // rows whose (KV, batch) hull is tested as one
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
-
-// LDS byte address of a location in the kernel's dynamic LDS.
-__device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
-    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const unsigned char*)p;
-}
-
-// Walks NT consecutive staged trees (records rec_bytes apart, the first at
-// LDS byte address `tree`) from the root for one row; k[t] = leaf index of
-// tree t.  The walks of two trees interleave, so their chains of dependent
-// LDS reads overlap.
-template <int NF, int NT>
-__device__ __forceinline__ void walk(uint32_t tree, uint32_t rec_bytes, int32_t depth, float xf, float kv, float bs,
-                                     float xe, int32_t (&k)[NT]) {
-    // the loop carries node byte addresses: child 2k+1 of the node at
-    // a = root + 16 k sits at 2 a + (16 - root), child 2k+2 16 bytes later
-    uint32_t a[NT], cl[NT], cr[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        a[t] = tree + t * rec_bytes;
-        cl[t] = 16u - a[t];
-        cr[t] = 32u - a[t];
-        // opaque to the optimizer, which would otherwise rewrite the select
-        // of the two offsets as an add after the compare
-        asm volatile("" : "+v"(cl[t]), "+v"(cr[t]));
-    }
-    for (int32_t level = 0; level < depth; ++level) {
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const u32x4 w = *(lds_u32x4*)(uintptr_t)a[t];
-            const uint4 nd = make_uint4(w.x, w.y, w.z, w.w);
-            const bool left = node_feature<NF>(nd, xf, kv, bs, xe) < __uint_as_float(nd.x);
-            a[t] = 2u * a[t] + (left ? cl[t] : cr[t]);
-        }
-    }
-    const int32_t n_int = (1 << depth) - 1;
-#pragma unroll
-    for (int t = 0; t < NT; ++t) k[t] = (int32_t)((a[t] - (tree + t * rec_bytes)) >> 4) - n_int;
-}
 
 __device__ __forceinline__ float4 box_meet(const float4& a, const float4& b) {
     return make_float4(a.x > b.x ? a.x : b.x, a.y < b.y ? a.y : b.y, a.z > b.z ? a.z : b.z, a.w < b.w ? a.w : b.w);

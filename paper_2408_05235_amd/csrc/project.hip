@@ -13,6 +13,10 @@
 // where comb_diff gets +1 at j0 and -1 at the first comb point >= e.  The
 // batch curve is the prefix sum of +1 at 0 / -1 at e.
 //
+// For admission control a new query can be appended to every scenario as a
+// request that starts now (Sec. 4.3.2, the "virtual" scoreboard); it adds
+// in-flight events like the others.
+//
 // Queued requests are admitted in FIFO order by the same wave, each at the
 // first iteration from its arrival (and from the previous admission) where
 // its KV contribution over its in-horizon lifetime fits under the capacity.
@@ -43,6 +47,32 @@ __device__ __forceinline__ int32_t sum_range(const int32_t* DA, int32_t j, int32
         acc += (t <= j2) ? DA[t] : 0;
     }
     return wave_sum(acc);
+}
+
+// Events of one request that holds c cached tokens now and stays in the batch
+// on [0, e): batch +1 at 0 / -1 at e, KV +ceil(c/N) at 0 and -KV_i[e-1] at
+// e, and the block comb from its first new-block iteration (see above).
+// Counts it in n_in, kv0 (blocks at iteration 0) and n_end.
+__device__ __forceinline__ void inflight_events(int32_t c, int32_t e, int32_t H, int32_t N, const DivU32& divN,
+                                                int32_t* BI, int32_t* KV, int32_t* CD, int32_t& n_in,
+                                                int32_t& kv0, int32_t& n_end) {
+    ++n_in;
+    kv0 += (int32_t)ceil_div_u32((uint32_t)c, divN);
+    const int32_t lim = min(e, H);
+    n_end = max(n_end, lim);
+    if (e < H) {
+        atomicAdd(&BI[e], -1);
+        atomicAdd(&KV[e], -(int32_t)ceil_div_u32((uint32_t)(c + e - 1), divN));
+    }
+    const int32_t rc = (int32_t)((uint32_t)c - div_u32((uint32_t)c, divN) * (uint32_t)N);
+    const int32_t j0 = (rc == 0) ? 1 : (N + 1 - rc);
+    if (j0 < lim) {
+        atomicAdd(&CD[j0], 1);
+        if (e < H) {
+            const int32_t jend = j0 + N * (int32_t)ceil_div_u32((uint32_t)(e - j0), divN);
+            if (jend < H) atomicAdd(&CD[jend], -1);
+        }
+    }
 }
 
 __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
@@ -99,6 +129,17 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
             arr_carry = max(arr_carry, __shfl(incl, kWave - 1));
         }
     }
+    // the appended query (admission control): one more request that starts
+    // now; a malformed one is left out and flagged
+    int32_t cand_p = 0, cand_l = 0;
+    bool cand = false;
+    if (P.cand_len && !bad_range) {
+        cand_p = P.cand_prompt[s];
+        cand_l = P.cand_len[s];
+        cand = entry_ok(cand_p, 0, cand_l, -1);
+        if (!cand) fl |= TL_FLAG_BAD_CANDIDATE;
+        else if (lane == 0) bound += ceil_div_u32((uint32_t)(cand_p + H), divN);
+    }
     bound = wave_sum_u64(bound);
     fl = wave_or(fl);
     has_queue = wave_max(has_queue);
@@ -131,27 +172,12 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
         if (!entry_ok(p, g, r, a) || a != -1) continue;
         const int32_t c = p + g;
         const int32_t e = r;
-        ++n_in;
-        kv0 += (int32_t)ceil_div_u32((uint32_t)c, divN);
-        const int32_t lim = min(e, H);
-        n_end = max(n_end, lim);
-        if (e < H) {
-            atomicAdd(&BI[e], -1);
-            atomicAdd(&KV[e], -(int32_t)ceil_div_u32((uint32_t)(c + e - 1), divN));
-        }
-        const int32_t rc = (int32_t)((uint32_t)c - div_u32((uint32_t)c, divN) * (uint32_t)N);
-        const int32_t j0 = (rc == 0) ? 1 : (N + 1 - rc);
-        if (j0 < lim) {
-            atomicAdd(&CD[j0], 1);
-            if (e < H) {
-                const int32_t jend = j0 + N * (int32_t)ceil_div_u32((uint32_t)(e - j0), divN);
-                if (jend < H) atomicAdd(&CD[jend], -1);
-            }
-        }
+        inflight_events(c, e, H, N, divN, BI, KV, CD, n_in, kv0, n_end);
         const bool is_lost = P.lost && P.lost[i];
         const uint64_t d = P.deadline ? P.deadline[i] : kNoDeadline;
         if (e <= H && !is_lost && d != kNoDeadline) atomicMin((unsigned long long*)&outDL[e - 1], (unsigned long long)d);
     }
+    if (cand && lane == 0) inflight_events(cand_p, cand_l, H, N, divN, BI, KV, CD, n_in, kv0, n_end);
     n_in = wave_sum(n_in);
     kv0 = wave_sum(kv0);
     n_end = wave_max(n_end);

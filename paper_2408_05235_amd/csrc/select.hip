@@ -8,6 +8,9 @@
 // which is compared with the deadline of requests ending at j.  The walk stops
 // at the first violated deadline.  Feasible frequencies are collected as a
 // bitmask in LDS and the lowest one is taken.
+//
+// The admission decision of Sec. 4.3.2 uses the same arithmetic at one
+// frequency (the maximum) per scenario.
 #include "device_util.h"
 #include "tl_internal.h"
 
@@ -82,7 +85,66 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams P) {
     }
 }
 
+// Admission decision (Sec. 4.3.2 checks 1-3) of one new query per scenario
+// from the projection with it and M at the maximum frequency: one wavefront
+// per scenario walks the projected iterations 64 at a time with the same
+// per-iteration time and scan as selection; the deadline of the query itself
+// (ending at cand_len, when inside the horizon) is checked apart from the
+// scheduled requests' deadlines in deadline_at.
+constexpr int kAdmitWaves = 4;
+
+__global__ __launch_bounds__(kAdmitWaves * kWave) void admit_kernel(AdmitParams P) {
+    const int64_t s = (int64_t)blockIdx.x * kAdmitWaves + threadIdx.x / kWave;
+    if (s >= P.S) return;
+    const int lane = lane_id();
+    const int32_t H = P.H;
+    const uint32_t fl = P.proj_flags[s];
+    uint32_t dec;
+    if (fl & (TL_FLAG_OVERFLOW | TL_FLAG_BAD_CANDIDATE)) {
+        dec = TL_ADMIT_INVALID;
+    } else if (fl & TL_FLAG_OVERCOMMIT) {
+        // the requests running now (the query among them) exceed the KV
+        // capacity at some iteration or the batch cap: every value of the
+        // projected KV vector is within the capacity otherwise, since queued
+        // requests are only admitted where they fit
+        dec = TL_ADMIT_QUEUE_CAPACITY;
+    } else {
+        const int32_t n = min(max(P.n_iters[s], 0), H);
+        const int32_t L = P.cand_len[s];
+        const uint64_t d_own = P.cand_deadline ? P.cand_deadline[s] : kNoDeadline;
+        const int32_t own_at = (d_own != kNoDeadline && L <= H) ? L - 1 : -1;   // T_R[L] = T_R[own_at + 1]
+        const float* ips = P.ips + s * H;
+        const uint64_t* dl = P.deadline_at + s * H;
+        uint64_t carry = 0;
+        bool miss = false, miss_own = false;
+        for (int32_t j0 = 0; j0 < n; j0 += kWave) {
+            const int32_t j = j0 + lane;
+            const bool in = j < n;
+            const uint64_t lat = in ? latency_ns(ips[j]) : 0ull;
+            const uint64_t tr = wave_incl_scan_u64(lat) + carry;
+            const uint64_t d = in ? dl[j] : kNoDeadline;
+            miss |= in && d != kNoDeadline && !(tr < d);
+            miss_own |= in && j == own_at && !(tr < d_own);
+            carry = __shfl(tr, kWave - 1);
+        }
+        const uint64_t slo = P.tbt_slo_ns[s];
+        const uint64_t budget = n == 0 ? ~0ull : (slo > ~0ull / (uint64_t)n) ? ~0ull : slo * (uint64_t)n;
+        if (!(carry <= budget)) dec = TL_ADMIT_QUEUE_TBT;
+        else if (__ballot(miss)) dec = TL_ADMIT_QUEUE_E2E;
+        else if (__ballot(miss_own)) dec = TL_ADMIT_LOST;
+        else dec = TL_ADMIT_OK;
+    }
+    if (lane == 0) P.decision[s] = dec;
+}
+
 }  // namespace
+
+hipError_t launch_admit(const AdmitParams& p, hipStream_t stream) {
+    if (p.S == 0) return hipSuccess;
+    hipLaunchKernelGGL(admit_kernel, dim3((unsigned)((p.S + kAdmitWaves - 1) / kAdmitWaves)),
+                       dim3(kAdmitWaves * kWave), 0, stream, p);
+    return hipGetLastError();
+}
 
 hipError_t launch_select(const SelectParams& p, hipStream_t stream) {
     hipLaunchKernelGGL(select_kernel, dim3((unsigned)p.S), dim3(256), 0, stream, p);

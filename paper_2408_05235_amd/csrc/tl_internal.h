@@ -33,6 +33,39 @@ struct ProjectParams {
     const float* freqs;
     const float* engine;
     float* rows;                    // nullable
+    // a new query appended to every scenario as a request that starts now
+    // (admission control); both nullable together
+    const int32_t* cand_prompt;     // [S]
+    const int32_t* cand_len;        // [S]
+};
+
+// The model at one frequency per scenario on the projection grid:
+// out[s][j] = M(f_s, kv[s][j], batch[s][j] [, engine[s]]), f_s = freqs[fidx[s]]
+// or `freq` when fidx is null.
+struct ColumnParams {
+    int64_t S;
+    int32_t H;
+    const int32_t* kv;
+    const int32_t* batch;
+    float freq;
+    const float* freqs;             // with fidx
+    const int32_t* fidx;            // nullable
+    const float* engine;            // 4-feature forests
+    float* out;
+};
+
+// Admission decision from the IPS at the maximum frequency.
+struct AdmitParams {
+    const float* ips;               // [S][H]
+    int64_t S;
+    int32_t H;
+    const uint64_t* deadline_at;
+    const int32_t* n_iters;
+    const uint64_t* tbt_slo_ns;
+    const uint32_t* proj_flags;
+    const int32_t* cand_len;
+    const uint64_t* cand_deadline;  // nullable
+    uint32_t* decision;
 };
 
 struct SelectParams {
@@ -120,5 +153,7 @@ hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_r
                               hipStream_t stream);
 hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, hipStream_t stream);
 hipError_t launch_select(const SelectParams& p, hipStream_t stream);
+hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream);
+hipError_t launch_admit(const AdmitParams& p, hipStream_t stream);
 
 }  // namespace tl

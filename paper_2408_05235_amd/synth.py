@@ -227,6 +227,22 @@ def make_inputs(cfg, seed=None):
     )
 
 
+def make_candidates(cfg, inp, seed=None):
+    """One new query per scenario for admission control (Sec. 4.3.2): its
+    prompt and predicted length drawn like the workload's requests (arrival
+    distributions where the workload has arrivals), and an E2E deadline of
+    sigma_s per predicted token, the rule of the in-flight deadlines.
+    Deterministic in (cfg, seed)."""
+    seed = (cfg["seed"] if seed is None else seed) + 7919
+    rng = _rng(np.random.SeedSequence(seed))
+    S = int(inp["n_scenarios"])
+    arr = cfg.get("arrivals")
+    prompt = _draw(rng, arr["prompt"] if arr else cfg["prompt"], S)
+    length = _draw(rng, arr["length"] if arr else cfg["remaining"], S)
+    deadline = np.asarray(inp["tbt_slo_ns"], np.uint64) * length.astype(np.uint64)
+    return dict(cand_prompt=prompt, cand_len=length, cand_deadline_ns=deadline)
+
+
 def scaled(cfg, **overrides):
     """A copy of a workload with some sizes replaced (same distributions)."""
     out = dict(cfg)

@@ -1,0 +1,155 @@
+"""Parity of tl_admit (admission control of Sec. 4.3.2, one new query per
+scenario) with the oracle, through the C ABI.
+
+Decisions, the projection with the query and the flags must match bit for
+bit; the model at the maximum frequency must match within 1e-5 relative (it
+is expected to be bit-identical, and the tests count exact matches).  Inputs
+come from the seeded generators or are written here; expected values come
+from the oracle or the hand-computed fixture.
+"""
+import numpy as np
+import pytest
+
+import goldens
+import oracle
+from paper_2408_05235_amd import configs, synth
+from test_gpu_parity import assert_ips_close, assert_projection_equal, random_boards, random_forest
+
+pytestmark = pytest.mark.gpu
+
+NONE = np.uint64(0xFFFFFFFFFFFFFFFF)
+
+
+def _np(t, dtype=None):
+    a = t.detach().cpu().numpy()
+    return a.view(dtype) if dtype is not None else a
+
+
+def gpu_admit(inp, forest_dict, fmax, cand_prompt, cand_len, cand_deadline):
+    import torch
+    from paper_2408_05235_amd import api
+    S = int(inp["n_scenarios"])
+    d = api.upload(dict(inp, freqs_mhz=np.zeros(1, np.float32), n_features=forest_dict["n_features"],
+                        engine_size=inp.get("engine_size")))
+    t = lambda a, dt: None if a is None else torch.from_numpy(np.ascontiguousarray(a, dt).view(
+        np.int64 if dt == np.uint64 else dt)).cuda()
+    forest = api.Forest.from_dict(forest_dict)
+    out = api.tl_admit(forest, fmax, d["tbt_slo_ns"], t(cand_prompt, np.int32), t(cand_len, np.int32),
+                       d["req_offset"], d["prompt"], d["generated"], d["remaining"], d["arrival"],
+                       d["kv_capacity"], d["horizon"], d["block_tokens"], d["deadline_ns"], d["lost"],
+                       d["batch_cap"], d["engine_size"], t(cand_deadline, np.uint64))
+    torch.cuda.synchronize()
+    res = dict(batch=_np(out["batch"]), kv=_np(out["kv"]), deadline_at=_np(out["deadline_at"], np.uint64),
+               n_iters=_np(out["n_iters"]), flags=_np(out["flags"], np.uint32), ips=_np(out["ips"]),
+               decision=_np(out["decision"]).view(np.uint32))
+    forest.close()
+    assert res["decision"].shape == (S,)
+    return res
+
+
+def check_admit(inp, forest_dict, fmax, cand, where=""):
+    cp, cl, cd = cand["cand_prompt"], cand["cand_len"], cand.get("cand_deadline_ns")
+    g = gpu_admit(inp, forest_dict, fmax, cp, cl, cd)
+    o = oracle.admit(inp, cp, cl, cd, fmax, forest_dict)
+    bad = np.nonzero(g["decision"] != o["decision"])[0]
+    assert bad.size == 0, f"{where} decision differs at {bad[:5].tolist()}: gpu {g['decision'][bad[:5]]} " \
+                          f"oracle {o['decision'][bad[:5]]}"
+    # the projection with the query, wherever the query was well formed
+    ok_q = (np.asarray(cp) >= 0) & (np.asarray(cp) <= (1 << 30)) & (np.asarray(cl) >= 1)
+    assert np.all(g["flags"][~ok_q] & 32), f"{where} malformed query not flagged"
+    sel = np.nonzero(ok_q)[0]
+    assert_projection_equal({k: g[k][sel] for k in ("batch", "kv", "deadline_at", "n_iters", "flags")},
+                            {k: o[k][sel] for k in ("batch", "kv", "deadline_at", "n_iters", "flags")}, where)
+    # the model at the maximum frequency on every projected scenario (the
+    # oracle's own admission stops at check 1; evaluate the rest here)
+    nf = int(forest_dict["n_features"])
+    eng = None if nf == 3 else np.asarray(inp["engine_size"], np.float32)[sel]
+    x = oracle.rows(np.array([fmax], np.float32), o["batch"][sel], o["kv"][sel], eng, nf)
+    want = oracle.forest_predict(forest_dict, x)[:, 0]
+    exact = assert_ips_close(g["ips"][sel], want, where)
+    assert exact == want.size
+    return g["decision"]
+
+
+def test_admit_golden_gpu(gpu):
+    g = goldens.load("admit_two_stumps.json")
+    forest = goldens.forest(g)
+    for case in g["cases"]:
+        sigma = case["sigma_ns"]
+        inp = goldens.scoreboard(g, deadline_ns=[sigma * r for r in g["remaining"]], lost=case.get("lost"))
+        if "kv_capacity" in case:
+            inp["kv_capacity"] = np.array([case["kv_capacity"]], np.int32)
+        if "batch_cap" in case:
+            inp["batch_cap"] = np.array([case["batch_cap"]], np.int32)
+        inp["tbt_slo_ns"] = np.array([sigma], np.uint64)
+        d = case["cand_deadline"]
+        out = gpu_admit(inp, forest, g["max_freq_mhz"], [case["cand_prompt"]], [case["cand_len"]],
+                        None if d is None else [d])
+        assert int(out["decision"][0]) == case["decision"], case["note"]
+        ex = g["expect_by_len"].get(str(case["cand_len"]))
+        if ex is not None:
+            assert out["kv"][0].tolist() == ex["kv"]
+            assert out["batch"][0].tolist() == ex["batch"]
+            assert out["ips"][0].tolist() == ex["ips"]
+
+
+def random_candidates(rng, inp, bad=0.05, beyond=0.1, no_deadline=0.15):
+    S, H = int(inp["n_scenarios"]), int(inp["horizon"])
+    p = rng.integers(0, 600, S).astype(np.int32)
+    L = rng.integers(1, max(2, H), S).astype(np.int32)
+    L[rng.random(S) < beyond] = H + rng.integers(0, 50)
+    m = rng.random(S) < bad
+    p[m & (rng.random(S) < 0.5)] = -1
+    L[m & (rng.random(S) < 0.5)] = 0
+    slo = np.asarray(inp["tbt_slo_ns"], np.uint64)
+    dl = (slo * np.maximum(L, 1).astype(np.uint64)).astype(np.uint64)
+    dl = (dl.astype(np.float64) * rng.uniform(0.5, 1.5, S)).astype(np.uint64)
+    dl[rng.random(S) < no_deadline] = NONE
+    return dict(cand_prompt=p, cand_len=L, cand_deadline_ns=dl)
+
+
+@pytest.mark.parametrize("H,N,T,d,nf,seed", [
+    (8, 4, 3, 2, 3, 0), (64, 16, 40, 6, 3, 1), (100, 3, 25, 8, 3, 2), (513, 16, 30, 10, 4, 3),
+    (1, 16, 5, 3, 3, 4), (77, 7, 6, 12, 4, 5), (300, 16, 0, 4, 3, 6), (130, 8, 9, 0, 3, 7),
+    (2048, 16, 12, 11, 3, 8)])
+def test_admit_random_boards(gpu, H, N, T, d, nf, seed):
+    rng = np.random.default_rng(500 + seed)
+    S = 37
+    inp = random_boards(rng, S, H, N, rmax=30)
+    inp["tbt_slo_ns"] = rng.integers(5_000_000, 60_000_000, S).astype(np.uint64)
+    inp["deadline_ns"] = np.where(inp["deadline_ns"] == NONE, NONE,
+                                  (inp["remaining"].astype(np.uint64) * np.uint64(20_000_000))).astype(np.uint64)
+    if nf == 4:
+        inp["engine_size"] = rng.choice([1.0, 2.0, 4.0, 8.0], S).astype(np.float32)
+    fd = random_forest(rng, T, d, nf, kvmax=400, bmax=40)
+    fd["base_score"] = np.float32(60.0)
+    dec = check_admit(inp, fd, 2000.0, random_candidates(rng, inp), f"H={H} T={T} d={d}")
+    assert len(set(dec.tolist())) >= 2
+
+
+def test_admit_without_query_deadlines(gpu):
+    rng = np.random.default_rng(9)
+    inp = random_boards(rng, 20, 200, 16, rmax=20)
+    inp["tbt_slo_ns"] = rng.integers(5_000_000, 60_000_000, 20).astype(np.uint64)
+    fd = random_forest(rng, 20, 6, 3, kvmax=400, bmax=40)
+    cand = random_candidates(rng, inp)
+    cand["cand_deadline_ns"] = None
+    dec = check_admit(inp, fd, 2000.0, cand, "no deadlines")
+    assert not np.any(dec == oracle.ADMIT_LOST)
+
+
+SCALED = [
+    (0, dict()),
+    (1, dict(n_scenarios=10)),
+    (2, dict(n_scenarios=6)),
+    (3, dict(n_scenarios=4, forest_n_trees=300)),
+    (4, dict(n_scenarios=5)),
+]
+
+
+@pytest.mark.parametrize("ci,over", SCALED, ids=[c["name"] for c in configs.CONFIGS])
+def test_admit_scaled_configs(gpu, ci, over):
+    cfg = synth.scaled(configs.get_config(ci), **over)
+    inp = synth.make_inputs(cfg)
+    cand = synth.make_candidates(cfg, inp)
+    check_admit(inp, inp["forest"], float(inp["freqs_mhz"][-1]), cand, cfg["name"])
