@@ -4,14 +4,15 @@
 // for every projected iteration) and of one probe of a search over
 // frequencies (Sec. 4.5).
 //
-// A wavefront takes 64 consecutive iterations of one scenario, one row per
-// lane; the rows differ, so every lane walks every tree (the grid kernel's
-// leaf reuse needs many frequencies on the same row sequence).  Sixteen
-// wavefronts of a workgroup share double-buffered blocks of tree records in
-// LDS, loaded into registers while the current block is evaluated and stored
-// after it.  The walks of up to four trees interleave, so their chains of
-// dependent LDS reads overlap.  Leaves are accumulated in fp64 in tree order
-// and rounded once, as everywhere in the library.
+// A wavefront takes RPL stripes of 64 consecutive iterations of one scenario,
+// RPL rows per lane; the rows differ, so every lane walks every tree (the grid
+// kernel's leaf reuse needs many frequencies on the same row sequence).
+// Sixteen wavefronts of a workgroup share double-buffered blocks of tree
+// records in LDS, loaded into registers while the current block is evaluated
+// and stored after it.  A lane walks its RPL rows through up to four trees at
+// once, so RPL x trees chains of dependent LDS reads overlap (deep trees leave
+// room for only two trees per block).  Leaves are accumulated in fp64 in tree
+// order and rounded once, as everywhere in the library.
 //
 // Forests too deep for LDS records are walked from global memory.
 #include <algorithm>
@@ -28,21 +29,28 @@ constexpr int kColThreads = kColWaves * kWave;
 constexpr int kColStage = 8;                       // staged 16-byte words per thread per block
 constexpr size_t kColLdsBudget = 152 * 1024;
 
+template <int RPL>
 struct ColumnItem {
     int64_t s;
-    int32_t j;          // this lane's iteration
+    int32_t j[RPL];     // this lane's iterations (clamped into the horizon)
+    bool row[RPL];      // ... and whether each is inside it
     bool valid;         // the wavefront has a scenario
-    bool row;           // this lane's row is inside the horizon
 };
 
-__device__ __forceinline__ ColumnItem column_item(const ColumnParams& P, int64_t item) {
-    const int32_t n_cols = (P.H + kWave - 1) / kWave;
-    ColumnItem c;
+template <int RPL>
+__device__ __forceinline__ ColumnItem<RPL> column_item(const ColumnParams& P, int64_t item) {
+    const int32_t span = kWave * RPL;
+    const int32_t n_cols = (P.H + span - 1) / span;
+    ColumnItem<RPL> c;
     c.valid = item < P.S * n_cols;
     c.s = c.valid ? item / n_cols : 0;
-    const int32_t j = (int32_t)(item % n_cols) * kWave + lane_id();
-    c.row = c.valid && j < P.H;
-    c.j = min(j, P.H - 1);
+    const int32_t j0 = (int32_t)(item % n_cols) * span + lane_id();
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) {
+        const int32_t j = j0 + r * kWave;
+        c.row[r] = c.valid && j < P.H;
+        c.j[r] = min(j, P.H - 1);
+    }
     return c;
 }
 
@@ -50,16 +58,50 @@ __device__ __forceinline__ float column_freq(const ColumnParams& P, int64_t s) {
     return P.fidx ? P.freqs[P.fidx[s]] : P.freq;
 }
 
-template <int NF, int NT>
-__device__ __forceinline__ void add_leaves(const unsigned char* smem, uint32_t tree, const RecordLayout& R,
-                                           int32_t depth, float xf, float kv, float bs, float xe, double& acc) {
-    int32_t k[NT];
-    walk<NF, NT>(lds_addr(smem) + tree, R.bytes, depth, xf, kv, bs, xe, k);
+// Walks NT consecutive staged trees (records rec_bytes apart, the first at
+// LDS byte address `tree`) for the RPL rows of a lane, all RPL x NT chains
+// interleaved, and adds the leaves to each row's sum in tree order.
+template <int NF, int NT, int RPL>
+__device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, uint32_t vals_off, int32_t depth,
+                                           float xf, const float (&kv)[RPL], const float (&bs)[RPL], float xe,
+                                           double (&acc)[RPL]) {
+    uint32_t a[RPL][NT], cl[NT], cr[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) acc += (double)((const float*)(smem + tree + t * R.bytes + R.vals))[k[t]];
+    for (int t = 0; t < NT; ++t) {
+        const uint32_t root = tree + t * rec_bytes;
+        cl[t] = 16u - root;
+        cr[t] = 32u - root;
+        asm volatile("" : "+v"(cl[t]), "+v"(cr[t]));
+#pragma unroll
+        for (int r = 0; r < RPL; ++r) a[r][t] = root;
+    }
+    for (int32_t level = 0; level < depth; ++level) {
+        u32x4 w[RPL][NT];
+#pragma unroll
+        for (int r = 0; r < RPL; ++r)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) w[r][t] = *(lds_u32x4*)(uintptr_t)a[r][t];
+#pragma unroll
+        for (int r = 0; r < RPL; ++r)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const uint4 nd = make_uint4(w[r][t].x, w[r][t].y, w[r][t].z, w[r][t].w);
+                const bool left = node_feature<NF>(nd, xf, kv[r], bs[r], xe) < __uint_as_float(nd.x);
+                a[r][t] = 2u * a[r][t] + (left ? cl[t] : cr[t]);
+            }
+    }
+    const int32_t n_int = (1 << depth) - 1;
+#pragma unroll
+    for (int r = 0; r < RPL; ++r)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const uint32_t root = tree + t * rec_bytes;
+            const int32_t k = (int32_t)((a[r][t] - root) >> 4) - n_int;
+            acc[r] += (double)*(__attribute__((address_space(3))) const float*)(uintptr_t)(root + vals_off + 4u * k);
+        }
 }
 
-template <int NF>
+template <int NF, int RPL>
 __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const uint4* __restrict__ records,
                                                                        int32_t n_trees, int32_t depth, int32_t tb,
                                                                        float base, ColumnParams P) {
@@ -69,12 +111,19 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     const uint32_t buf_bytes = (uint32_t)tb * R.bytes;
     const int wave = threadIdx.x / kWave;
     const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kColWaves + wave);
-    const ColumnItem c = column_item(P, item);
+    const ColumnItem<RPL> c = column_item<RPL>(P, item);
     const float xf = column_freq(P, c.s);
     const float xe = NF == 4 ? P.engine[c.s] : 0.0f;
-    const float kv = (float)P.kv[c.s * P.H + c.j];
-    const float bs = (float)P.batch[c.s * P.H + c.j];
-    double acc = (double)base;
+    float kv[RPL], bs[RPL];
+    double acc[RPL];
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) {
+        kv[r] = (float)P.kv[c.s * P.H + c.j[r]];
+        bs[r] = (float)P.batch[c.s * P.H + c.j[r]];
+        acc[r] = (double)base;
+        // the rows are complete before any staging load is in flight
+        asm volatile("" ::"v"(kv[r]), "v"(bs[r]));
+    }
 
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
     // block b: trees [b*tb, b*tb + cnt), one contiguous range of words; each
@@ -109,8 +158,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
         TL_COL_STORE_WORD(4, st4) TL_COL_STORE_WORD(5, st5)                    \
         TL_COL_STORE_WORD(6, st6) TL_COL_STORE_WORD(7, st7)                    \
     }
-    // the row is complete before any staging load is in flight
-    asm volatile("" ::"v"(xf), "v"(xe), "v"(kv), "v"(bs));
+    asm volatile("" ::"v"(xf), "v"(xe));
     if (n_blocks > 0) {
         TL_COL_FETCH(0)
         TL_COL_STORE(0, 0)
@@ -121,14 +169,14 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
         if (b + 1 < n_blocks) TL_COL_FETCH(b + 1)
         if (c.valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
-            const uint32_t base_off = cur * buf_bytes;
+            const uint32_t first = lds_addr(smem) + cur * buf_bytes;
             int32_t t = 0;
-            for (; t + 4 <= cnt; t += 4) add_leaves<NF, 4>(smem, base_off + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
-            if (t + 2 <= cnt) {
-                add_leaves<NF, 2>(smem, base_off + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
-                t += 2;
-            }
-            if (t < cnt) add_leaves<NF, 1>(smem, base_off + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
+            if (RPL == 1)
+                for (; t + 4 <= cnt; t += 4)
+                    add_leaves<NF, 4, RPL>(first + t * R.bytes, R.bytes, R.vals, depth, xf, kv, bs, xe, acc);
+            for (; t + 2 <= cnt; t += 2)
+                add_leaves<NF, 2, RPL>(first + t * R.bytes, R.bytes, R.vals, depth, xf, kv, bs, xe, acc);
+            if (t < cnt) add_leaves<NF, 1, RPL>(first + t * R.bytes, R.bytes, R.vals, depth, xf, kv, bs, xe, acc);
         }
         if (b + 1 < n_blocks) TL_COL_STORE(b + 1, cur ^ 1)
         __syncthreads();
@@ -137,7 +185,9 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
 #undef TL_COL_STORE_WORD
 #undef TL_COL_FETCH
 #undef TL_COL_FETCH_WORD
-    if (c.row) P.out[c.s * P.H + c.j] = (float)acc;
+#pragma unroll
+    for (int r = 0; r < RPL; ++r)
+        if (c.row[r]) P.out[c.s * P.H + c.j[r]] = (float)acc[r];
 }
 
 // Global-memory walks for forests without LDS records.
@@ -147,12 +197,12 @@ __global__ __launch_bounds__(256) void forest_column_global_kernel(const uint2* 
                                                                   int32_t n_trees, int32_t depth, float base,
                                                                   ColumnParams P) {
     const int64_t item = (int64_t)blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
-    const ColumnItem c = column_item(P, item);
-    if (!c.row) return;
+    const ColumnItem<1> c = column_item<1>(P, item);
+    if (!c.row[0]) return;
     float x[4];
     x[0] = column_freq(P, c.s);
-    x[1] = (float)P.kv[c.s * P.H + c.j];
-    x[2] = (float)P.batch[c.s * P.H + c.j];
+    x[1] = (float)P.kv[c.s * P.H + c.j[0]];
+    x[2] = (float)P.batch[c.s * P.H + c.j[0]];
     x[3] = NF == 4 ? P.engine[c.s] : 0.0f;
     const int64_t stride = (int64_t)1 << depth;
     const int32_t n_int = (1 << depth) - 1;
@@ -167,7 +217,7 @@ __global__ __launch_bounds__(256) void forest_column_global_kernel(const uint2* 
         }
         acc += (double)leaves[t * stride + (k - n_int)];
     }
-    P.out[c.s * P.H + c.j] = (float)acc;
+    P.out[c.s * P.H + c.j[0]] = (float)acc;
 }
 
 // Trees per staged block: double buffers within the LDS budget, and no more
@@ -182,23 +232,32 @@ int32_t column_trees_per_block(const ForestDev& f, size_t* lds) {
     return tb;
 }
 
+template <int NF, int RPL>
+hipError_t launch_column_lds(const ForestDev& f, const ColumnParams& c, int32_t tb, size_t lds, hipStream_t stream) {
+    const int64_t n_cols = (c.H + kWave * RPL - 1) / (kWave * RPL);
+    const int64_t items = c.S * n_cols;
+    const auto kern = forest_column_lds_kernel<NF, RPL>;
+    const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)((items + kColWaves - 1) / kColWaves)), dim3(kColThreads), lds, stream,
+                       f.records, f.n_trees, f.depth, tb, f.base_score, c);
+    return hipGetLastError();
+}
+
 template <int NF>
 hipError_t launch_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream) {
-    const int64_t n_cols = (c.H + kWave - 1) / kWave;
-    const int64_t items = c.S * n_cols;
     size_t lds = 0;
     const int32_t tb = column_trees_per_block(f, &lds);
     if (tb > 0) {
-        const auto kern = forest_column_lds_kernel<NF>;
-        const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 (int)lds);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(kern, dim3((unsigned)((items + kColWaves - 1) / kColWaves)), dim3(kColThreads), lds,
-                           stream, f.records, f.n_trees, f.depth, tb, f.base_score, c);
-    } else {
-        hipLaunchKernelGGL(forest_column_global_kernel<NF>, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, stream,
-                           f.nodes, f.leaves, f.n_trees, f.depth, f.base_score, c);
+        // rows per lane: enough chains to overlap, without idle stripes on
+        // short horizons
+        if (c.H > 2 * kWave) return launch_column_lds<NF, 4>(f, c, tb, lds, stream);
+        if (c.H > kWave) return launch_column_lds<NF, 2>(f, c, tb, lds, stream);
+        return launch_column_lds<NF, 1>(f, c, tb, lds, stream);
     }
+    const int64_t items = c.S * ((c.H + kWave - 1) / kWave);
+    hipLaunchKernelGGL(forest_column_global_kernel<NF>, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, stream,
+                       f.nodes, f.leaves, f.n_trees, f.depth, f.base_score, c);
     return hipGetLastError();
 }
 
