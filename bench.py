@@ -8,8 +8,9 @@ batch of synthetic scenarios already resident in HBM.
                     [--cpu-procs C]
 
 Prints one JSON line: whole-step throughput, per-stage HIP-event times (mean,
-median, min over the K timed steps), the forest kernel's roofline record and
-the oracle's CPU baseline (one thread, and C single-threaded processes).
+median, min over the K timed steps), the forest kernel's roofline record, the
+oracle's CPU baseline (one thread, and C single-threaded processes), and the
+admission-control what-ifs (one new query per scenario) on the same workload.
 """
 import argparse
 import hashlib
@@ -125,19 +126,69 @@ def cpu_baseline(inp, budget_s=12.0, max_scen=64, procs=0):
     return out
 
 
+def admission_bench(inp, cfg, dev_in, forest, steps, warmup):
+    """Admission control (Sec. 4.3.2) of one new query per scenario of the same
+    workload: projection with the query, the model at the maximum frequency on
+    every projected iteration, checks 1-3 (one tl_admit call), timed like the
+    step with HIP events on the launch stream."""
+    import torch
+
+    from paper_2408_05235_amd import api, synth
+    cand = synth.make_candidates(cfg, inp)
+    t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a, dt).view(np.int64 if dt == np.uint64 else dt)).cuda()
+    cp, cl, cd = t(cand["cand_prompt"], np.int32), t(cand["cand_len"], np.int32), t(cand["cand_deadline_ns"], np.uint64)
+    d = dev_in
+    fmax = float(inp["freqs_mhz"][-1])
+    res = None
+
+    def call():
+        nonlocal res
+        res = api.tl_admit(forest, fmax, d["tbt_slo_ns"], cp, cl, d["req_offset"], d["prompt"], d["generated"],
+                           d["remaining"], d["arrival"], d["kv_capacity"], d["horizon"], d["block_tokens"],
+                           d["deadline_ns"], d["lost"], d["batch_cap"], d["engine_size"], cd, res)
+
+    for _ in range(max(1, warmup)):
+        call()
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        call()
+        e1.record()
+        ms.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in ms])
+    S, H = inp["n_scenarios"], inp["horizon"]
+    dec = np.bincount(res["decision"].cpu().numpy(), minlength=6)
+    return {"what_ifs": S, "ms_mean": float(ms.mean()), "ms_median": float(np.median(ms)), "ms_min": float(ms.min()),
+            "what_ifs_per_s": S / (ms.mean() / 1e3), "rows_per_s": S * H / (ms.mean() / 1e3),
+            "decisions": dict(zip(("admit", "admit_lost", "queue_capacity", "queue_tbt", "queue_e2e", "invalid"),
+                                  dec.tolist()))}
+
+
 def _clock_record():
-    """Clock state as rocm-smi reports it (clocks are left at their defaults)."""
-    import subprocess
-    try:
-        r = subprocess.run(["rocm-smi", "--showperflevel", "--showclocks", "--json"],
-                           capture_output=True, text=True, timeout=20)
-        rec = json.loads(r.stdout)
-        card = next(iter(rec.values()))
-        keep = {k: v for k, v in card.items() if "perf" in k.lower() or "sclk" in k.lower()
-                or "mclk" in k.lower() or "fclk" in k.lower()}
-        return keep or card
-    except Exception as e:  # noqa: BLE001 - a missing tool only loses this record
-        return {"error": f"{type(e).__name__}: {e}"[:200]}
+    """Clock state of the first AMD GPU as the driver reports it in sysfs
+    (clocks are left at their defaults): performance level and the current
+    shader / memory clock levels.  Read from files; no other program runs."""
+    import glob
+    out = {}
+    for dev in sorted(glob.glob("/sys/class/drm/card*/device")):
+        try:
+            if open(os.path.join(dev, "vendor")).read().strip() != "0x1002":
+                continue
+        except OSError:
+            continue
+        for name in ("power_dpm_force_performance_level", "pp_dpm_sclk", "pp_dpm_mclk"):
+            try:
+                lines = open(os.path.join(dev, name)).read().split("\n")
+            except OSError as e:
+                out[name] = f"unreadable: {e.strerror}"
+                continue
+            cur = [ln.strip() for ln in lines if ln.strip().endswith("*")]
+            out[name] = (cur[0] if cur else " ".join(ln.strip() for ln in lines if ln.strip()))[:120]
+        break
+    return out or {"error": "no AMD GPU in /sys/class/drm"}
 
 
 def main():
@@ -254,6 +305,7 @@ def main():
                      "traffic": traffic, "ops_per_row": ops_per_row,
                      "ops_note": "one fp64 leaf add per (row, tree); peak = non-packed VALU lane ops"},
     }
+    out["admission"] = admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup)
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda:0")

@@ -153,3 +153,45 @@ def test_admit_scaled_configs(gpu, ci, over):
     inp = synth.make_inputs(cfg)
     cand = synth.make_candidates(cfg, inp)
     check_admit(inp, inp["forest"], float(inp["freqs_mhz"][-1]), cand, cfg["name"])
+
+
+# (config, scenarios checked against the oracle at full size)
+PLAN_FULL = {0: [0], 1: [0, 517, 1023], 2: [0, 128, 255], 3: [0, 2048, 4095], 4: [0, 9000, 16383]}
+
+
+@pytest.mark.parametrize("ci", range(5), ids=[c["name"] for c in configs.CONFIGS])
+def test_admit_full_size(gpu, ci):
+    """Every workload at full size through tl_admit, in the launch
+    configuration the benchmark times: sampled scenarios equal the oracle
+    (decision, projection with the query, model at the maximum frequency);
+    over every scenario the decision agrees with the projection's flags and
+    capacity."""
+    import time
+    cfg = configs.get_config(ci)
+    t0 = time.time()
+    inp = synth.make_inputs(cfg)
+    cand = synth.make_candidates(cfg, inp)
+    fmax = float(inp["freqs_mhz"][-1])
+    g = gpu_admit(inp, inp["forest"], fmax, cand["cand_prompt"], cand["cand_len"], cand["cand_deadline_ns"])
+    print(f"{cfg['name']}: admission on the GPU {time.time() - t0:.1f}s, decisions "
+          f"{np.bincount(g['decision'], minlength=6).tolist()}", flush=True)
+    dec, fl = g["decision"], g["flags"]
+    assert np.all(dec <= oracle.ADMIT_INVALID)
+    invalid = (fl & (oracle.FLAG_OVERFLOW | 32)) != 0
+    assert np.array_equal(dec == oracle.ADMIT_INVALID, invalid)
+    assert np.array_equal(dec == oracle.QUEUE_CAPACITY, ~invalid & ((fl & oracle.FLAG_OVERCOMMIT) != 0))
+    fits = g["kv"].max(axis=1) <= np.asarray(inp["kv_capacity"])
+    assert np.all(fits[(dec != oracle.QUEUE_CAPACITY) & ~invalid])
+    nf = int(inp["n_features"])
+    for s in PLAN_FULL[ci]:
+        sub = synth.subset(inp, [s])
+        o = oracle.admit(sub, cand["cand_prompt"][s:s + 1], cand["cand_len"][s:s + 1],
+                         cand["cand_deadline_ns"][s:s + 1], fmax, inp["forest"])
+        assert int(dec[s]) == int(o["decision"][0]), s
+        for k in ("batch", "kv", "deadline_at", "n_iters", "flags"):
+            assert np.array_equal(g[k][s], o[k][0]), (s, k)
+        eng = None if nf == 3 else np.asarray(sub["engine_size"], np.float32)
+        want = oracle.forest_predict(inp["forest"], oracle.rows(np.array([fmax], np.float32), o["batch"],
+                                                                o["kv"], eng, nf))[0, 0]
+        assert assert_ips_close(g["ips"][s], want, f"s={s}") == want.size
+    print(f"{cfg['name']}: checked {PLAN_FULL[ci]} in {time.time() - t0:.1f}s", flush=True)
