@@ -323,11 +323,11 @@ tl_status tl_admit(const tl_admit_args* a, void* stream) {
     if (st != TL_OK) return st;
     const tl_forest* f = a->forest;
     if (!f) return fail(TL_EINVAL, "tl_admit: forest is NULL");
+    if (!a->tbt_slo_ns || !a->cand_prompt || !a->cand_len || !a->ips || !a->decision)
+        return fail(TL_EINVAL, "tl_admit: NULL required pointer");
     if (f->dev.n_features != 3 && f->dev.n_features != 4)
         return fail(TL_EINVAL, "tl_admit: the forest has %d features, admission needs 3 or 4", f->dev.n_features);
     if (f->dev.n_features == 4 && !a->engine_size) return fail(TL_EINVAL, "tl_admit: 4 features need engine_size");
-    if (!a->tbt_slo_ns || !a->cand_prompt || !a->cand_len || !a->ips || !a->decision)
-        return fail(TL_EINVAL, "tl_admit: NULL required pointer");
     const int64_t S = a->proj.n_scenarios;
     if (S == 0) return ok();
     const hipStream_t st_h = (hipStream_t)stream;

@@ -87,6 +87,40 @@ def test_select_and_predict_reject_bad_arguments():
     assert L.tl_forest_predict(None, d, 1, d, None) == _lib.TL_EINVAL
 
 
+def _admit_args(**kw):
+    b = _lib.AdmitArgs()
+    b.struct_size = ctypes.sizeof(_lib.AdmitArgs)
+    b.proj = _args()
+    dummy = ctypes.c_void_p(16)   # never dereferenced: validation fails first
+    for f in ("forest", "tbt_slo_ns", "cand_prompt", "cand_len", "ips", "decision"):
+        setattr(b, f, dummy)
+    b.max_freq_mhz = 2000.0
+    for k, v in kw.items():
+        if k.startswith("proj_"):
+            setattr(b.proj, k[5:], v)
+        else:
+            setattr(b, k, v)
+    return b
+
+
+@pytest.mark.parametrize("kw,needle", [
+    (dict(struct_size=16), "struct_size"),
+    (dict(proj_struct_size=8), "struct_size"),
+    (dict(proj_horizon=0), "horizon"),
+    (dict(proj_block_tokens=0), "block_tokens"),
+    (dict(proj_req_offset=None), "NULL"),
+    (dict(forest=None), "forest is NULL"),
+    (dict(cand_len=None), "NULL required pointer"),
+    (dict(decision=None), "NULL required pointer"),
+])
+def test_admit_rejects_bad_arguments(kw, needle):
+    L = _lib.lib()
+    b = _admit_args(**kw)
+    assert L.tl_admit(ctypes.byref(b), None) == _lib.TL_EINVAL
+    assert needle in L.tl_last_error().decode()
+    assert L.tl_admit(None, None) == _lib.TL_EINVAL
+
+
 def test_forest_create_rejects_bad_trees():
     L = _lib.lib()
     h = ctypes.c_void_p(123)
