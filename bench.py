@@ -9,7 +9,8 @@ batch of synthetic scenarios already resident in HBM.
 
 Prints one JSON line: whole-step throughput, per-stage HIP-event times (mean,
 median, min over the K timed steps), the forest kernel's roofline record, the
-oracle's CPU baseline (one thread, and C single-threaded processes), and the
+oracle's CPU baseline (one thread, and C single-threaded processes), the
+paper's binary-search controller on the same projection, and the
 admission-control what-ifs (one new query per scenario) on the same workload.
 """
 import argparse
@@ -124,6 +125,34 @@ def cpu_baseline(inp, budget_s=12.0, max_scen=64, procs=0):
                               sample=f"{n} of {S} scenarios in {procs} single-threaded processes, "
                                      f"longest {t_max:.1f} s of oracle time ({wall:.1f} s wall with start-up)")
     return out
+
+
+def binary_search_bench(ctl, steps, warmup):
+    """The controller as the paper states it (Sec. 4.5): binary search over the
+    frequencies, the model evaluated only at probed frequencies, on the
+    projection of the last timed step; timed with HIP events, and compared
+    with the exhaustive selection of that step (the two agree wherever
+    feasibility is monotone in the frequency)."""
+    import torch
+    for _ in range(max(1, warmup)):
+        ctl.select_binary()
+    torch.cuda.synchronize()
+    ev = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        idx, st = ctl.select_binary()
+        e1.record()
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    bi, ei = idx.cpu().numpy(), ctl.sel["freq_idx"].cpu().numpy()
+    S, H = ctl.d["n_scenarios"], ctl.d["horizon"]
+    F = ctl.d["freqs_mhz"].numel()
+    probes = int(np.ceil(np.log2(F))) + 1 if F > 1 else 1
+    return {"ms_mean": float(ms.mean()), "ms_median": float(np.median(ms)), "ms_min": float(ms.min()),
+            "rows_evaluated_per_call": S * H * probes, "scenarios_per_s": S / (ms.mean() / 1e3),
+            "same_index_as_exhaustive": float((bi == ei).mean())}
 
 
 def admission_bench(inp, cfg, dev_in, forest, steps, warmup):
@@ -305,6 +334,7 @@ def main():
                      "traffic": traffic, "ops_per_row": ops_per_row,
                      "ops_note": "one fp64 leaf add per (row, tree); peak = non-packed VALU lane ops"},
     }
+    out["binary_search"] = binary_search_bench(ctl, args.steps, args.warmup)
     out["admission"] = admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup)
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4

@@ -14,8 +14,10 @@
  *                     lowest frequency whose predicted per-iteration times
  *                     pass the TBT check and the E2E deadlines (Sec. 4.3.2,
  *                     checks 2 and 3, Eq. 3-4).
- * and, from the same stages, tl_admit: the admission control of Sec. 4.3.2
- * for one new query per scenario.
+ * and, from the same stages, tl_select_freq_binary (the controller's binary
+ * search as the paper states it, querying the model only at probed
+ * frequencies) and tl_admit (the admission control of Sec. 4.3.2 for one new
+ * query per scenario).
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers (memory of the device that is current on
@@ -239,6 +241,28 @@ tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs,
                          const uint64_t* deadline_at, const int32_t* n_iters,
                          const uint64_t* tbt_slo_ns, const uint32_t* proj_flags,
                          int32_t* freq_idx, uint32_t* status, void* stream);
+
+/* ------------------------------------------------------------------------
+ * The paper's throttling controller as it states it (Sec. 4.5): a binary
+ * search over the candidate frequencies that queries the model only at the
+ * frequency each scenario probes.  Per scenario, with lo = 0, hi = F-1:
+ * while lo < hi, mid = lo + (hi - lo) / 2, M on every projected iteration at
+ * freqs_mhz[mid], feasible as in tl_select_freq -> hi = mid, else lo =
+ * mid + 1; finally lo is checked: feasible -> freq_idx = lo (OK), else F-1
+ * (INFEASIBLE).  Flags as in tl_select_freq (OVERFLOW -> INVALID, LOST ->
+ * F-1 without a search).  It equals tl_select_freq whenever feasibility is
+ * monotone in the frequency, and evaluates M on ceil(log2 F) + 1 rows per
+ * (scenario, iteration) instead of F.
+ * kv, batch, deadline_at, n_iters, proj_flags: as written by tl_project;
+ * freqs_mhz [F] ascending; engine_size [S] for 4-feature forests.
+ * Work arrays of the caller: ips_work [S][H] fp32 (left holding M at the
+ * final probe) and search_work [3][S] int32.  Allocates nothing.
+ * ---------------------------------------------------------------------- */
+tl_status tl_select_freq_binary(const tl_forest* forest, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
+                                const float* freqs_mhz, const int32_t* kv, const int32_t* batch,
+                                const float* engine_size, const uint64_t* deadline_at, const int32_t* n_iters,
+                                const uint64_t* tbt_slo_ns, const uint32_t* proj_flags, float* ips_work,
+                                int32_t* search_work, int32_t* freq_idx, uint32_t* status, void* stream);
 
 /* ------------------------------------------------------------------------
  * Admission control (Sec. 4.3.2) for one new query per scenario, as a batch

@@ -22,7 +22,8 @@ ADMIT_OK, ADMIT_LOST, ADMIT_QUEUE_CAPACITY, ADMIT_QUEUE_TBT, ADMIT_QUEUE_E2E, AD
 MAX_HORIZON, MAX_BLOCK_TOKENS, MAX_FREQS, MAX_FEATURES, MAX_DEPTH = 8192, 65536, 4096, 4, 14
 
 EXPORTED = ("tl_abi_version", "tl_last_error", "tl_forest_create", "tl_forest_destroy",
-            "tl_project", "tl_forest_predict", "tl_forest_predict_grid", "tl_select_freq", "tl_admit")
+            "tl_project", "tl_forest_predict", "tl_forest_predict_grid", "tl_select_freq", "tl_admit",
+            "tl_select_freq_binary")
 
 
 class ProjectArgs(ctypes.Structure):
@@ -80,6 +81,8 @@ def lib():
     L.tl_forest_predict_grid.restype = ctypes.c_int
     L.tl_select_freq.argtypes = [P, i64, i32, i32, P, P, P, P, P, P, P]
     L.tl_select_freq.restype = ctypes.c_int
+    L.tl_select_freq_binary.argtypes = [P, i64, i32, i32] + [P] * 13
+    L.tl_select_freq_binary.restype = ctypes.c_int
     L.tl_admit.argtypes = [ctypes.POINTER(AdmitArgs), P]
     L.tl_admit.restype = ctypes.c_int
     _lib = L

@@ -245,9 +245,46 @@ def tl_select_freq(ips, deadline_at, n_iters, tbt_slo_ns, proj_flags=None, out=N
     return idx, st
 
 
+def tl_select_freq_binary(forest, freqs_mhz, kv, batch, deadline_at, n_iters, tbt_slo_ns, proj_flags=None,
+                          engine_size=None, out=None):
+    """The controller's binary search over frequencies (tl_select_freq_binary),
+    querying the model only at probed frequencies.  kv, batch [S,H] int32 as
+    written by tl_project.  Returns (freq_idx int32 [S], status int32 [S])."""
+    _need(kv, torch.int32, "kv")
+    if kv.dim() != 2:
+        raise ValueError("kv must be [S, H]")
+    S, H = kv.shape
+    F = int(freqs_mhz.numel())
+    _need(freqs_mhz, torch.float32, "freqs_mhz", (F,))
+    _need(batch, torch.int32, "batch", (S, H))
+    _need(deadline_at, torch.int64, "deadline_at", (S, H))
+    _need(n_iters, torch.int32, "n_iters", (S,))
+    _need(tbt_slo_ns, torch.int64, "tbt_slo_ns", (S,))
+    _opt(proj_flags, torch.int32, "proj_flags", (S,))
+    if forest.n_features == 4:
+        _need(engine_size, torch.float32, "engine_size", (S,))
+    o = out or {}
+    dev = kv.device
+
+    def buf(name, shape, dtype):
+        t = o.get(name) if o.get(name) is not None else torch.empty(shape, dtype=dtype, device=dev)
+        return _need(t, dtype, name, shape)
+
+    ips = buf("ips_work", (S, H), torch.float32)
+    work = buf("search_work", (3, S), torch.int32)
+    idx = buf("freq_idx", (S,), torch.int32)
+    st = buf("status", (S,), torch.int32)
+    check(lib().tl_select_freq_binary(forest._h, S, F, H, _p(freqs_mhz), _p(kv), _p(batch),
+                                      _p(engine_size) if forest.n_features == 4 else None, _p(deadline_at),
+                                      _p(n_iters), _p(tbt_slo_ns), _p(proj_flags), _p(ips), _p(work), _p(idx),
+                                      _p(st), _stream()))
+    return idx, st
+
+
 # short names
 project = tl_project
 select_freq = tl_select_freq
+select_freq_binary = tl_select_freq_binary
 admit = tl_admit
 
 
@@ -325,3 +362,17 @@ class Controller:
         self.project()
         self.predict()
         return self.select()
+
+    def select_binary(self):
+        """The paper's binary search over the frequencies on the projection
+        (tl_select_freq_binary): the model only at probed frequencies."""
+        d, b = self.d, self.buf
+        if "search" not in self.__dict__:
+            S, H = d["n_scenarios"], d["horizon"]
+            dev = d["req_offset"].device
+            self.search = dict(ips_work=torch.empty((S, H), dtype=torch.float32, device=dev),
+                               search_work=torch.empty((3, S), dtype=torch.int32, device=dev),
+                               freq_idx=torch.empty(S, dtype=torch.int32, device=dev),
+                               status=torch.empty(S, dtype=torch.int32, device=dev))
+        return tl_select_freq_binary(self.forest, d["freqs_mhz"], b["kv"], b["batch"], b["deadline_at"],
+                                     b["n_iters"], d["tbt_slo_ns"], b["flags"], d["engine_size"], self.search)

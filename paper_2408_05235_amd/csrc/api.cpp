@@ -425,4 +425,60 @@ tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs,
     return from_hip(tl::launch_select(p, (hipStream_t)stream), "tl_select_freq: launch");
 }
 
+tl_status tl_select_freq_binary(const tl_forest* f, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
+                                const float* freqs_mhz, const int32_t* kv, const int32_t* batch,
+                                const float* engine_size, const uint64_t* deadline_at, const int32_t* n_iters,
+                                const uint64_t* tbt_slo_ns, const uint32_t* proj_flags, float* ips_work,
+                                int32_t* search_work, int32_t* freq_idx, uint32_t* status, void* stream) {
+    if (!f) return fail(TL_EINVAL, "tl_select_freq_binary: forest is NULL");
+    if (n_scenarios < 0 || n_scenarios > 0x7fffffffll)
+        return fail(TL_EINVAL, "tl_select_freq_binary: n_scenarios %lld outside [0, 2^31-1]", (long long)n_scenarios);
+    if (n_freqs < 1 || n_freqs > TL_MAX_FREQS)
+        return fail(TL_EINVAL, "tl_select_freq_binary: n_freqs %d outside [1, %d]", n_freqs, TL_MAX_FREQS);
+    if (horizon < 1 || horizon > TL_MAX_HORIZON)
+        return fail(TL_EINVAL, "tl_select_freq_binary: horizon %d outside [1, %d]", horizon, TL_MAX_HORIZON);
+    if (n_scenarios == 0) return ok();
+    if (!freqs_mhz || !kv || !batch || !deadline_at || !n_iters || !tbt_slo_ns || !ips_work || !search_work ||
+        !freq_idx || !status)
+        return fail(TL_EINVAL, "tl_select_freq_binary: NULL required pointer");
+    if (f->dev.n_features != 3 && f->dev.n_features != 4)
+        return fail(TL_EINVAL, "tl_select_freq_binary: the forest has %d features, the search needs 3 or 4",
+                    f->dev.n_features);
+    if (f->dev.n_features == 4 && !engine_size)
+        return fail(TL_EINVAL, "tl_select_freq_binary: 4 features need engine_size");
+    const hipStream_t st = (hipStream_t)stream;
+    tl::SearchParams sp{};
+    sp.ips = ips_work;
+    sp.S = n_scenarios;
+    sp.F = n_freqs;
+    sp.H = horizon;
+    sp.deadline_at = deadline_at;
+    sp.n_iters = n_iters;
+    sp.tbt_slo_ns = tbt_slo_ns;
+    sp.proj_flags = proj_flags;
+    sp.work = search_work;
+    sp.freq_idx = freq_idx;
+    sp.status = status;
+    tl::ColumnParams c{};
+    c.S = n_scenarios;
+    c.H = horizon;
+    c.kv = kv;
+    c.batch = batch;
+    c.freqs = freqs_mhz;
+    c.fidx = search_work + 2 * n_scenarios;
+    c.engine = engine_size;
+    c.out = ips_work;
+    int32_t rounds = 0;
+    while ((int64_t)1 << rounds < n_freqs) ++rounds;
+    hipError_t e = tl::launch_search_step(sp, 0, st);
+    for (int32_t r = 0; r < rounds && e == hipSuccess; ++r) {
+        e = tl::launch_forest_column(f->dev, c, st);
+        if (e == hipSuccess) e = tl::launch_search_step(sp, 1, st);
+    }
+    if (e == hipSuccess) e = tl::launch_search_step(sp, 3, st);
+    if (e == hipSuccess) e = tl::launch_forest_column(f->dev, c, st);
+    if (e == hipSuccess) e = tl::launch_search_step(sp, 2, st);
+    return from_hip(e, "tl_select_freq_binary: launch");
+}
+
 }  // extern "C"

@@ -1,5 +1,6 @@
 // The model M (Sec. 4.3.1) at one frequency per scenario on the projection
-// grid: out[s][j] = M(f_s, KV[s][j], B[s][j] [, E_s]).  This is the query of
+// grid: out[s][j] = M(f_s, KV[s][j], B[s][j] [, E_s]), f_s = freqs[fidx[s]]
+// (scenarios with fidx[s] < 0 are skipped) or one frequency for all.  This is the query of
 // the admission checks (Sec. 4.3.2 check 2 asks M at the maximum frequency
 // for every projected iteration) and of one probe of a search over
 // frequencies (Sec. 4.5).
@@ -44,6 +45,8 @@ __device__ __forceinline__ ColumnItem<RPL> column_item(const ColumnParams& P, in
     ColumnItem<RPL> c;
     c.valid = item < P.S * n_cols;
     c.s = c.valid ? item / n_cols : 0;
+    // a scenario without a frequency to evaluate (index < 0) is skipped
+    if (P.fidx && P.fidx[c.s] < 0) c.valid = false;
     const int32_t j0 = (int32_t)(item % n_cols) * span + lane_id();
 #pragma unroll
     for (int r = 0; r < RPL; ++r) {
@@ -55,7 +58,7 @@ __device__ __forceinline__ ColumnItem<RPL> column_item(const ColumnParams& P, in
 }
 
 __device__ __forceinline__ float column_freq(const ColumnParams& P, int64_t s) {
-    return P.fidx ? P.freqs[P.fidx[s]] : P.freq;
+    return P.fidx ? P.freqs[max(P.fidx[s], 0)] : P.freq;
 }
 
 // Walks NT consecutive staged trees (records rec_bytes apart, the first at

@@ -9,8 +9,9 @@
 // at the first violated deadline.  Feasible frequencies are collected as a
 // bitmask in LDS and the lowest one is taken.
 //
-// The admission decision of Sec. 4.3.2 uses the same arithmetic at one
-// frequency (the maximum) per scenario.
+// The admission decision of Sec. 4.3.2 and the steps of the paper's binary
+// search over frequencies use the same arithmetic at one frequency per
+// scenario.
 #include "device_util.h"
 #include "tl_internal.h"
 
@@ -85,18 +86,46 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams P) {
     }
 }
 
+// Eq. 3-4 at one frequency for one scenario, by one wavefront: with
+// per-iteration times of `ips` over the n projected iterations, returns
+// T_R[n] and whether some deadline of `dl` (T_R[j+1] < dl[j]) is missed;
+// *miss_own tells whether T_R[own_at + 1] < d_own fails (own_at < 0: none).
+// Every lane returns the same values.
+__device__ __forceinline__ uint64_t wave_times(const float* ips, const uint64_t* dl, int32_t n, int32_t own_at,
+                                               uint64_t d_own, bool* miss, bool* miss_own) {
+    const int lane = lane_id();
+    uint64_t carry = 0;
+    bool m = false, mo = false;
+    for (int32_t j0 = 0; j0 < n; j0 += kWave) {
+        const int32_t j = j0 + lane;
+        const bool in = j < n;
+        const uint64_t lat = in ? latency_ns(ips[j]) : 0ull;
+        const uint64_t tr = wave_incl_scan_u64(lat) + carry;
+        const uint64_t d = in ? dl[j] : kNoDeadline;
+        m |= in && d != kNoDeadline && !(tr < d);
+        mo |= in && j == own_at && !(tr < d_own);
+        carry = __shfl(tr, kWave - 1);
+    }
+    *miss = __ballot(m) != 0;
+    *miss_own = __ballot(mo) != 0;
+    return carry;
+}
+
+__device__ __forceinline__ bool within_tbt(uint64_t t_r_n, uint64_t slo, int32_t n) {
+    const uint64_t budget = n == 0 ? ~0ull : (slo > ~0ull / (uint64_t)n) ? ~0ull : slo * (uint64_t)n;
+    return t_r_n <= budget;
+}
+
 // Admission decision (Sec. 4.3.2 checks 1-3) of one new query per scenario
 // from the projection with it and M at the maximum frequency: one wavefront
-// per scenario walks the projected iterations 64 at a time with the same
-// per-iteration time and scan as selection; the deadline of the query itself
-// (ending at cand_len, when inside the horizon) is checked apart from the
-// scheduled requests' deadlines in deadline_at.
+// per scenario; the deadline of the query itself (ending at cand_len, when
+// inside the horizon) is checked apart from the scheduled requests'
+// deadlines in deadline_at.
 constexpr int kAdmitWaves = 4;
 
 __global__ __launch_bounds__(kAdmitWaves * kWave) void admit_kernel(AdmitParams P) {
     const int64_t s = (int64_t)blockIdx.x * kAdmitWaves + threadIdx.x / kWave;
     if (s >= P.S) return;
-    const int lane = lane_id();
     const int32_t H = P.H;
     const uint32_t fl = P.proj_flags[s];
     uint32_t dec;
@@ -113,28 +142,74 @@ __global__ __launch_bounds__(kAdmitWaves * kWave) void admit_kernel(AdmitParams 
         const int32_t L = P.cand_len[s];
         const uint64_t d_own = P.cand_deadline ? P.cand_deadline[s] : kNoDeadline;
         const int32_t own_at = (d_own != kNoDeadline && L <= H) ? L - 1 : -1;   // T_R[L] = T_R[own_at + 1]
-        const float* ips = P.ips + s * H;
-        const uint64_t* dl = P.deadline_at + s * H;
-        uint64_t carry = 0;
-        bool miss = false, miss_own = false;
-        for (int32_t j0 = 0; j0 < n; j0 += kWave) {
-            const int32_t j = j0 + lane;
-            const bool in = j < n;
-            const uint64_t lat = in ? latency_ns(ips[j]) : 0ull;
-            const uint64_t tr = wave_incl_scan_u64(lat) + carry;
-            const uint64_t d = in ? dl[j] : kNoDeadline;
-            miss |= in && d != kNoDeadline && !(tr < d);
-            miss_own |= in && j == own_at && !(tr < d_own);
-            carry = __shfl(tr, kWave - 1);
-        }
-        const uint64_t slo = P.tbt_slo_ns[s];
-        const uint64_t budget = n == 0 ? ~0ull : (slo > ~0ull / (uint64_t)n) ? ~0ull : slo * (uint64_t)n;
-        if (!(carry <= budget)) dec = TL_ADMIT_QUEUE_TBT;
-        else if (__ballot(miss)) dec = TL_ADMIT_QUEUE_E2E;
-        else if (__ballot(miss_own)) dec = TL_ADMIT_LOST;
+        bool miss, miss_own;
+        const uint64_t t_r = wave_times(P.ips + s * H, P.deadline_at + s * H, n, own_at, d_own, &miss, &miss_own);
+        if (!within_tbt(t_r, P.tbt_slo_ns[s], n)) dec = TL_ADMIT_QUEUE_TBT;
+        else if (miss) dec = TL_ADMIT_QUEUE_E2E;
+        else if (miss_own) dec = TL_ADMIT_LOST;
         else dec = TL_ADMIT_OK;
     }
-    if (lane == 0) P.decision[s] = dec;
+    if (lane_id() == 0) P.decision[s] = dec;
+}
+
+// Binary search over the candidate frequencies (Sec. 4.5), one step per
+// launch for every scenario.  State per scenario: lo, hi (the search
+// interval) and probe (the frequency index M was evaluated at, -1 = none).
+// Step: feasible at the probe -> hi = probe, else lo = probe + 1; then the
+// next probe is the midpoint while lo < hi.  The last step (final = true)
+// checks lo itself and writes the result.  Scenarios flagged overflow / lost
+// are settled by the first step (mode init) without probes.
+constexpr int kSearchWaves = 4;
+
+__global__ __launch_bounds__(kSearchWaves * kWave) void search_kernel(SearchParams P, int mode) {
+    const int64_t s = (int64_t)blockIdx.x * kSearchWaves + threadIdx.x / kWave;
+    if (s >= P.S) return;
+    const int lane = lane_id();
+    int32_t* lo = P.work;
+    int32_t* hi = P.work + P.S;
+    int32_t* probe = P.work + 2 * P.S;
+    const int32_t F = P.F, H = P.H;
+    if (mode == 0) {   // init
+        const uint32_t fl = P.proj_flags ? P.proj_flags[s] : 0u;
+        const bool settled = (fl & (TL_FLAG_OVERFLOW | TL_FLAG_LOST)) != 0;
+        if (lane == 0) {
+            lo[s] = settled ? -1 : 0;
+            hi[s] = settled ? -1 : F - 1;
+            probe[s] = (settled || F == 1) ? -1 : (F - 1) / 2;
+            if (settled) {
+                P.freq_idx[s] = F - 1;
+                P.status[s] = (fl & TL_FLAG_OVERFLOW) ? TL_STATUS_INVALID : TL_STATUS_LOST;
+            }
+        }
+        return;
+    }
+    const int32_t p = probe[s];
+    if (p < 0) return;
+    const int32_t n = min(max(P.n_iters[s], 0), H);
+    bool miss, miss_own;
+    const uint64_t t_r = wave_times(P.ips + s * H, P.deadline_at + s * H, n, -1, kNoDeadline, &miss, &miss_own);
+    const bool ok = !miss && within_tbt(t_r, P.tbt_slo_ns[s], n);
+    if (lane != 0) return;
+    if (mode == 2) {   // final check of lo
+        P.freq_idx[s] = ok ? p : F - 1;
+        P.status[s] = ok ? TL_STATUS_OK : TL_STATUS_INFEASIBLE;
+        probe[s] = -1;
+        return;
+    }
+    int32_t l = lo[s], h = hi[s];
+    if (ok) h = p;
+    else l = p + 1;
+    lo[s] = l;
+    hi[s] = h;
+    probe[s] = l < h ? l + (h - l) / 2 : -1;
+}
+
+// Before the final check every unsettled scenario probes lo.
+__global__ __launch_bounds__(256) void search_final_probe_kernel(SearchParams P) {
+    const int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (s >= P.S) return;
+    const int32_t l = P.work[s];
+    P.work[2 * P.S + s] = l;   // -1 stays -1 (settled)
 }
 
 }  // namespace
@@ -143,6 +218,17 @@ hipError_t launch_admit(const AdmitParams& p, hipStream_t stream) {
     if (p.S == 0) return hipSuccess;
     hipLaunchKernelGGL(admit_kernel, dim3((unsigned)((p.S + kAdmitWaves - 1) / kAdmitWaves)),
                        dim3(kAdmitWaves * kWave), 0, stream, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_search_step(const SearchParams& p, int mode, hipStream_t stream) {
+    if (p.S == 0) return hipSuccess;
+    if (mode == 3) {
+        hipLaunchKernelGGL(search_final_probe_kernel, dim3((unsigned)((p.S + 255) / 256)), dim3(256), 0, stream, p);
+    } else {
+        hipLaunchKernelGGL(search_kernel, dim3((unsigned)((p.S + kSearchWaves - 1) / kSearchWaves)),
+                           dim3(kSearchWaves * kWave), 0, stream, p, mode);
+    }
     return hipGetLastError();
 }
 

@@ -41,7 +41,7 @@ struct ProjectParams {
 
 // The model at one frequency per scenario on the projection grid:
 // out[s][j] = M(f_s, kv[s][j], batch[s][j] [, engine[s]]), f_s = freqs[fidx[s]]
-// or `freq` when fidx is null.
+// or `freq` when fidx is null; scenarios with fidx[s] < 0 are left alone.
 struct ColumnParams {
     int64_t S;
     int32_t H;
@@ -66,6 +66,23 @@ struct AdmitParams {
     const int32_t* cand_len;
     const uint64_t* cand_deadline;  // nullable
     uint32_t* decision;
+};
+
+// State and inputs of the binary search over frequencies: work holds lo[S],
+// hi[S] and probe[S] (the index M is evaluated at next, -1 = none); ips
+// [S][H] holds M at each scenario's probe.
+struct SearchParams {
+    const float* ips;
+    int64_t S;
+    int32_t F;
+    int32_t H;
+    const uint64_t* deadline_at;
+    const int32_t* n_iters;
+    const uint64_t* tbt_slo_ns;
+    const uint32_t* proj_flags;     // nullable
+    int32_t* work;                  // [3][S]
+    int32_t* freq_idx;
+    uint32_t* status;
 };
 
 struct SelectParams {
@@ -155,5 +172,7 @@ hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, hipStream
 hipError_t launch_select(const SelectParams& p, hipStream_t stream);
 hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream);
 hipError_t launch_admit(const AdmitParams& p, hipStream_t stream);
+// mode 0: init, 1: one search step, 3: probe lo, 2: final check
+hipError_t launch_search_step(const SearchParams& p, int mode, hipStream_t stream);
 
 }  // namespace tl
