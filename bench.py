@@ -127,6 +127,45 @@ def cpu_baseline(inp, budget_s=12.0, max_scen=64, procs=0):
     return out
 
 
+def copy_bandwidth_gbs(mib=2048, reps=5):
+    """Device-to-device copy bandwidth measured on this GPU (read + write
+    bytes per second of a plain torch copy), the practical HBM ceiling."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    del src, dst
+    return 2 * n * 4 / (best / 1e3) / 1e9
+
+
+def d2h_results_ms(ctl, reps=5):
+    """Copy of the per-scenario results (frequency index and status, S int32
+    each) to pinned host memory, reported apart from the step."""
+    import torch
+    S = ctl.d["n_scenarios"]
+    host = torch.empty((2, S), dtype=torch.int32, pin_memory=True)
+    ts = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        host[0].copy_(ctl.sel["freq_idx"], non_blocking=True)
+        host[1].copy_(ctl.sel["status"], non_blocking=True)
+        torch.cuda.synchronize()
+        ts.append((time.perf_counter() - t0) * 1e3)
+    return float(np.median(ts))
+
+
 def binary_search_bench(ctl, steps, warmup):
     """The controller as the paper states it (Sec. 4.5): binary search over the
     frequencies, the model evaluated only at probed frequencies, on the
@@ -283,6 +322,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     log(f"timed {args.steps} steps in {wall:.2f}s")
+    copy_gbs = copy_bandwidth_gbs()
 
     st = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] for e in ev])  # ms
     step_ev = np.array([e[0].elapsed_time(e[3]) for e in ev])
@@ -318,6 +358,7 @@ def main():
                    "features": inp["n_features"], "requests": int(inp["req_offset"][-1])},
         "scenarios_per_s": S / (step_ms / 1e3),
         "hbm_frac_end_to_end": tot_bytes / (step_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+        "hbm_copy_gbs_measured": copy_gbs,
         "stages_ms": {"project": stage_ms[0], "predict": stage_ms[1], "select": stage_ms[2]},
         "stages_ms_median": dict(zip(("project", "predict", "select"), np.median(st, axis=0).tolist())),
         "stages_ms_min": dict(zip(("project", "predict", "select"), st.min(axis=0).tolist())),
@@ -334,6 +375,7 @@ def main():
                      "traffic": traffic, "ops_per_row": ops_per_row,
                      "ops_note": "one fp64 leaf add per (row, tree); peak = non-packed VALU lane ops"},
     }
+    out["results_d2h_ms"] = d2h_results_ms(ctl)
     out["binary_search"] = binary_search_bench(ctl, args.steps, args.warmup)
     out["admission"] = admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup)
     if args.copy_calibration_mib:

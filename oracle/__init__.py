@@ -8,8 +8,9 @@ code with the HIP library and never imports it.
 Functions follow the paper: ``project`` (Sec. 4.2, Eq. 1-2, admission check 1
 of Sec. 4.3.2), ``rows`` and ``forest_predict`` (Sec. 4.3.1), ``select`` and
 ``select_binary`` (Sec. 4.3.2 checks 2-3, Eq. 3-4, Sec. 4.5), ``latency_ns``
-(T' = 1/T in ns), ``end_to_end`` (all three stages) and ``admit`` (the
-admission control of Sec. 4.3.2 for one new query per scenario).
+(T' = 1/T in ns), ``end_to_end`` (all three stages), ``admit`` (the
+admission control of Sec. 4.3.2 for one new query per scenario) and
+``adjust_lengths`` (the generation-length error handling of Sec. 4.6).
 """
 from __future__ import annotations
 
@@ -272,3 +273,30 @@ def admit(inp, cand_prompt, cand_len, cand_deadline_ns, max_freq_mhz, forest=Non
             continue
         dec[s] = ADMIT_OK
     return dict(proj_all, decision=dec, ips=ips_all)
+
+
+def adjust_lengths(req_offset, generated, pred_len, scale_num, scale_den, max_tokens):
+    """Remaining-token counts of the scoreboard from the predictor's total
+    generation lengths (Sec. 4.6): the prediction is inflated by the
+    scenario's factor num/den (rounded up; den = 0 means no inflation) and
+    limited to max_tokens; a request that has already generated at least that
+    many tokens is updated to max_tokens.  remaining = max(length - generated,
+    1).  max_tokens < 1 means no limit.  Entries with generated < 0 or a
+    predicted length < 1 get 0 (the projection ignores them as malformed)."""
+    off = np.asarray(req_offset, np.int64)
+    out = np.zeros(int(off[-1]) if off.size else 0, np.int32)
+    for s in range(off.size - 1):
+        num, den, mt = int(scale_num[s]), int(scale_den[s]), int(max_tokens[s])
+        for i in range(int(off[s]), int(off[s + 1])):
+            g, r = int(generated[i]), int(pred_len[i])
+            if g < 0 or r < 1:
+                out[i] = 0
+                continue
+            length = -(-(r * num) // den) if den > 0 else r
+            length = min(length, 2 ** 31 - 1)
+            if mt >= 1:
+                length = min(length, mt)
+                if g >= length:
+                    length = mt
+            out[i] = max(length - g, 1)
+    return out

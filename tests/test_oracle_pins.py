@@ -682,3 +682,44 @@ def test_admission_monotone_in_slo_and_own_deadline():
         later = NONE if dc == NONE else np.uint64(int(dc) + 50_000_000)
         d2 = int(oracle.admit(inp, [p], [L], np.array([later], np.uint64), fmax, forest)["decision"][0])
         assert d2 == d0 or (d0 == oracle.ADMIT_LOST and d2 == oracle.ADMIT_OK)
+
+
+# ------------------------------------ generation-length errors (Sec. 4.6)
+
+def test_adjust_lengths_hand_values():
+    """Hand-computed entries: inflation rounded up, the max_tokens limit, the
+    overrun reset to max_tokens, and malformed entries."""
+    # scenario 0: factor 3/2, max 100; scenario 1: factor 1, max 64;
+    # scenario 2: factor 2, max 150; scenario 3: no inflation (den 0), no limit
+    off = [0, 3, 6, 8, 11]
+    gen = [10, 0, 5,    30, 70, 3,    0, 149,    4, -1, 2]
+    pred = [15, 1, 7,   20, 20, 60,   100, 90,   9, 5, 0]
+    num, den, mt = [3, 1, 2, 7], [2, 1, 1, 0], [100, 64, 150, 0]
+    want = [
+        13,   # ceil(15 * 1.5) = 23 tokens, 10 generated
+        2,    # ceil(1.5) = 2
+        6,    # ceil(10.5) = 11, 5 generated
+        34,   # 20 tokens but 30 generated: overrun -> 64 - 30
+        1,    # overrun -> 64, already past it: ends now
+        57,   # 60 - 3, no inflation at factor 1
+        150,  # 200 limited to 150
+        1,    # 180 -> 150, 149 generated
+        5,    # den 0: 9 - 4
+        0,    # negative generated count: malformed
+        0,    # predicted length 0: malformed
+    ]
+    got = oracle.adjust_lengths(off, gen, pred, num, den, mt)
+    assert got.tolist() == want
+
+
+def test_adjust_lengths_identity_and_monotone():
+    rng = np.random.default_rng(3)
+    n = 500
+    gen = rng.integers(0, 300, n)
+    pred = gen + rng.integers(1, 300, n)
+    off = [0, n]
+    # factor 1 without a limit leaves the scoreboard's remaining counts
+    assert oracle.adjust_lengths(off, gen, pred, [5], [5], [0]).tolist() == (pred - gen).tolist()
+    base = oracle.adjust_lengths(off, gen, pred, [11], [10], [1 << 20])
+    more = oracle.adjust_lengths(off, gen, pred, [13], [10], [1 << 20])
+    assert np.all(more >= base) and np.all(base >= pred - gen) and np.all(base >= 1)
