@@ -135,6 +135,24 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
 void tl_forest_destroy(tl_forest* forest);   /* NULL is ignored; synchronizes the device */
 
 /* ------------------------------------------------------------------------
+ * Scoreboard lengths under generation-length errors (Sec. 4.6): the
+ * remaining-token counts tl_project takes, from the predictor's total
+ * generation lengths.  Per request i of scenario s (CSR req_offset as in
+ * tl_project):
+ *   len = ceil(pred_len[i] * scale_num[s] / scale_den[s])   (scale_den 0: pred_len)
+ *   len = min(len, max_tokens[s]);  if generated[i] >= len: len = max_tokens[s]
+ *                                                   (both only when max_tokens[s] >= 1)
+ *   remaining_out[i] = max(len - generated[i], 1)
+ * Entries with generated < 0 or pred_len < 1 get 0, which tl_project ignores
+ * as malformed.  Scenarios whose request range is invalid are not written.
+ * remaining_out may alias neither input.
+ * ---------------------------------------------------------------------- */
+tl_status tl_adjust_lengths(int64_t n_scenarios, int64_t n_requests, const int64_t* req_offset,
+                            const int32_t* generated, const int32_t* pred_len, const uint32_t* scale_num,
+                            const uint32_t* scale_den, const int32_t* max_tokens, int32_t* remaining_out,
+                            void* stream);
+
+/* ------------------------------------------------------------------------
  * Stage 1 -- KV usage and batch-size projection (Sec. 4.2, Eq. 1-2).
  *
  * Scenario s owns requests req_offset[s] .. req_offset[s+1]-1 (a scoreboard,

@@ -23,7 +23,7 @@ MAX_HORIZON, MAX_BLOCK_TOKENS, MAX_FREQS, MAX_FEATURES, MAX_DEPTH = 8192, 65536,
 
 EXPORTED = ("tl_abi_version", "tl_last_error", "tl_forest_create", "tl_forest_destroy",
             "tl_project", "tl_forest_predict", "tl_forest_predict_grid", "tl_select_freq", "tl_admit",
-            "tl_select_freq_binary")
+            "tl_select_freq_binary", "tl_adjust_lengths")
 
 
 class ProjectArgs(ctypes.Structure):
@@ -83,6 +83,8 @@ def lib():
     L.tl_select_freq.restype = ctypes.c_int
     L.tl_select_freq_binary.argtypes = [P, i64, i32, i32] + [P] * 13
     L.tl_select_freq_binary.restype = ctypes.c_int
+    L.tl_adjust_lengths.argtypes = [i64, i64] + [P] * 8
+    L.tl_adjust_lengths.restype = ctypes.c_int
     L.tl_admit.argtypes = [ctypes.POINTER(AdmitArgs), P]
     L.tl_admit.restype = ctypes.c_int
     _lib = L

@@ -281,11 +281,31 @@ def tl_select_freq_binary(forest, freqs_mhz, kv, batch, deadline_at, n_iters, tb
     return idx, st
 
 
+def tl_adjust_lengths(req_offset, generated, pred_len, scale_num, scale_den, max_tokens, out=None):
+    """Scoreboard remaining-token counts from predicted total lengths under
+    generation-length errors (tl_adjust_lengths).  Per-scenario scale_num,
+    scale_den (int32 tensors holding uint32 bits) and max_tokens.  Returns
+    remaining [R] int32."""
+    _need(req_offset, torch.int64, "req_offset")
+    S = req_offset.numel() - 1
+    R = generated.numel()
+    _need(generated, torch.int32, "generated", (R,))
+    _need(pred_len, torch.int32, "pred_len", (R,))
+    for name, t in (("scale_num", scale_num), ("scale_den", scale_den), ("max_tokens", max_tokens)):
+        _need(t, torch.int32, name, (S,))
+    rem = out if out is not None else torch.empty(R, dtype=torch.int32, device=req_offset.device)
+    _need(rem, torch.int32, "out", (R,))
+    check(lib().tl_adjust_lengths(S, R, _p(req_offset), _p(generated), _p(pred_len), _p(scale_num),
+                                  _p(scale_den), _p(max_tokens), _p(rem), _stream()))
+    return rem
+
+
 # short names
 project = tl_project
 select_freq = tl_select_freq
 select_freq_binary = tl_select_freq_binary
 admit = tl_admit
+adjust_lengths = tl_adjust_lengths
 
 
 def upload(inp, device="cuda"):

@@ -425,6 +425,31 @@ tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs,
     return from_hip(tl::launch_select(p, (hipStream_t)stream), "tl_select_freq: launch");
 }
 
+tl_status tl_adjust_lengths(int64_t n_scenarios, int64_t n_requests, const int64_t* req_offset,
+                            const int32_t* generated, const int32_t* pred_len, const uint32_t* scale_num,
+                            const uint32_t* scale_den, const int32_t* max_tokens, int32_t* remaining_out,
+                            void* stream) {
+    if (n_scenarios < 0 || n_scenarios > 0x7fffffffll)
+        return fail(TL_EINVAL, "tl_adjust_lengths: n_scenarios %lld outside [0, 2^31-1]", (long long)n_scenarios);
+    if (n_requests < 0) return fail(TL_EINVAL, "tl_adjust_lengths: n_requests < 0");
+    if (n_scenarios == 0) return ok();
+    if (!req_offset || !scale_num || !scale_den || !max_tokens)
+        return fail(TL_EINVAL, "tl_adjust_lengths: NULL required pointer");
+    if (n_requests > 0 && (!generated || !pred_len || !remaining_out))
+        return fail(TL_EINVAL, "tl_adjust_lengths: NULL request array");
+    tl::AdjustParams p{};
+    p.S = n_scenarios;
+    p.n_requests = n_requests;
+    p.off = req_offset;
+    p.gen = generated;
+    p.pred = pred_len;
+    p.num = scale_num;
+    p.den = scale_den;
+    p.max_tokens = max_tokens;
+    p.out = remaining_out;
+    return from_hip(tl::launch_adjust(p, (hipStream_t)stream), "tl_adjust_lengths: launch");
+}
+
 tl_status tl_select_freq_binary(const tl_forest* f, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
                                 const float* freqs_mhz, const int32_t* kv, const int32_t* batch,
                                 const float* engine_size, const uint64_t* deadline_at, const int32_t* n_iters,

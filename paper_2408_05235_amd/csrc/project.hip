@@ -439,7 +439,46 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     }
 }
 
+// Remaining-token counts from the predictor's total lengths (Sec. 4.6):
+// inflate by num/den (rounded up; den = 0: none), limit to max_tokens, reset
+// to max_tokens past an outrun prediction, remaining = max(length - gen, 1);
+// malformed entries get 0.  One wavefront per scenario, 64 entries a step.
+constexpr int kAdjustWaves = 4;
+
+__global__ __launch_bounds__(kAdjustWaves * kWave) void adjust_kernel(AdjustParams P) {
+    const int64_t s = (int64_t)blockIdx.x * kAdjustWaves + threadIdx.x / kWave;
+    if (s >= P.S) return;
+    const int64_t lo = P.off[s], hi = P.off[s + 1];
+    if (lo < 0 || hi < lo || hi > P.n_requests) return;
+    const uint32_t num = P.num[s], den = P.den[s];
+    const int32_t mt = P.max_tokens[s];
+    for (int64_t i = lo + lane_id(); i < hi; i += kWave) {
+        const int32_t g = P.gen[i], r = P.pred[i];
+        int32_t out = 0;
+        if (g >= 0 && r >= 1) {
+            int64_t len = r;
+            if (den > 0) {
+                const uint64_t x = (uint64_t)r * num;
+                len = (int64_t)min((x + den - 1) / den, (uint64_t)0x7fffffff);
+            }
+            if (mt >= 1) {
+                len = min(len, (int64_t)mt);
+                if (g >= len) len = mt;
+            }
+            out = (int32_t)max(len - g, (int64_t)1);
+        }
+        P.out[i] = out;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_adjust(const AdjustParams& p, hipStream_t stream) {
+    if (p.S == 0) return hipSuccess;
+    hipLaunchKernelGGL(adjust_kernel, dim3((unsigned)((p.S + kAdjustWaves - 1) / kAdjustWaves)),
+                       dim3(kAdjustWaves * kWave), 0, stream, p);
+    return hipGetLastError();
+}
 
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream) {
     const size_t lds = (size_t)3 * p.H * sizeof(int32_t);

@@ -85,6 +85,19 @@ struct SearchParams {
     uint32_t* status;
 };
 
+// Scoreboard lengths from predicted lengths (Sec. 4.6).
+struct AdjustParams {
+    int64_t S;
+    int64_t n_requests;
+    const int64_t* off;
+    const int32_t* gen;
+    const int32_t* pred;
+    const uint32_t* num;
+    const uint32_t* den;
+    const int32_t* max_tokens;
+    int32_t* out;
+};
+
 struct SelectParams {
     const float* ips;
     int64_t S;
@@ -166,6 +179,7 @@ struct GridParams {
 };
 
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
+hipError_t launch_adjust(const AdjustParams& p, hipStream_t stream);
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,
                               hipStream_t stream);
 hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, hipStream_t stream);

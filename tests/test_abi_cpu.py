@@ -121,6 +121,29 @@ def test_admit_rejects_bad_arguments(kw, needle):
     assert L.tl_admit(None, None) == _lib.TL_EINVAL
 
 
+def test_adjust_lengths_rejects_bad_arguments():
+    L = _lib.lib()
+    d = ctypes.c_void_p(16)
+    assert L.tl_adjust_lengths(-1, 0, d, d, d, d, d, d, d, None) == _lib.TL_EINVAL
+    assert L.tl_adjust_lengths(1, -1, d, d, d, d, d, d, d, None) == _lib.TL_EINVAL
+    assert L.tl_adjust_lengths(1, 5, None, d, d, d, d, d, d, None) == _lib.TL_EINVAL
+    assert L.tl_adjust_lengths(1, 5, d, None, d, d, d, d, d, None) == _lib.TL_EINVAL
+    assert "NULL request array" in L.tl_last_error().decode()
+    assert L.tl_adjust_lengths(0, 0, None, None, None, None, None, None, None, None) == _lib.TL_OK
+
+
+def test_binary_search_rejects_bad_arguments():
+    L = _lib.lib()
+    d = ctypes.c_void_p(16)
+    args = [d, 1, 4, 8] + [d] * 12 + [None]
+    for pos, bad, needle in ((0, None, "forest is NULL"), (1, -1, "n_scenarios"), (2, 0, "n_freqs"),
+                             (2, 4097, "n_freqs"), (3, 0, "horizon"), (4, None, "NULL required pointer")):
+        a = list(args)
+        a[pos] = bad
+        assert L.tl_select_freq_binary(*a) == _lib.TL_EINVAL
+        assert needle in L.tl_last_error().decode()
+
+
 def test_forest_create_rejects_bad_trees():
     L = _lib.lib()
     h = ctypes.c_void_p(123)
