@@ -166,6 +166,36 @@ def d2h_results_ms(ctl, reps=5):
     return float(np.median(ts))
 
 
+def adjust_lengths_bench(inp, dev_in, steps, copy_gbs):
+    """The scoreboard stage of Sec. 4.6 (predicted lengths inflated by 11/10,
+    limited to 4096 tokens) over every request of the workload; HBM-bound:
+    8 bytes read and 4 written per request, 16 read per scenario."""
+    import torch
+
+    from paper_2408_05235_amd import api
+    S, R = inp["n_scenarios"], int(inp["req_offset"][-1])
+    d = dev_in
+    pred = (d["generated"].to(torch.int64) + d["remaining"]).to(torch.int32)
+    num = torch.full((S,), 11, dtype=torch.int32, device="cuda:0")
+    den = torch.full((S,), 10, dtype=torch.int32, device="cuda:0")
+    mt = torch.full((S,), 4096, dtype=torch.int32, device="cuda:0")
+    out = torch.empty(R, dtype=torch.int32, device="cuda:0")
+    api.tl_adjust_lengths(d["req_offset"], d["generated"], pred, num, den, mt, out)
+    torch.cuda.synchronize()
+    ev = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        api.tl_adjust_lengths(d["req_offset"], d["generated"], pred, num, den, mt, out)
+        e1.record()
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    byt = 12 * R + 16 * S
+    return {"requests": R, "ms_median": ms, "gbs": byt / (ms / 1e3) / 1e9,
+            "frac_of_copy": byt / (ms / 1e3) / 1e9 / copy_gbs, "frac_of_hbm_peak": byt / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}
+
+
 def binary_search_bench(ctl, steps, warmup):
     """The controller as the paper states it (Sec. 4.5): binary search over the
     frequencies, the model evaluated only at probed frequencies, on the
@@ -376,6 +406,7 @@ def main():
                      "ops_note": "one fp64 leaf add per (row, tree); peak = non-packed VALU lane ops"},
     }
     out["results_d2h_ms"] = d2h_results_ms(ctl)
+    out["adjust_lengths"] = adjust_lengths_bench(inp, dev_in, args.steps, copy_gbs)
     out["binary_search"] = binary_search_bench(ctl, args.steps, args.warmup)
     out["admission"] = admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup)
     if args.copy_calibration_mib:
