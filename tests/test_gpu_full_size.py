@@ -1,6 +1,8 @@
 """Parity at the five workloads' full sizes, in the configuration bench.py
 times (fused grid prediction), on outputs the oracle can afford: a few whole
-scenarios end to end, sampled rows, and properties over every scenario."""
+scenarios end to end, the selection stage on every scenario (the oracle's
+selection on the GPU's IPS), a million random forest rows (400 000 on the
+2000-tree workload), and properties over every scenario."""
 import time
 
 import numpy as np
@@ -68,6 +70,33 @@ def test_full_size(gpu, ci):
         assert np.allclose(got, o["ips"][0], rtol=RTOL, atol=0) and exact == got.size, (s, exact)
         assert (idx[s], st[s]) == (o["freq_idx"][0], o["status"][0]), s
     print(f"{cfg['name']}: end-to-end scenarios ok {time.time() - t0:.1f}s", flush=True)
+
+    # the selection stage on every scenario (c4: a block of 2048 scenarios):
+    # the oracle's selection on the GPU's own projections and IPS
+    blk = slice(0, S) if S * F * H <= 300_000_000 else slice(4096, 4096 + 2048)
+    ips_all = _np(ctl.ips[blk])
+    oi, os_ = oracle.select(ips_all, dl[blk], n_iters[blk], inp["tbt_slo_ns"][blk], flags[blk])
+    assert np.array_equal(idx[blk], oi) and np.array_equal(st[blk], os_), \
+        np.nonzero((idx[blk] != oi) | (st[blk] != os_))[0][:5]
+    print(f"{cfg['name']}: selection on {ips_all.shape[0]} scenarios ok {time.time() - t0:.1f}s", flush=True)
+    del ips_all
+
+    # the forest stage on random (scenario, frequency, iteration) rows built
+    # from the GPU's own curves (c3, 2000 trees of depth 10: 400 000 rows)
+    n_rows = min(S * F * H, 400_000 if ci == 3 else 1_000_000)
+    rs = rng.integers(0, S, n_rows)
+    rf = rng.integers(0, F, n_rows)
+    rj = rng.integers(0, H, n_rows)
+    cols = [inp["freqs_mhz"][rf], kv[rs, rj].astype(np.float32), batch[rs, rj].astype(np.float32)]
+    if inp["n_features"] == 4:
+        cols.append(inp["engine_size"][rs])
+    want = oracle.forest_predict(inp["forest"], np.stack(cols, axis=1).astype(np.float32))
+    import torch
+    flat = ctl.ips.reshape(-1)
+    pos = torch.from_numpy((rs * F + rf) * H + rj).cuda()
+    got = _np(flat[pos])
+    assert np.array_equal(got, want), int((got != want).sum())
+    print(f"{cfg['name']}: {n_rows} random rows ok {time.time() - t0:.1f}s", flush=True)
 
     # properties over every scenario
     assert np.all((st == oracle.STATUS_LOST) == ((flags & oracle.FLAG_LOST) != 0))
