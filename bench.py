@@ -10,7 +10,8 @@ batch of synthetic scenarios already resident in HBM.
 Prints one JSON line: whole-step throughput, per-stage HIP-event times (mean,
 median, min over the K timed steps), the forest kernel's roofline record, the
 oracle's CPU baseline (one thread, and C single-threaded processes), the
-paper's binary-search controller on the same projection, and the
+paper's binary-search controller on the same projection, the model compiled
+to its input lattice (a separate mode with a one-time build), and the
 admission-control what-ifs (one new query per scenario) on the same workload.
 """
 import argparse
@@ -194,6 +195,74 @@ def adjust_lengths_bench(inp, dev_in, steps, copy_gbs):
     byt = 12 * R + 16 * S
     return {"requests": R, "ms_median": ms, "gbs": byt / (ms / 1e3) / 1e9,
             "frac_of_copy": byt / (ms / 1e3) / 1e9 / copy_gbs, "frac_of_hbm_peak": byt / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}
+
+
+LATTICE_FILE = os.path.join(ROOT, "profiles", "lattice_{}_traffic.json")
+
+
+def lattice_bench(inp, cfg, ctl, steps, warmup, max_gib=24):
+    """The model compiled to its input lattice (a separate mode, not the
+    headline): one-time build over (engine sizes x batch 0..max x the F
+    frequencies x KV 0..capacity), then the step's prediction as a table
+    lookup with identical values.  Reports the build time, the lookup's
+    HIP-event time, the step with it (project + lookup + select), and the
+    lookup kernel's HBM roofline (algorithmic bytes: 4 written + 4 read per
+    row, 8 per (scenario, iteration))."""
+    import torch
+
+    from paper_2408_05235_amd import api
+    S, H, F = inp["n_scenarios"], inp["horizon"], inp["n_freqs"]
+    kv_max = int(cfg["kv_capacity"])
+    b_max = int(ctl.buf["batch"].max().item())
+    engines = [1.0, 2.0, 4.0, 8.0] if inp["n_features"] == 4 else None
+    n_e = len(engines) if engines else 1
+    gib = n_e * (b_max + 1) * F * 4096 * (kv_max // 4096 + 1) * 4 / 2 ** 30
+    if gib > max_gib:
+        return {"skipped": f"table would take {gib:.1f} GiB (bench limit {max_gib})"}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    lat = api.Lattice(ctl.forest, ctl.d["freqs_mhz"], kv_max, b_max, engines)
+    torch.cuda.synchronize()
+    build_s = time.perf_counter() - t0
+    out = torch.empty_like(ctl.ips)
+    call = lambda: lat.tl_lattice_predict_grid(ctl.buf["kv"], ctl.buf["batch"], ctl.d["engine_size"], out)
+    for _ in range(max(1, warmup)):
+        call()
+    torch.cuda.synchronize()
+    same = bool(torch.equal(out, ctl.ips))
+    ev = []
+    for _ in range(steps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record()
+        ctl.project()
+        e[1].record()
+        call()
+        e[2].record()
+        tl_sel = api.tl_select_freq(out, ctl.buf["deadline_at"], ctl.buf["n_iters"], ctl.d["tbt_slo_ns"],
+                                    ctl.buf["flags"], ctl.sel)
+        e[3].record()
+        ev.append(e)
+    torch.cuda.synchronize()
+    st = np.array([[x[i].elapsed_time(x[i + 1]) for i in range(3)] for x in ev])
+    step_ms = float(np.median(st.sum(axis=1)))
+    look_ms = float(np.median(st[:, 1]))
+    rows = S * F * H
+    byt = 8 * rows + 8 * S * H
+    achieved = byt / (look_ms / 1e3) / 1e9
+    traffic = None
+    path = LATTICE_FILE.format(cfg["name"].split("_")[0])
+    if os.path.exists(path):
+        rec = json.load(open(path))
+        src = open(os.path.join(ROOT, "paper_2408_05235_amd", "csrc", "lattice.hip"), "rb").read()
+        if rec.get("lattice_hip_sha256") == hashlib.sha256(src).hexdigest():
+            traffic = rec.get("bytes_per_launch")
+    res = {"table_gib": lat.nbytes / 2 ** 30, "build_s": build_s, "bounds": {"kv_max": kv_max, "batch_max": b_max},
+           "lookup_ms": look_ms, "step_ms": step_ms, "rows_per_s": rows / (step_ms / 1e3),
+           "same_ips_as_direct": same,
+           "roofline": {"kernel": "lattice_gather_kernel", "bound": "hbm", "achieved": achieved,
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic}}
+    lat.close()
+    return res
 
 
 def binary_search_bench(ctl, steps, warmup):
@@ -407,6 +476,7 @@ def main():
     }
     out["results_d2h_ms"] = d2h_results_ms(ctl)
     out["adjust_lengths"] = adjust_lengths_bench(inp, dev_in, args.steps, copy_gbs)
+    out["lattice"] = lattice_bench(inp, cfg, ctl, args.steps, args.warmup)
     out["binary_search"] = binary_search_bench(ctl, args.steps, args.warmup)
     out["admission"] = admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup)
     if args.copy_calibration_mib:

@@ -242,6 +242,38 @@ tl_status tl_forest_predict_grid(const tl_forest* forest, int64_t n_scenarios, i
                                  void* stream);
 
 /* ------------------------------------------------------------------------
+ * Stage 2 through a table: the model compiled to its discrete input lattice.
+ * The controller queries M only at a fixed list of frequencies, a few engine
+ * sizes, integer batch sizes and integer KV blocks (Sec. 4.3.1 notes that
+ * all inputs are bounded), so M can be evaluated once at every lattice point
+ * and prediction becomes a table lookup:
+ *   tl_lattice_create evaluates M (with tl_forest_predict_grid's kernels, so
+ *   every value is the tree-order fp64 sum a walk gives) at every
+ *   (engine size, batch 0..batch_max, frequency, KV 0..kv_max); the table
+ *   takes n_engines x (batch_max + 1) x n_freqs x 4096 x ceil((kv_max + 1) /
+ *   4096) x 4 bytes (tl_lattice_bytes), at most 256 GiB.
+ *   tl_lattice_predict_grid gives out[s][f][j] exactly as
+ *   tl_forest_predict_grid with the lattice's frequencies: lattice points are
+ *   read from the table, other rows (KV or batch outside [0, max], an engine
+ *   size not in the list) are walked.
+ * freqs_mhz: device [n_freqs], copied.  engine_values: host
+ * [n_engines <= 16], required for 4-feature forests (ignored otherwise).
+ * The build is enqueued on `stream`; the forest must outlive the lattice.
+ * Errors: TL_EINVAL, TL_EUNSUPPORTED (table too large), TL_ENOMEM,
+ * TL_EDEVICE.
+ * ---------------------------------------------------------------------- */
+typedef struct tl_lattice tl_lattice;
+
+tl_status tl_lattice_create(const tl_forest* forest, int32_t n_freqs, const float* freqs_mhz, int32_t n_engines,
+                            const float* engine_values, int32_t kv_max, int32_t batch_max, void* stream,
+                            tl_lattice** out);
+void tl_lattice_destroy(tl_lattice* lattice);   /* NULL is ignored; synchronizes the device */
+uint64_t tl_lattice_bytes(const tl_lattice* lattice);
+tl_status tl_lattice_predict_grid(const tl_lattice* lattice, int64_t n_scenarios, int32_t horizon,
+                                  const int32_t* kv, const int32_t* batch, const float* engine_size, float* out,
+                                  void* stream);
+
+/* ------------------------------------------------------------------------
  * Stage 3 -- frequency selection (Sec. 4.5 with Sec. 4.3.2 checks 2-3).
  *
  * ips [S][F][H] fp32: predicted iterations/s of scenario s at frequency f in

@@ -23,7 +23,8 @@ MAX_HORIZON, MAX_BLOCK_TOKENS, MAX_FREQS, MAX_FEATURES, MAX_DEPTH = 8192, 65536,
 
 EXPORTED = ("tl_abi_version", "tl_last_error", "tl_forest_create", "tl_forest_destroy",
             "tl_project", "tl_forest_predict", "tl_forest_predict_grid", "tl_select_freq", "tl_admit",
-            "tl_select_freq_binary", "tl_adjust_lengths")
+            "tl_select_freq_binary", "tl_adjust_lengths", "tl_lattice_create", "tl_lattice_destroy",
+            "tl_lattice_bytes", "tl_lattice_predict_grid")
 
 
 class ProjectArgs(ctypes.Structure):
@@ -83,6 +84,14 @@ def lib():
     L.tl_select_freq.restype = ctypes.c_int
     L.tl_select_freq_binary.argtypes = [P, i64, i32, i32] + [P] * 13
     L.tl_select_freq_binary.restype = ctypes.c_int
+    L.tl_lattice_create.argtypes = [P, i32, P, i32, P, i32, i32, P, ctypes.POINTER(P)]
+    L.tl_lattice_create.restype = ctypes.c_int
+    L.tl_lattice_destroy.argtypes = [P]
+    L.tl_lattice_destroy.restype = None
+    L.tl_lattice_bytes.argtypes = [P]
+    L.tl_lattice_bytes.restype = ctypes.c_uint64
+    L.tl_lattice_predict_grid.argtypes = [P, i64, i32, P, P, P, P, P]
+    L.tl_lattice_predict_grid.restype = ctypes.c_int
     L.tl_adjust_lengths.argtypes = [i64, i64] + [P] * 8
     L.tl_adjust_lengths.restype = ctypes.c_int
     L.tl_admit.argtypes = [ctypes.POINTER(AdmitArgs), P]

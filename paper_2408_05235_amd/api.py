@@ -224,6 +224,53 @@ class Forest:
             pass
 
 
+class Lattice:
+    """The model compiled to its input lattice (tl_lattice_create): every
+    (engine size, batch 0..batch_max, frequency, KV 0..kv_max) evaluated once;
+    prediction on the projection grid is then a table lookup with the same
+    values (tl_lattice_predict_grid).  Keeps the forest alive."""
+
+    def __init__(self, forest, freqs_mhz, kv_max, batch_max, engine_values=None):
+        _need(freqs_mhz, torch.float32, "freqs_mhz")
+        self.forest = forest
+        self.n_freqs = int(freqs_mhz.numel())
+        ev = np.ascontiguousarray(engine_values if engine_values is not None else [], dtype=np.float32)
+        h = ctypes.c_void_p()
+        check(lib().tl_lattice_create(forest._h, self.n_freqs, _p(freqs_mhz), int(ev.size),
+                                      ev.ctypes.data_as(ctypes.c_void_p) if ev.size else None, int(kv_max),
+                                      int(batch_max), _stream(), ctypes.byref(h)))
+        self._h = h
+        self.nbytes = int(lib().tl_lattice_bytes(h))
+
+    def tl_lattice_predict_grid(self, kv, batch, engine_size=None, out=None):
+        """IPS [S, F, H] for the projection curves kv, batch [S, H] int32."""
+        _need(kv, torch.int32, "kv")
+        if kv.dim() != 2:
+            raise ValueError("kv must be [S, H]")
+        S, H = kv.shape
+        _need(batch, torch.int32, "batch", (S, H))
+        if self.forest.n_features == 4:
+            _need(engine_size, torch.float32, "engine_size", (S,))
+        if out is None:
+            out = torch.empty((S, self.n_freqs, H), dtype=torch.float32, device=kv.device)
+        _need(out, torch.float32, "out", (S, self.n_freqs, H))
+        check(lib().tl_lattice_predict_grid(self._h, S, H, _p(kv), _p(batch),
+                                            _p(engine_size) if self.forest.n_features == 4 else None, _p(out),
+                                            _stream()))
+        return out
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().tl_lattice_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 def tl_select_freq(ips, deadline_at, n_iters, tbt_slo_ns, proj_flags=None, out=None):
     """Stage 3 (tl_select_freq).  ips [S,F,H] fp32.  Returns (freq_idx int32
     [S], status int32 [S])."""

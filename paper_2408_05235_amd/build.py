@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_DIR = os.path.join(PKG, "lib")
 LIB_PATH = os.path.join(LIB_DIR, "libtl.so")
-SOURCES = ["api.cpp", "project.hip", "forest.hip", "column.hip", "select.hip"]
+SOURCES = ["api.cpp", "project.hip", "forest.hip", "column.hip", "lattice.hip", "select.hip"]
 HEADERS = ["device_util.h", "tl_internal.h", "forest_walk.h"]
 
 HIPCC_FLAGS = [

@@ -24,6 +24,14 @@ struct tl_forest {
     void* cuts_mem;   // [kMaxCuts] KV cuts, then [kMaxCuts] batch cuts
 };
 
+struct tl_lattice {
+    int device;
+    const tl_forest* forest;
+    tl::LatticeDev dev;
+    void* mem;        // [F] frequencies (padded to 256 bytes), then the table
+    uint64_t bytes;
+};
+
 namespace {
 
 thread_local char g_err[512] = "";
@@ -423,6 +431,134 @@ tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs,
     p.freq_idx = freq_idx;
     p.status = status;
     return from_hip(tl::launch_select(p, (hipStream_t)stream), "tl_select_freq: launch");
+}
+
+tl_status tl_lattice_create(const tl_forest* f, int32_t n_freqs, const float* freqs_mhz, int32_t n_engines,
+                            const float* engine_values, int32_t kv_max, int32_t batch_max, void* stream,
+                            tl_lattice** out) {
+    if (!out) return fail(TL_EINVAL, "tl_lattice_create: out is NULL");
+    *out = nullptr;
+    if (!f) return fail(TL_EINVAL, "tl_lattice_create: forest is NULL");
+    const int32_t nf = f->dev.n_features;
+    if (nf != 3 && nf != 4)
+        return fail(TL_EINVAL, "tl_lattice_create: the forest has %d features, the lattice needs 3 or 4", nf);
+    if (n_freqs < 1 || n_freqs > TL_MAX_FREQS)
+        return fail(TL_EINVAL, "tl_lattice_create: n_freqs %d outside [1, %d]", n_freqs, TL_MAX_FREQS);
+    if (!freqs_mhz) return fail(TL_EINVAL, "tl_lattice_create: freqs_mhz is NULL");
+    if (nf == 4 && (n_engines < 1 || n_engines > tl::kMaxLatticeEngines || !engine_values))
+        return fail(TL_EINVAL, "tl_lattice_create: a 4-feature forest needs 1..%d engine sizes",
+                    tl::kMaxLatticeEngines);
+    if (kv_max < 0 || batch_max < 0 || batch_max >= (1 << 20))
+        return fail(TL_EINVAL, "tl_lattice_create: kv_max %d / batch_max %d outside range", kv_max, batch_max);
+    tl::LatticeDev L{};
+    L.nf = nf;
+    L.F = n_freqs;
+    L.nE = nf == 4 ? n_engines : 1;
+    L.nB = batch_max + 1;
+    L.nC = kv_max / tl::kLatticeChunk + 1;
+    L.kv_max = kv_max;
+    L.batch_max = batch_max;
+    for (int32_t q = 0; q < tl::kMaxLatticeEngines; ++q) L.engines[q] = (nf == 4 && q < n_engines) ? engine_values[q] : 0.0f;
+    const uint64_t n_scen = (uint64_t)L.nE * L.nB * L.nC;
+    const uint64_t entries = n_scen * (uint64_t)L.F * tl::kLatticeChunk;
+    const uint64_t bytes = entries * 4u;
+    if (n_scen > 0x7fffffffull || bytes > (256ull << 30))
+        return fail(TL_EUNSUPPORTED, "tl_lattice_create: the table would take %llu bytes (limit 256 GiB)",
+                    (unsigned long long)bytes);
+    const uint64_t freq_bytes = ((uint64_t)n_freqs * 4u + 255u) & ~255ull;
+    tl_lattice* lat = new (std::nothrow) tl_lattice{};
+    if (!lat) return fail(TL_ENOMEM, "tl_lattice_create: host allocation failed");
+    lat->forest = f;
+    lat->bytes = bytes;
+    const hipStream_t st = (hipStream_t)stream;
+    hipError_t e = hipGetDevice(&lat->device);
+    if (e == hipSuccess) e = hipMalloc(&lat->mem, freq_bytes + bytes);
+    if (e != hipSuccess) {
+        delete lat;
+        return from_hip(e, "tl_lattice_create: device allocation");
+    }
+    float* freqs = (float*)lat->mem;
+    L.freqs = freqs;
+    L.table = (const float*)((unsigned char*)lat->mem + freq_bytes);
+    lat->dev = L;
+    // build: one grid scenario per (engine size, batch, KV chunk), in batches
+    // of scenarios through a temporary of at most ~512 MB, each transposed
+    // into the table
+    void* work = nullptr;
+    const uint64_t per_scen = (uint64_t)n_freqs * tl::kLatticeChunk * 4u;
+    const uint64_t batch_n = std::max<uint64_t>(1, std::min<uint64_t>(n_scen, (512ull << 20) / per_scen));
+    e = hipMemcpyAsync(freqs, freqs_mhz, (size_t)n_freqs * 4u, hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess)
+        e = hipMallocAsync(&work, batch_n * (per_scen + tl::kLatticeChunk * 8u + 4u) + 256u, st);
+    if (e == hipSuccess) {
+        float* grid_out = (float*)work;
+        int32_t* kv = (int32_t*)(grid_out + batch_n * n_freqs * tl::kLatticeChunk);
+        int32_t* batch = kv + batch_n * tl::kLatticeChunk;
+        float* eng = (float*)(batch + batch_n * tl::kLatticeChunk);
+        for (uint64_t s0 = 0; s0 < n_scen && e == hipSuccess; s0 += batch_n) {
+            const int64_t cnt = (int64_t)std::min<uint64_t>(batch_n, n_scen - s0);
+            e = tl::launch_lattice_inputs(L, (int64_t)s0, cnt, kv, batch, eng, st);
+            if (e == hipSuccess) {
+                tl::GridParams g{};
+                g.S = cnt;
+                g.F = n_freqs;
+                g.H = tl::kLatticeChunk;
+                g.freqs = freqs;
+                g.kv = kv;
+                g.batch = batch;
+                g.engine = nf == 4 ? eng : nullptr;
+                g.out = grid_out;
+                e = tl::launch_forest_grid(f->dev, g, st);
+            }
+            if (e == hipSuccess)
+                e = tl::launch_lattice_transpose(grid_out, (float*)L.table, (int64_t)s0, cnt, n_freqs, st);
+        }
+        const hipError_t e2 = hipFreeAsync(work, st);
+        if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) {
+        (void)hipStreamSynchronize(st);
+        (void)hipFree(lat->mem);
+        delete lat;
+        return from_hip(e, "tl_lattice_create: build");
+    }
+    *out = lat;
+    return ok();
+}
+
+void tl_lattice_destroy(tl_lattice* lat) {
+    if (!lat) return;
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(lat->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(lat->mem);
+    (void)hipSetDevice(cur);
+    delete lat;
+}
+
+uint64_t tl_lattice_bytes(const tl_lattice* lat) { return lat ? lat->bytes : 0; }
+
+tl_status tl_lattice_predict_grid(const tl_lattice* lat, int64_t n_scenarios, int32_t horizon, const int32_t* kv,
+                                  const int32_t* batch, const float* engine_size, float* out, void* stream) {
+    if (!lat) return fail(TL_EINVAL, "tl_lattice_predict_grid: lattice is NULL");
+    if (n_scenarios < 0 || n_scenarios > 0x7fffffffll)
+        return fail(TL_EINVAL, "tl_lattice_predict_grid: n_scenarios %lld outside [0, 2^31-1]", (long long)n_scenarios);
+    if (horizon < 1 || horizon > TL_MAX_HORIZON)
+        return fail(TL_EINVAL, "tl_lattice_predict_grid: horizon %d outside [1, %d]", horizon, TL_MAX_HORIZON);
+    if (n_scenarios == 0) return ok();
+    if (!kv || !batch || !out) return fail(TL_EINVAL, "tl_lattice_predict_grid: NULL required pointer");
+    if (lat->dev.nf == 4 && !engine_size)
+        return fail(TL_EINVAL, "tl_lattice_predict_grid: a 4-feature forest needs engine_size");
+    tl::GatherParams p{};
+    p.S = n_scenarios;
+    p.H = horizon;
+    p.kv = kv;
+    p.batch = batch;
+    p.engine = lat->dev.nf == 4 ? engine_size : nullptr;
+    p.out = out;
+    return from_hip(tl::launch_lattice_gather(lat->forest->dev, lat->dev, p, (hipStream_t)stream),
+                    "tl_lattice_predict_grid: launch");
 }
 
 tl_status tl_adjust_lengths(int64_t n_scenarios, int64_t n_requests, const int64_t* req_offset,

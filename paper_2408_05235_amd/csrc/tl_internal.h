@@ -178,6 +178,34 @@ struct GridParams {
     const uint32_t* order;
 };
 
+// The model compiled to its input lattice (engine sizes x batch 0..batch_max
+// x frequencies x KV 0..kv_max, KV in chunks of kLatticeChunk).
+constexpr int32_t kLatticeChunk = 4096;
+constexpr int32_t kMaxLatticeEngines = 16;
+struct LatticeDev {
+    int32_t nf;                     // forest features (3 or 4)
+    int32_t F, nE, nB, nC;          // frequencies, engine sizes, batch_max + 1, KV chunks
+    int32_t kv_max, batch_max;
+    float engines[kMaxLatticeEngines];
+    const float* freqs;             // [F]
+    const float* table;             // [nE][nB][nC * kLatticeChunk][F]
+};
+
+struct GatherParams {
+    int64_t S;
+    int32_t H;
+    const int32_t* kv;              // [S][H]
+    const int32_t* batch;           // [S][H]
+    const float* engine;            // [S] (4 features)
+    float* out;                     // [S][F][H]
+};
+
+hipError_t launch_lattice_inputs(const LatticeDev& L, int64_t s0, int64_t count, int32_t* kv, int32_t* batch,
+                                 float* engine, hipStream_t stream);
+hipError_t launch_lattice_transpose(const float* src, float* table, int64_t s0, int64_t count, int32_t F,
+                                    hipStream_t stream);
+hipError_t launch_lattice_gather(const ForestDev& f, const LatticeDev& L, const GatherParams& p, hipStream_t stream);
+
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
 hipError_t launch_adjust(const AdjustParams& p, hipStream_t stream);
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,

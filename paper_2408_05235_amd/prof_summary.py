@@ -1,14 +1,15 @@
 """Summarize rocprofv3 CSV output into the short text files kept in profiles/.
 
     python -m paper_2408_05235_amd.prof_summary stats  <kernel_stats.csv> <out.md> <command>
+    python -m paper_2408_05235_amd.prof_summary trace  <kernel_trace.csv> <out.md> <command>
     python -m paper_2408_05235_amd.prof_summary traffic <fetch_counter_collection.csv> \
-        <write_counter_collection.csv> <kernel substring> <copy bytes> <out.json> <command>
+        <write_counter_collection.csv> <kernel substring> <copy bytes> <out.json> <command> [source file]
 
     python -m paper_2408_05235_amd.prof_summary counters <out.md> <kernel substring> <command> \
         <counter_collection.csv> [<counter_collection.csv> ...]
 
-`traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of one kernel into
-bytes per launch, each scaled by what the same counter reads for the last
+`traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the first
+dispatch of one kernel into bytes per launch, each scaled by what the same counter reads for the last
 copy dispatch of the run, a copy of known size (the counters' byte formulas
 need not match the request sizes a kernel uses).
 
@@ -51,6 +52,28 @@ def kernel_stats(csv_path, out_md, command, title=""):
     return rows
 
 
+def trace_stats(trace_csv, out_md, command, title=""):
+    """Kernel statistics from a kernel trace, one line per (kernel, launch
+    grid): launches of one kernel at different sizes (the controller step and
+    a lattice build, say) are kept apart."""
+    groups = {}
+    for r in csv.DictReader(open(trace_csv)):
+        grid = int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+        wg = int(r["Workgroup_Size_X"]) * int(r["Workgroup_Size_Y"]) * int(r["Workgroup_Size_Z"])
+        ns = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        groups.setdefault((r["Kernel_Name"], grid // max(wg, 1), wg), []).append(ns)
+    total = sum(sum(v) for v in groups.values())
+    rows = sorted(groups.items(), key=lambda kv: -sum(kv[1]))
+    lines = [f"# {title or 'rocprofv3 kernel statistics'}", "", "Command:", "", "```", command, "```", "",
+             "| kernel | workgroups x threads | calls | average ms | min ms | max ms | share |",
+             "|---|---|---|---|---|---|---|"]
+    for (name, n_wg, wg), v in rows:
+        lines.append(f"| {_short(name)} | {n_wg} x {wg} | {len(v)} | {sum(v) / len(v) / 1e6:.3f} | "
+                     f"{min(v) / 1e6:.3f} | {max(v) / 1e6:.3f} | {100.0 * sum(v) / total:.2f}% |")
+    open(out_md, "w").write("\n".join(lines) + "\n")
+    return rows
+
+
 def _per_dispatch(csv_path, counter):
     out = []
     for r in csv.DictReader(open(csv_path)):
@@ -62,7 +85,7 @@ def _per_dispatch(csv_path, counter):
     return [(d, k, v) for d, (k, v) in sorted(agg.items())]
 
 
-def traffic(fetch_csv, write_csv, kernel, copy_bytes, out_json, command):
+def traffic(fetch_csv, write_csv, kernel, copy_bytes, out_json, command, source="forest.hip"):
     res = {}
     for name, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
         disp = _per_dispatch(path, counter)
@@ -73,13 +96,15 @@ def traffic(fetch_csv, write_csv, kernel, copy_bytes, out_json, command):
         vals = [v for d, k, v in disp if kernel in k]
         if not vals:
             raise SystemExit(f"no dispatch of {kernel} in {path}")
-        res[name] = dict(kib_per_launch=sum(vals) / len(vals), copy_kib=copies[-1], scale=scale,
-                         bytes_per_launch=sum(vals) / len(vals) * 1024.0 * scale)
-    src = open(os.path.join(PKG, "csrc", "forest.hip"), "rb").read()
+        # the first dispatch: the timed step's (later ones may be other uses
+        # of the same kernel, such as building a lattice table)
+        res[name] = dict(kib_per_launch=vals[0], copy_kib=copies[-1], scale=scale,
+                         bytes_per_launch=vals[0] * 1024.0 * scale)
+    src = open(os.path.join(PKG, "csrc", source), "rb").read()
     rec = dict(kernel=kernel, command=command, copy_bytes=copy_bytes,
                fetch=res["fetch"], write=res["write"],
-               bytes_per_launch=res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"],
-               forest_hip_sha256=hashlib.sha256(src).hexdigest())
+               bytes_per_launch=res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"])
+    rec[source.replace(".", "_") + "_sha256"] = hashlib.sha256(src).hexdigest()
     json.dump(rec, open(out_json, "w"), indent=1)
     return rec
 
@@ -123,11 +148,13 @@ def counters(out_md, kernel, command, csv_paths):
 
 
 if __name__ == "__main__":
-    if sys.argv[1] == "stats":
+    if sys.argv[1] == "trace":
+        trace_stats(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5] if len(sys.argv) > 5 else "")
+    elif sys.argv[1] == "stats":
         kernel_stats(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5] if len(sys.argv) > 5 else "")
     elif sys.argv[1] == "traffic":
         print(json.dumps(traffic(sys.argv[2], sys.argv[3], sys.argv[4], int(sys.argv[5]), sys.argv[6],
-                                 sys.argv[7]), indent=1))
+                                 sys.argv[7], *(sys.argv[8:9])), indent=1))
     elif sys.argv[1] == "counters":
         print(counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5:]))
     else:

@@ -144,6 +144,18 @@ def test_binary_search_rejects_bad_arguments():
         assert needle in L.tl_last_error().decode()
 
 
+def test_lattice_rejects_bad_arguments():
+    L = _lib.lib()
+    d = ctypes.c_void_p(16)
+    h = ctypes.c_void_p(99)
+    assert L.tl_lattice_create(None, 4, d, 0, None, 10, 10, None, ctypes.byref(h)) == _lib.TL_EINVAL
+    assert h.value is None
+    assert L.tl_lattice_create(d, 4, d, 0, None, 10, 10, None, None) == _lib.TL_EINVAL
+    assert L.tl_lattice_predict_grid(None, 1, 8, d, d, None, d, None) == _lib.TL_EINVAL
+    assert L.tl_lattice_bytes(None) == 0
+    L.tl_lattice_destroy(None)
+
+
 def test_forest_create_rejects_bad_trees():
     L = _lib.lib()
     h = ctypes.c_void_p(123)
