@@ -38,9 +38,14 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(inp, F, rows):
+def algorithmic_bytes(inp, F, rows, sel=None):
     """Bytes each stage must move at least (inputs read once, outputs written
-    once) for one step of the fused pipeline (rows are never materialized)."""
+    once) for one step of the fused pipeline (rows are never materialized).
+    Selection stops at the first round of four frequencies with a feasible
+    one, so with the step's results `sel` = (freq_idx, status, n_iters) its
+    bytes are the IPS of the frequencies up to that round (all of them when
+    none is feasible, none for lost / invalid scenarios) over the projected
+    iterations, plus the deadline map."""
     S, H = inp["n_scenarios"], inp["horizon"]
     R = int(inp["req_offset"][-1])
     f = inp["forest"]
@@ -49,6 +54,10 @@ def algorithmic_bytes(inp, F, rows):
     k1 = R * 25 + S * 8 + S * 8 + S * H * 16 + S * 8        # requests; offsets, caps; curves; scalars
     k2 = S * H * 8 + F * 4 + S * 4 + forest_bytes + rows * 4
     k3 = rows * 4 + S * H * 8 + S * 28
+    if sel is not None:
+        idx, st, n = (np.asarray(a, np.int64) for a in sel)
+        evaluated = np.where(st == 0, np.minimum(F, 4 * (idx // 4 + 1)), np.where(st == 1, F, 0))
+        k3 = int((evaluated * n).sum()) * 4 + int(n.sum()) * 8 + S * 28
     return dict(project=k1, predict=k2, select=k3)
 
 
@@ -427,7 +436,8 @@ def main():
     step_ev = np.array([e[0].elapsed_time(e[3]) for e in ev])
     stage_ms = st.mean(axis=0)
     step_ms = wall * 1e3 / args.steps
-    byt = algorithmic_bytes(inp, F, rows)
+    byt = algorithmic_bytes(inp, F, rows, (ctl.sel["freq_idx"].cpu().numpy(), ctl.sel["status"].cpu().numpy(),
+                                           np.clip(ctl.buf["n_iters"].cpu().numpy(), 0, H)))
     tot_bytes = sum(byt.values())
 
     f = inp["forest"]

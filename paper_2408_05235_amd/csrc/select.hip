@@ -2,12 +2,13 @@
 // Sec. 4.3.2 (checks 2 and 3, Eq. 3-4).
 //
 // One 256-thread workgroup per scenario; its four wavefronts take the
-// candidate frequencies in turn.  For one frequency a wave walks the projected
-// iterations 64 at a time: per-iteration time in integer ns, an inclusive
-// wave scan plus the running carry gives Eq. 3's cumulative time T_R[j+1],
-// which is compared with the deadline of requests ending at j.  The walk stops
-// at the first violated deadline.  Feasible frequencies are collected as a
-// bitmask in LDS and the lowest one is taken.
+// candidate frequencies in rounds of four, lowest first, and the first round
+// with a feasible frequency ends the search.  For one frequency a wave walks
+// the projected iterations 256 at a time, four consecutive ones per lane:
+// per-iteration time in integer ns, the lane's running sum plus an exclusive
+// wave scan of lane totals and the carry gives Eq. 3's cumulative time
+// T_R[j+1], which is compared with the deadline of requests ending at j.  The
+// walk stops at the first violated deadline.
 //
 // The admission decision of Sec. 4.3.2 and the steps of the paper's binary
 // search over frequencies use the same arithmetic at one frequency per
@@ -30,9 +31,47 @@ __device__ __forceinline__ uint64_t latency_ns(float ips) {
 }
 
 constexpr int kWavesPerBlock = 4;
+constexpr int kPerLane = 4;                   // consecutive iterations per lane
+constexpr int kStep = kWave * kPerLane;       // iterations per wavefront step
 
+// Eq. 3-4 for one frequency, by one wavefront: per-iteration times of `ips`
+// over the n projected iterations, T_R[j+1] < dl[j] for every deadline and
+// T_R[n] <= budget.  A lane takes four consecutive iterations: their running
+// sum, then one wave scan of the lane totals per 256 iterations.  Stops at
+// the first missed deadline.  Every lane returns the same value.
+__device__ __forceinline__ bool feasible_wave(const float* ips, const uint64_t* dl, int32_t n, uint64_t budget) {
+    const int lane = lane_id();
+    uint64_t carry = 0;
+    for (int32_t j0 = 0; j0 < n; j0 += kStep) {
+        const int32_t jb = j0 + kPerLane * lane;
+        uint64_t p[kPerLane];
+        uint64_t run = 0;
+#pragma unroll
+        for (int k = 0; k < kPerLane; ++k) {
+            run += (jb + k < n) ? latency_ns(ips[jb + k]) : 0ull;
+            p[k] = run;
+        }
+        const uint64_t before = wave_incl_scan_u64(run) - run + carry;   // T_R[jb]
+        bool bad = false;
+#pragma unroll
+        for (int k = 0; k < kPerLane; ++k) {
+            if (jb + k < n) {
+                const uint64_t d = dl[jb + k];
+                bad |= d != kNoDeadline && !(before + p[k] < d);
+            }
+        }
+        carry = __shfl(before + run, kWave - 1);
+        if (__ballot(bad)) return false;
+    }
+    return carry <= budget;
+}
+
+// The lowest feasible frequency of one scenario.  The four wavefronts of the
+// workgroup take frequencies in rounds of four, lowest first; the first
+// round with a feasible frequency ends the search (no higher frequency can
+// be the minimum).
 __global__ __launch_bounds__(256) void select_kernel(SelectParams P) {
-    __shared__ uint32_t feasible[TL_MAX_FREQS / 32];
+    __shared__ uint32_t round_ok;
     const int64_t s = blockIdx.x;
     const int wave = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -53,34 +92,26 @@ __global__ __launch_bounds__(256) void select_kernel(SelectParams P) {
         }
         return;
     }
-    const int32_t n_words = (F + 31) / 32;
-    for (int w = threadIdx.x; w < n_words; w += blockDim.x) feasible[w] = 0;
+    if (threadIdx.x == 0) round_ok = 0;
     __syncthreads();
-
     const uint64_t slo = P.tbt_slo_ns[s];
     const uint64_t budget = (slo > ~0ull / (uint64_t)n) ? ~0ull : slo * (uint64_t)n;
     const uint64_t* dl = P.deadline_at + s * H;
-    for (int32_t f = wave; f < F; f += kWavesPerBlock) {
-        const float* ips = P.ips + ((int64_t)s * F + f) * H;
-        uint64_t carry = 0;
-        bool ok = true;
-        for (int32_t j0 = 0; j0 < n; j0 += kWave) {
-            const int32_t j = j0 + lane;
-            const bool in = j < n;
-            const uint64_t lat = in ? latency_ns(ips[j]) : 0ull;
-            const uint64_t tr = wave_incl_scan_u64(lat) + carry;
-            const uint64_t d = in ? dl[j] : kNoDeadline;
-            const bool bad = in && d != kNoDeadline && !(tr < d);
-            carry = __shfl(tr, kWave - 1);
-            if (__ballot(bad)) { ok = false; break; }
+    int32_t best = -1;
+    for (int32_t f0 = 0; f0 < F; f0 += kWavesPerBlock) {
+        const int32_t f = f0 + wave;
+        const bool ok = f < F && feasible_wave(P.ips + ((int64_t)s * F + f) * H, dl, n, budget);
+        if (ok && lane == 0) atomicOr(&round_ok, 1u << wave);
+        __syncthreads();
+        const uint32_t m = round_ok;
+        // every thread has read this round's mask before the next round writes
+        __syncthreads();
+        if (m) {
+            best = f0 + __ffs(m) - 1;
+            break;
         }
-        if (ok && carry <= budget && lane == 0) atomicOr(&feasible[f >> 5], 1u << (f & 31));
     }
-    __syncthreads();
     if (threadIdx.x == 0) {
-        int32_t best = -1;
-        for (int32_t w = 0; w < n_words; ++w)
-            if (feasible[w]) { best = w * 32 + __ffs(feasible[w]) - 1; break; }
         P.freq_idx[s] = best >= 0 ? best : F - 1;
         P.status[s] = best >= 0 ? TL_STATUS_OK : TL_STATUS_INFEASIBLE;
     }
