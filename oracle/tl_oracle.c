@@ -22,8 +22,9 @@
  * order, returned as fp32) and the per-iteration time 1e9 / IPS (one IEEE fp64
  * division, rounded up to whole nanoseconds).
  *
- * Every reading of a point the paper leaves open is listed in the design doc under
- * "Readings"; the code below follows those readings.
+ * Where the paper leaves a point open, the comment at each function states
+ * the reading it follows (relative iterations, the token produced in an
+ * iteration not yet cached, strict E2E deadlines, exhaustive minimum, ...).
  */
 #include <math.h>
 #include <stdint.h>

@@ -13,7 +13,7 @@ tokens, generations of tens to hundreds of tokens with a long tail (Sec. 3.4,
 trace analysis), 16-token KV blocks, a few hundred to a few thousand future
 iterations and per-token latencies of 10-50 ms (Sec. 5.2 reports 15-30 ms
 TBT).  Fields marked ``proposed`` are not fixed by the workload description
-and are chosen here; the choices are recorded in the design doc.
+and are chosen here.
 """
 
 CONFIGS = [
