@@ -11,7 +11,10 @@
 // at e.  So KV = prefix-sum over j of
 //   (jumps at 0 and e)  +  C[j],  C[j] = C[j - N] + comb_diff[j],
 // where comb_diff gets +1 at j0 and -1 at the first comb point >= e.  The
-// batch curve is the prefix sum of +1 at 0 / -1 at e.
+// batch curve is the prefix sum of +1 at 0 / -1 at e.  One LDS array holds
+// the comb differences, then (scanned in place) C, then C plus the jumps,
+// then KV: two H-long int32 arrays per scenario in all, so more scenarios'
+// wavefronts share a compute unit.
 //
 // For admission control a new query can be appended to every scenario as a
 // request that starts now (Sec. 4.3.2, the "virtual" scoreboard); it adds
@@ -50,28 +53,33 @@ __device__ __forceinline__ int32_t sum_range(const int32_t* DA, int32_t j, int32
 }
 
 // Events of one request that holds c cached tokens now and stays in the batch
-// on [0, e): batch +1 at 0 / -1 at e, KV +ceil(c/N) at 0 and -KV_i[e-1] at
-// e, and the block comb from its first new-block iteration (see above).
-// Counts it in n_in, kv0 (blocks at iteration 0) and n_end.
-__device__ __forceinline__ void inflight_events(int32_t c, int32_t e, int32_t H, int32_t N, const DivU32& divN,
-                                                int32_t* BI, int32_t* KV, int32_t* CD, int32_t& n_in,
-                                                int32_t& kv0, int32_t& n_end) {
-    ++n_in;
-    kv0 += (int32_t)ceil_div_u32((uint32_t)c, divN);
+// on [0, e), in two parts.  The block comb: +1 at its first new-block
+// iteration j0 and -1 at the first comb point at or past e (a stride-N prefix
+// scan turns these into the per-iteration increments).  The jumps: batch +1
+// at 0 / -1 at e, KV +ceil(c/N) at 0 (counted in kv0) and -KV_i[e-1] at e;
+// the request is counted in n_in and n_end.
+__device__ __forceinline__ void inflight_comb(int32_t c, int32_t e, int32_t H, int32_t N, const DivU32& divN,
+                                              int32_t* X) {
     const int32_t lim = min(e, H);
-    n_end = max(n_end, lim);
-    if (e < H) {
-        atomicAdd(&BI[e], -1);
-        atomicAdd(&KV[e], -(int32_t)ceil_div_u32((uint32_t)(c + e - 1), divN));
-    }
     const int32_t rc = (int32_t)((uint32_t)c - div_u32((uint32_t)c, divN) * (uint32_t)N);
     const int32_t j0 = (rc == 0) ? 1 : (N + 1 - rc);
     if (j0 < lim) {
-        atomicAdd(&CD[j0], 1);
+        atomicAdd(&X[j0], 1);
         if (e < H) {
             const int32_t jend = j0 + N * (int32_t)ceil_div_u32((uint32_t)(e - j0), divN);
-            if (jend < H) atomicAdd(&CD[jend], -1);
+            if (jend < H) atomicAdd(&X[jend], -1);
         }
+    }
+}
+
+__device__ __forceinline__ void inflight_jumps(int32_t c, int32_t e, int32_t H, const DivU32& divN, int32_t* BI,
+                                               int32_t* X, int32_t& n_in, int32_t& kv0, int32_t& n_end) {
+    ++n_in;
+    kv0 += (int32_t)ceil_div_u32((uint32_t)c, divN);
+    n_end = max(n_end, min(e, H));
+    if (e < H) {
+        atomicAdd(&BI[e], -1);
+        atomicAdd(&X[e], -(int32_t)ceil_div_u32((uint32_t)(c + e - 1), divN));
     }
 }
 
@@ -80,9 +88,8 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     const int32_t H = P.H;
     const int32_t N = P.N;
     const DivU32 divN{(uint32_t)N, P.div_m, P.div_l};
-    int32_t* KV = lds;            // KV curve (diff, then values)
-    int32_t* BI = lds + H;        // in-flight batch curve (diff, then values)
-    int32_t* CD = lds + 2 * H;    // comb diff / prefix; later the admitted-batch diff
+    int32_t* KV = lds;            // comb diff, comb prefix, + jumps, then KV values
+    int32_t* BI = lds + H;        // batch difference array
     const int lane = lane_id();
     const int64_t s = blockIdx.x;
     int32_t* outB = P.batch + s * H;
@@ -92,7 +99,6 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     for (int32_t t = lane; t < H; t += kWave) {
         KV[t] = 0;
         BI[t] = 0;
-        CD[t] = 0;
         outDL[t] = kNoDeadline;
     }
     __threadfence();
@@ -163,21 +169,48 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
         return;
     }
 
-    // pass B: in-flight requests -> events
+    // pass B1: the in-flight requests' block combs, then their stride-N
+    // prefix in place (every later write adds to it)
+    for (int64_t base = lo; base < hi; base += kWave) {
+        const int64_t i = base + lane;
+        if (i >= hi) continue;
+        const int32_t p = P.prompt[i], g = P.gen[i], r = P.rem[i], a = P.arr[i];
+        if (!entry_ok(p, g, r, a) || a != -1) continue;
+        inflight_comb(p + g, r, H, N, divN, KV);
+    }
+    if (cand && lane == 0) inflight_comb(cand_p, cand_l, H, N, divN, KV);
+    __syncthreads();
+    {
+        const int32_t lane_mod = lane % N;
+        for (int32_t t0 = 0; t0 < H; t0 += kWave) {
+            const int32_t t = t0 + lane;
+            const bool in = t < H;
+            int32_t c = in ? KV[t] : 0;
+            for (int32_t d = N; d < kWave; d <<= 1) {
+                const int32_t u = __shfl_up(c, d);
+                if (lane >= d) c += u;
+            }
+            const int32_t prev = t0 + lane_mod - N;
+            if (prev >= 0 && in) c += KV[prev];
+            if (in) KV[t] = c;
+        }
+    }
+    __syncthreads();
+
+    // pass B2: jumps, batch events, deadline checkpoints
     int32_t n_end = 0, n_in = 0, kv0 = 0;
     for (int64_t base = lo; base < hi; base += kWave) {
         const int64_t i = base + lane;
         if (i >= hi) continue;
         const int32_t p = P.prompt[i], g = P.gen[i], r = P.rem[i], a = P.arr[i];
         if (!entry_ok(p, g, r, a) || a != -1) continue;
-        const int32_t c = p + g;
         const int32_t e = r;
-        inflight_events(c, e, H, N, divN, BI, KV, CD, n_in, kv0, n_end);
+        inflight_jumps(p + g, e, H, divN, BI, KV, n_in, kv0, n_end);
         const bool is_lost = P.lost && P.lost[i];
         const uint64_t d = P.deadline ? P.deadline[i] : kNoDeadline;
         if (e <= H && !is_lost && d != kNoDeadline) atomicMin((unsigned long long*)&outDL[e - 1], (unsigned long long)d);
     }
-    if (cand && lane == 0) inflight_events(cand_p, cand_l, H, N, divN, BI, KV, CD, n_in, kv0, n_end);
+    if (cand && lane == 0) inflight_jumps(cand_p, cand_l, H, divN, BI, KV, n_in, kv0, n_end);
     n_in = wave_sum(n_in);
     kv0 = wave_sum(kv0);
     n_end = wave_max(n_end);
@@ -187,26 +220,17 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     }
     __syncthreads();
 
-    // scans: comb (stride N) then the KV prefix sum; last over-capacity
-    // iteration.  The batch curve stays a difference array: admissions add
-    // their +1 / -1 to it and the output takes its prefix sum.
+    // the KV prefix sum; last over-capacity iteration.  The batch curve stays
+    // a difference array: admissions add their +1 / -1 to it and the output
+    // takes its prefix sum.
     const int32_t cap = P.kv_cap[s];
     int32_t last_over = -1;
     {
-        const int32_t lane_mod = lane % N;
         int32_t carry_kv = 0;
         for (int32_t t0 = 0; t0 < H; t0 += kWave) {
             const int32_t t = t0 + lane;
             const bool in = t < H;
-            int32_t c = in ? CD[t] : 0;
-            for (int32_t d = N; d < kWave; d <<= 1) {
-                const int32_t u = __shfl_up(c, d);
-                if (lane >= d) c += u;
-            }
-            const int32_t prev = t0 + lane_mod - N;
-            if (prev >= 0 && in) c += CD[prev];
-            if (in) CD[t] = c;
-            const int32_t y = wave_incl_scan((in ? KV[t] : 0) + c) + carry_kv;
+            const int32_t y = wave_incl_scan(in ? KV[t] : 0) + carry_kv;
             carry_kv = __builtin_amdgcn_readlane(y, kWave - 1);
             if (in) {
                 KV[t] = y;
@@ -225,10 +249,7 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     // of one wave are processed in order, so one lane's updates are seen by
     // the later reads of every lane.
     int32_t* BD = BI;   // batch differences: in-flight requests, then admitted ones
-    int32_t* W = CD;    // scratch curve of batched admission, kept zero between batches
     if (has_queue) {
-        __syncthreads();
-        for (int32_t t = lane; t < H; t += kWave) W[t] = 0;
         __syncthreads();
         int32_t j = 0;
         int32_t run = 0;    // batch size at j (prefix of BD; kept only under a batch cap)
@@ -267,7 +288,8 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 // everywhere, so does every request's own check at its target
                 // (each sees the KV of the requests before it, which is no
                 // more than the sum): these are exactly the admissions the
-                // one-at-a-time loop makes.  Otherwise retry with fewer.
+                // one-at-a-time loop makes.  Otherwise the contributions are
+                // taken out again and fewer are tried.
                 const int32_t lo_j = max(j, last_over + 1);
                 const uint32_t below = __builtin_amdgcn_mbcnt_hi(
                     (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
@@ -288,24 +310,29 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                     // LDS adds without a returned value: no wait per chunk
                     for (int32_t t0 = am; t0 < lim; t0 += kWave) {
                         const int32_t t = t0 + lane;
-                        if (t < lim) atomicAdd(&W[t], (int32_t)ceil_div_u32((uint32_t)(cm + t - am), divN));
+                        if (t < lim) atomicAdd(&KV[t], (int32_t)ceil_div_u32((uint32_t)(cm + t - am), divN));
                     }
                 }
                 const int32_t a_first = __builtin_amdgcn_readlane(a, __ffsll((unsigned long long)take) - 1);
                 bool bad = false;
                 for (int32_t t0 = a_first; t0 < r_end; t0 += kWave) {
                     const int32_t t = t0 + lane;
-                    if (t < r_end && KV[t] + W[t] > cap) bad = true;
+                    if (t < r_end && KV[t] > cap) bad = true;
                 }
                 const bool fits = __ballot(bad) == 0;
-                for (int32_t t0 = a_first; t0 < r_end; t0 += kWave) {
-                    const int32_t t = t0 + lane;
-                    if (t < r_end) {
-                        if (fits) KV[t] += W[t];
-                        W[t] = 0;
-                    }
-                }
                 if (!fits) {
+                    // take the batch's contributions out again
+                    for (uint64_t mm = take; mm; mm &= mm - 1) {
+                        const int m = __ffsll((unsigned long long)mm) - 1;
+                        const int32_t am = __builtin_amdgcn_readlane(a, m);
+                        const int32_t cm = __builtin_amdgcn_readlane(q_c, m);
+                        const int32_t lm = __builtin_amdgcn_readlane(q_len, m);
+                        const int32_t lim = (int32_t)min((int64_t)am + lm, (int64_t)H);
+                        for (int32_t t0 = am; t0 < lim; t0 += kWave) {
+                            const int32_t t = t0 + lane;
+                            if (t < lim) atomicAdd(&KV[t], -(int32_t)ceil_div_u32((uint32_t)(cm + t - am), divN));
+                        }
+                    }
                     // shrink the batch; once down to single requests, admit
                     // a growing number of them one at a time before batching
                     // again (the capacity binds)
@@ -481,7 +508,7 @@ hipError_t launch_adjust(const AdjustParams& p, hipStream_t stream) {
 }
 
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream) {
-    const size_t lds = (size_t)3 * p.H * sizeof(int32_t);
+    const size_t lds = (size_t)2 * p.H * sizeof(int32_t);
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)project_kernel,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
