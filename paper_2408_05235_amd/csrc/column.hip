@@ -239,6 +239,7 @@ template <int NF, int RPL>
 hipError_t launch_column_lds(const ForestDev& f, const ColumnParams& c, int32_t tb, size_t lds, hipStream_t stream) {
     const int64_t n_cols = (c.H + kWave * RPL - 1) / (kWave * RPL);
     const int64_t items = c.S * n_cols;
+    if (!grid_fits((items + kColWaves - 1) / kColWaves)) return hipErrorInvalidConfiguration;
     const auto kern = forest_column_lds_kernel<NF, RPL>;
     const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -259,6 +260,7 @@ hipError_t launch_column(const ForestDev& f, const ColumnParams& c, hipStream_t 
         return launch_column_lds<NF, 1>(f, c, tb, lds, stream);
     }
     const int64_t items = c.S * ((c.H + kWave - 1) / kWave);
+    if (!grid_fits((items + 3) / 4)) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(forest_column_global_kernel<NF>, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, stream,
                        f.nodes, f.leaves, f.n_trees, f.depth, f.base_score, c);
     return hipGetLastError();

@@ -548,6 +548,7 @@ hipError_t launch_nf(const ForestDev& f, const float* rows, int64_t n_rows, floa
     constexpr int TPB = 256;
     const int64_t threads = (n_rows + RPT - 1) / RPT;
     const int64_t blocks = (threads + TPB - 1) / TPB;
+    if (!grid_fits(blocks)) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((forest_rows_kernel<NF, RPT>), dim3((unsigned)blocks), dim3(TPB), 0, stream,
                        f.nodes, f.leaves, f.n_trees, f.depth, f.base_score, rows, n_rows, out);
     return hipGetLastError();
@@ -580,6 +581,7 @@ hipError_t launch_grid_lds(const ForestDev& f, const GridParams& g, int32_t tb, 
     const int64_t n_fg = (g.F + kWave - 1) / kWave;
     const int64_t items = g.S * n_fg * n_chunks;
     const int64_t blocks = (items + kLdsWaves - 1) / kLdsWaves;
+    if (!grid_fits(blocks)) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kLdsThreads), lds, stream, f.records, f.n_trees,
                        f.depth, tb, f.base_score, g);
     return hipGetLastError();
@@ -591,6 +593,7 @@ hipError_t launch_grid_global(const ForestDev& f, const GridParams& g, hipStream
     const int64_t n_fg = (g.F + kWave - 1) / kWave;
     const int64_t items = g.S * n_fg * n_chunks;
     const int64_t blocks = (items + kGlobalWaves - 1) / kGlobalWaves;
+    if (!grid_fits(blocks)) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((forest_grid_global_kernel<NF, kGlobalJ>), dim3((unsigned)blocks), dim3(kGlobalWaves * kWave),
                        0, stream, f.nodes, f.leaves, f.kvb_box, f.n_trees, f.depth, f.base_score, g);
     return hipGetLastError();

@@ -147,6 +147,7 @@ __global__ __launch_bounds__(kGatherThreads) void lattice_gather_kernel(ForestDe
 hipError_t launch_lattice_inputs(const LatticeDev& L, int64_t s0, int64_t count, int32_t* kv, int32_t* batch,
                                  float* engine, hipStream_t stream) {
     const int64_t n = count * kLatticeChunk;
+    if (!grid_fits((n + 255) / 256)) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(lattice_inputs_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, L, s0, count,
                        kv, batch, engine);
     return hipGetLastError();
@@ -155,6 +156,7 @@ hipError_t launch_lattice_inputs(const LatticeDev& L, int64_t s0, int64_t count,
 hipError_t launch_lattice_transpose(const float* src, float* table, int64_t s0, int64_t count, int32_t F,
                                     hipStream_t stream) {
     const int64_t blocks = count * ((F + kTile - 1) / kTile) * (kLatticeChunk / kTile);
+    if (!grid_fits(blocks)) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(lattice_transpose_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, src, table, s0, F);
     return hipGetLastError();
 }
@@ -163,6 +165,7 @@ hipError_t launch_lattice_gather(const ForestDev& f, const LatticeDev& L, const 
     if (p.S == 0) return hipSuccess;
     const int32_t n_jb = (p.H + kGatherThreads - 1) / kGatherThreads;
     const int64_t blocks = p.S * n_jb;
+    if (!grid_fits(blocks)) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(lattice_gather_kernel, dim3((unsigned)blocks), dim3(kGatherThreads), 0, stream, f, L, p, n_jb);
     return hipGetLastError();
 }

@@ -206,6 +206,9 @@ hipError_t launch_lattice_transpose(const float* src, float* table, int64_t s0, 
                                     hipStream_t stream);
 hipError_t launch_lattice_gather(const ForestDev& f, const LatticeDev& L, const GatherParams& p, hipStream_t stream);
 
+// A launch of `blocks` workgroups fits the grid (at most 2^31 - 1 in x).
+inline bool grid_fits(int64_t blocks) { return blocks >= 0 && blocks <= 0x7fffffffll; }
+
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
 hipError_t launch_adjust(const AdjustParams& p, hipStream_t stream);
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,
