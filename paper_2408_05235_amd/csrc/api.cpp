@@ -236,12 +236,16 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
 
 void tl_forest_destroy(tl_forest* f) {
     if (!f) return;
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(f->device);
     (void)hipDeviceSynchronize();
     (void)hipFree(f->nodes_mem);
     (void)hipFree(f->leaves_mem);
     if (f->box_mem) (void)hipFree(f->box_mem);
     if (f->records_mem) (void)hipFree(f->records_mem);
     if (f->cuts_mem) (void)hipFree(f->cuts_mem);
+    (void)hipSetDevice(cur);
     delete f;
 }
 
