@@ -13,8 +13,8 @@ dispatch of one kernel into bytes per launch, each scaled by what the same count
 copy dispatch of the run, a copy of known size (the counters' byte formulas
 need not match the request sizes a kernel uses).
 
-`counters` averages every counter of the given runs over the dispatches of one
-kernel and derives the rates kept beside the kernel statistics: LDS bank
+`counters` takes every counter of the given runs at the first dispatch of one
+kernel (the timed step's) and derives the rates kept beside the kernel statistics: LDS bank
 conflict cycles per cycle of indexed LDS activity, and per LDS instruction.
 L2 hit rate from TCC_HIT and TCC_MISS (rocprofv3 has no L2CacheHit for gfx950).
 Derived counters that rocprofv3 computes itself (VALUBusy, VALUUtilization,
@@ -121,6 +121,12 @@ def counters(out_md, kernel, command, csv_paths):
             vals[key] = vals.get(key, 0.0) + float(r["Counter_Value"])
     if not vals:
         raise SystemExit(f"no dispatch of {kernel} in {csv_paths}")
+    # the first dispatch of each run: the timed step's (later ones may be
+    # other uses of the kernel, such as building a lattice table)
+    first = {}
+    for (c, path, d) in sorted(vals):
+        first.setdefault((c, path), d)
+    vals = {k: v for k, v in vals.items() if first[(k[0], k[1])] == k[2]}
     per = {}
     for (c, _, _), v in vals.items():
         per.setdefault(c, []).append(v)
