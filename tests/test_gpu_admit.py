@@ -111,7 +111,7 @@ def random_candidates(rng, inp, bad=0.05, beyond=0.1, no_deadline=0.15):
 @pytest.mark.parametrize("H,N,T,d,nf,seed", [
     (8, 4, 3, 2, 3, 0), (64, 16, 40, 6, 3, 1), (100, 3, 25, 8, 3, 2), (513, 16, 30, 10, 4, 3),
     (1, 16, 5, 3, 3, 4), (77, 7, 6, 12, 4, 5), (300, 16, 0, 4, 3, 6), (130, 8, 9, 0, 3, 7),
-    (2048, 16, 12, 11, 3, 8)])
+    (2048, 16, 12, 11, 3, 8), (8192, 16, 6, 8, 4, 9)])
 def test_admit_random_boards(gpu, H, N, T, d, nf, seed):
     rng = np.random.default_rng(500 + seed)
     S = 37

@@ -447,3 +447,33 @@ def test_determinism(gpu):
     part = ctl.forest.tl_forest_predict(rows[1001:].contiguous())
     torch.cuda.synchronize()
     assert np.array_equal(_np(part), _np(ctl.ips).reshape(-1)[1001:])
+
+
+def test_maximum_frequencies_and_horizon(gpu):
+    """F = TL_MAX_FREQS and H = TL_MAX_HORIZON through the grid kernel and
+    the selection (one scenario, 33.5 M rows, a small forest)."""
+    import torch
+    api = _api()
+    rng = np.random.default_rng(4242)
+    F, H = 4096, 8192
+    fd = random_forest(rng, 3, 4, 4, kvmax=6000, bmax=300)
+    fd["base_score"] = np.float32(60.0)
+    kv, bs = random_curves(rng, 1, H, kvmax=6000, bmax=300)
+    eng = np.array([4.0], np.float32)
+    freqs = synth.frequency_grid(F)
+    f = api.Forest.from_dict(fd)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    ips = f.tl_forest_predict_grid(t(freqs), t(kv), t(bs), t(eng))
+    dl = np.full((1, H), NONE, np.uint64)
+    dl[0, [10, 4000, 8191]] = [400_000_000, 80_000_000_000, 150_000_000_000]
+    n = np.array([H], np.int32)
+    tbt = np.array([16_500_000], np.uint64)        # the lowest passing index is 3760
+    idx, st = api.tl_select_freq(ips, t(dl.view(np.int64)), t(n), t(tbt.view(np.int64)), None)
+    torch.cuda.synchronize()
+    got = _np(ips)
+    exp = oracle.forest_predict(fd, oracle.rows(freqs, bs, kv, eng, 4))
+    assert np.array_equal(got, exp)
+    oi, os_ = oracle.select(exp, dl, n, tbt)
+    assert (int(_np(idx)[0]), int(_np(st)[0])) == (int(oi[0]), int(os_[0]))
+    assert int(oi[0]) > 1000          # deep into the rounds of four
+    f.close()
