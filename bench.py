@@ -209,20 +209,23 @@ def adjust_lengths_bench(inp, dev_in, steps, copy_gbs):
 LATTICE_FILE = os.path.join(ROOT, "profiles", "lattice_{}_traffic.json")
 
 
-def lattice_bench(inp, cfg, ctl, steps, warmup, max_gib=24):
+def lattice_bench(inp, cfg, ctl, steps, warmup, admission=None, max_gib=24):
     """The model compiled to its input lattice (a separate mode, not the
     headline): one-time build over (engine sizes x batch 0..max x the F
     frequencies x KV 0..capacity), then the step's prediction as a table
     lookup with identical values.  Reports the build time, the lookup's
     HIP-event time, the step with it (project + lookup + select), and the
     lookup kernel's HBM roofline (algorithmic bytes: 4 written + 4 read per
-    row, 8 per (scenario, iteration))."""
+    row, 8 per (scenario, iteration)).  The binary search and, when
+    `admission` is given (a function of the lattice), admission control are
+    timed again with M read from the table.  Batch bound: the step's largest
+    batch plus one, the batch a what-if query can add."""
     import torch
 
     from paper_2408_05235_amd import api
     S, H, F = inp["n_scenarios"], inp["horizon"], inp["n_freqs"]
     kv_max = int(cfg["kv_capacity"])
-    b_max = int(ctl.buf["batch"].max().item())
+    b_max = int(ctl.buf["batch"].max().item()) + 1
     engines = [1.0, 2.0, 4.0, 8.0] if inp["n_features"] == 4 else None
     n_e = len(engines) if engines else 1
     gib = n_e * (b_max + 1) * F * 4096 * (kv_max // 4096 + 1) * 4 / 2 ** 30
@@ -265,7 +268,22 @@ def lattice_bench(inp, cfg, ctl, steps, warmup, max_gib=24):
         src = open(os.path.join(ROOT, "paper_2408_05235_amd", "csrc", "lattice.hip"), "rb").read()
         if rec.get("lattice_hip_sha256") == hashlib.sha256(src).hexdigest():
             traffic = rec.get("bytes_per_launch")
+    # the binary search with M read from the table
+    for _ in range(max(1, warmup)):
+        ctl.select_binary(lat)
+    torch.cuda.synchronize()
+    ev_b = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        ctl.select_binary(lat)
+        e1.record()
+        ev_b.append((e0, e1))
+    torch.cuda.synchronize()
+    bin_ms = float(np.median([a.elapsed_time(b) for a, b in ev_b]))
     res = {"table_gib": lat.nbytes / 2 ** 30, "build_s": build_s, "bounds": {"kv_max": kv_max, "batch_max": b_max},
+           "binary_search_ms": bin_ms,
+           "admission": admission(lat) if admission else None,
            "lookup_ms": look_ms, "step_ms": step_ms, "rows_per_s": rows / (step_ms / 1e3),
            "same_ips_as_direct": same,
            "roofline": {"kernel": "lattice_gather_kernel", "bound": "hbm", "achieved": achieved,
@@ -302,7 +320,7 @@ def binary_search_bench(ctl, steps, warmup):
             "same_index_as_exhaustive": float((bi == ei).mean())}
 
 
-def admission_bench(inp, cfg, dev_in, forest, steps, warmup):
+def admission_bench(inp, cfg, dev_in, forest, steps, warmup, lattice=None):
     """Admission control (Sec. 4.3.2) of one new query per scenario of the same
     workload: projection with the query, the model at the maximum frequency on
     every projected iteration, checks 1-3 (one tl_admit call), timed like the
@@ -321,7 +339,7 @@ def admission_bench(inp, cfg, dev_in, forest, steps, warmup):
         nonlocal res
         res = api.tl_admit(forest, fmax, d["tbt_slo_ns"], cp, cl, d["req_offset"], d["prompt"], d["generated"],
                            d["remaining"], d["arrival"], d["kv_capacity"], d["horizon"], d["block_tokens"],
-                           d["deadline_ns"], d["lost"], d["batch_cap"], d["engine_size"], cd, res)
+                           d["deadline_ns"], d["lost"], d["batch_cap"], d["engine_size"], cd, res, lattice=lattice)
 
     for _ in range(max(1, warmup)):
         call()
@@ -486,7 +504,8 @@ def main():
     }
     out["results_d2h_ms"] = d2h_results_ms(ctl)
     out["adjust_lengths"] = adjust_lengths_bench(inp, dev_in, args.steps, copy_gbs)
-    out["lattice"] = lattice_bench(inp, cfg, ctl, args.steps, args.warmup)
+    out["lattice"] = lattice_bench(inp, cfg, ctl, args.steps, args.warmup,
+                                   lambda lat: admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup, lat))
     out["binary_search"] = binary_search_bench(ctl, args.steps, args.warmup)
     out["admission"] = admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup)
     if args.copy_calibration_mib:

@@ -307,12 +307,15 @@ tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs,
  * freqs_mhz [F] ascending; engine_size [S] for 4-feature forests.
  * Work arrays of the caller: ips_work [S][H] fp32 (left holding M at the
  * final probe) and search_work [3][S] int32.  Allocates nothing.
+ * lattice (nullable): a table of the same forest built for freqs_mhz
+ * (tl_lattice_create); M at the probes is then read from it (same values).
  * ---------------------------------------------------------------------- */
 tl_status tl_select_freq_binary(const tl_forest* forest, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
                                 const float* freqs_mhz, const int32_t* kv, const int32_t* batch,
                                 const float* engine_size, const uint64_t* deadline_at, const int32_t* n_iters,
                                 const uint64_t* tbt_slo_ns, const uint32_t* proj_flags, float* ips_work,
-                                int32_t* search_work, int32_t* freq_idx, uint32_t* status, void* stream);
+                                int32_t* search_work, int32_t* freq_idx, uint32_t* status,
+                                const tl_lattice* lattice, void* stream);
 
 /* ------------------------------------------------------------------------
  * Admission control (Sec. 4.3.2) for one new query per scenario, as a batch
@@ -356,6 +359,8 @@ typedef struct tl_admit_args {
     const uint64_t* cand_deadline_ns;  /* [S] t_dead - t_cur; NULL or TL_NO_DEADLINE = none */
     float* ips;                        /* out [S][H] */
     uint32_t* decision;                /* out [S], TL_ADMIT_* */
+    const tl_lattice* lattice;         /* nullable: a table of the same forest; used
+                                          when max_freq_mhz is one of its frequencies */
 } tl_admit_args;
 
 tl_status tl_admit(const tl_admit_args* args, void* stream);

@@ -42,7 +42,7 @@ class AdmitArgs(ctypes.Structure):
     _fields_ = [
         ("struct_size", u32), ("reserved", u32), ("proj", ProjectArgs), ("forest", P),
         ("max_freq_mhz", f32), ("engine_size", P), ("tbt_slo_ns", P), ("cand_prompt", P),
-        ("cand_len", P), ("cand_deadline_ns", P), ("ips", P), ("decision", P),
+        ("cand_len", P), ("cand_deadline_ns", P), ("ips", P), ("decision", P), ("lattice", P),
     ]
 
 
@@ -82,7 +82,7 @@ def lib():
     L.tl_forest_predict_grid.restype = ctypes.c_int
     L.tl_select_freq.argtypes = [P, i64, i32, i32, P, P, P, P, P, P, P]
     L.tl_select_freq.restype = ctypes.c_int
-    L.tl_select_freq_binary.argtypes = [P, i64, i32, i32] + [P] * 13
+    L.tl_select_freq_binary.argtypes = [P, i64, i32, i32] + [P] * 14
     L.tl_select_freq_binary.restype = ctypes.c_int
     L.tl_lattice_create.argtypes = [P, i32, P, i32, P, i32, i32, P, ctypes.POINTER(P)]
     L.tl_lattice_create.restype = ctypes.c_int

@@ -117,7 +117,7 @@ def tl_project(req_offset, prompt_len, generated, remaining, arrival_iter, kv_ca
 
 def tl_admit(forest, max_freq_mhz, tbt_slo_ns, cand_prompt, cand_len, req_offset, prompt_len, generated,
              remaining, arrival_iter, kv_capacity, horizon, block_tokens, deadline_ns=None, lost=None,
-             batch_cap=None, engine_size=None, cand_deadline_ns=None, out=None):
+             batch_cap=None, engine_size=None, cand_deadline_ns=None, out=None, lattice=None):
     """Admission control (tl_admit) for one new query per scenario.  Returns
     the projection with the query (batch, kv, deadline_at, n_iters, flags as
     in tl_project), ips [S,H] fp32 at max_freq_mhz and decision [S] int32
@@ -146,6 +146,7 @@ def tl_admit(forest, max_freq_mhz, tbt_slo_ns, cand_prompt, cand_len, req_offset
     b.tbt_slo_ns = _p(tbt_slo_ns)
     b.cand_prompt, b.cand_len, b.cand_deadline_ns = _p(cand_prompt), _p(cand_len), _p(cand_deadline_ns)
     b.ips, b.decision = _p(ips), _p(dec)
+    b.lattice = None if lattice is None else lattice._h
     check(lib().tl_admit(ctypes.byref(b), _stream()))
     res.update(ips=ips, decision=dec)
     return res
@@ -293,10 +294,12 @@ def tl_select_freq(ips, deadline_at, n_iters, tbt_slo_ns, proj_flags=None, out=N
 
 
 def tl_select_freq_binary(forest, freqs_mhz, kv, batch, deadline_at, n_iters, tbt_slo_ns, proj_flags=None,
-                          engine_size=None, out=None):
+                          engine_size=None, out=None, lattice=None):
     """The controller's binary search over frequencies (tl_select_freq_binary),
-    querying the model only at probed frequencies.  kv, batch [S,H] int32 as
-    written by tl_project.  Returns (freq_idx int32 [S], status int32 [S])."""
+    querying the model only at probed frequencies (read from ``lattice``, a
+    Lattice of the same forest built for freqs_mhz, when given).  kv, batch
+    [S,H] int32 as written by tl_project.  Returns (freq_idx int32 [S],
+    status int32 [S])."""
     _need(kv, torch.int32, "kv")
     if kv.dim() != 2:
         raise ValueError("kv must be [S, H]")
@@ -324,7 +327,7 @@ def tl_select_freq_binary(forest, freqs_mhz, kv, batch, deadline_at, n_iters, tb
     check(lib().tl_select_freq_binary(forest._h, S, F, H, _p(freqs_mhz), _p(kv), _p(batch),
                                       _p(engine_size) if forest.n_features == 4 else None, _p(deadline_at),
                                       _p(n_iters), _p(tbt_slo_ns), _p(proj_flags), _p(ips), _p(work), _p(idx),
-                                      _p(st), _stream()))
+                                      _p(st), None if lattice is None else lattice._h, _stream()))
     return idx, st
 
 
@@ -430,9 +433,10 @@ class Controller:
         self.predict()
         return self.select()
 
-    def select_binary(self):
+    def select_binary(self, lattice=None):
         """The paper's binary search over the frequencies on the projection
-        (tl_select_freq_binary): the model only at probed frequencies."""
+        (tl_select_freq_binary): the model only at probed frequencies, read
+        from ``lattice`` when given."""
         d, b = self.d, self.buf
         if "search" not in self.__dict__:
             S, H = d["n_scenarios"], d["horizon"]
@@ -442,4 +446,5 @@ class Controller:
                                freq_idx=torch.empty(S, dtype=torch.int32, device=dev),
                                status=torch.empty(S, dtype=torch.int32, device=dev))
         return tl_select_freq_binary(self.forest, d["freqs_mhz"], b["kv"], b["batch"], b["deadline_at"],
-                                     b["n_iters"], d["tbt_slo_ns"], b["flags"], d["engine_size"], self.search)
+                                     b["n_iters"], d["tbt_slo_ns"], b["flags"], d["engine_size"], self.search,
+                                     lattice)

@@ -30,6 +30,7 @@ struct tl_lattice {
     tl::LatticeDev dev;
     void* mem;        // [F] frequencies (padded to 256 bytes), then the table
     uint64_t bytes;
+    std::vector<float> host_freqs;
 };
 
 namespace {
@@ -355,7 +356,26 @@ tl_status tl_admit(const tl_admit_args* a, void* stream) {
     c.freq = a->max_freq_mhz;
     c.engine = a->engine_size;
     c.out = a->ips;
-    e = tl::launch_forest_column(f->dev, c, st_h);
+    int32_t lat_f = -1;
+    if (a->lattice) {
+        if (a->lattice->forest != f) return fail(TL_EINVAL, "tl_admit: the lattice was built from another forest");
+        const std::vector<float>& hf = a->lattice->host_freqs;
+        for (size_t q = 0; q < hf.size(); ++q)
+            if (hf[q] == a->max_freq_mhz) { lat_f = (int32_t)q; break; }
+    }
+    if (lat_f >= 0) {
+        // the maximum frequency is on the lattice: one table read per row
+        tl::GatherParams gp{};
+        gp.S = S;
+        gp.H = a->proj.horizon;
+        gp.kv = a->proj.kv;
+        gp.batch = a->proj.batch;
+        gp.engine = f->dev.n_features == 4 ? a->engine_size : nullptr;
+        gp.out = a->ips;
+        e = tl::launch_lattice_column(f->dev, a->lattice->dev, gp, nullptr, lat_f, st_h);
+    } else {
+        e = tl::launch_forest_column(f->dev, c, st_h);
+    }
     if (e != hipSuccess) return from_hip(e, "tl_admit: model launch");
     tl::AdmitParams d{};
     d.ips = a->ips;
@@ -491,7 +511,11 @@ tl_status tl_lattice_create(const tl_forest* f, int32_t n_freqs, const float* fr
     void* work = nullptr;
     const uint64_t per_scen = (uint64_t)n_freqs * tl::kLatticeChunk * 4u;
     const uint64_t batch_n = std::max<uint64_t>(1, std::min<uint64_t>(n_scen, (512ull << 20) / per_scen));
+    lat->host_freqs.assign((size_t)n_freqs, 0.0f);
     e = hipMemcpyAsync(freqs, freqs_mhz, (size_t)n_freqs * 4u, hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(lat->host_freqs.data(), freqs_mhz, (size_t)n_freqs * 4u, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e == hipSuccess)
         e = hipMallocAsync(&work, batch_n * (per_scen + tl::kLatticeChunk * 8u + 4u) + 256u, st);
     if (e == hipSuccess) {
@@ -594,8 +618,11 @@ tl_status tl_select_freq_binary(const tl_forest* f, int64_t n_scenarios, int32_t
                                 const float* freqs_mhz, const int32_t* kv, const int32_t* batch,
                                 const float* engine_size, const uint64_t* deadline_at, const int32_t* n_iters,
                                 const uint64_t* tbt_slo_ns, const uint32_t* proj_flags, float* ips_work,
-                                int32_t* search_work, int32_t* freq_idx, uint32_t* status, void* stream) {
+                                int32_t* search_work, int32_t* freq_idx, uint32_t* status,
+                                const tl_lattice* lattice, void* stream) {
     if (!f) return fail(TL_EINVAL, "tl_select_freq_binary: forest is NULL");
+    if (lattice && (lattice->forest != f || lattice->dev.F != n_freqs))
+        return fail(TL_EINVAL, "tl_select_freq_binary: the lattice was built from another forest or frequency count");
     if (n_scenarios < 0 || n_scenarios > 0x7fffffffll)
         return fail(TL_EINVAL, "tl_select_freq_binary: n_scenarios %lld outside [0, 2^31-1]", (long long)n_scenarios);
     if (n_freqs < 1 || n_freqs > TL_MAX_FREQS)
@@ -633,15 +660,27 @@ tl_status tl_select_freq_binary(const tl_forest* f, int64_t n_scenarios, int32_t
     c.fidx = search_work + 2 * n_scenarios;
     c.engine = engine_size;
     c.out = ips_work;
+    tl::GatherParams gp{};
+    gp.S = n_scenarios;
+    gp.H = horizon;
+    gp.kv = kv;
+    gp.batch = batch;
+    gp.engine = f->dev.n_features == 4 ? engine_size : nullptr;
+    gp.out = ips_work;
+    // M at every scenario's probe: a table read per row with a lattice, walks otherwise
+    auto model = [&]() {
+        return lattice ? tl::launch_lattice_column(f->dev, lattice->dev, gp, c.fidx, 0, st)
+                       : tl::launch_forest_column(f->dev, c, st);
+    };
     int32_t rounds = 0;
     while ((int64_t)1 << rounds < n_freqs) ++rounds;
     hipError_t e = tl::launch_search_step(sp, 0, st);
     for (int32_t r = 0; r < rounds && e == hipSuccess; ++r) {
-        e = tl::launch_forest_column(f->dev, c, st);
+        e = model();
         if (e == hipSuccess) e = tl::launch_search_step(sp, 1, st);
     }
     if (e == hipSuccess) e = tl::launch_search_step(sp, 3, st);
-    if (e == hipSuccess) e = tl::launch_forest_column(f->dev, c, st);
+    if (e == hipSuccess) e = model();
     if (e == hipSuccess) e = tl::launch_search_step(sp, 2, st);
     return from_hip(e, "tl_select_freq_binary: launch");
 }

@@ -142,7 +142,48 @@ __global__ __launch_bounds__(kGatherThreads) void lattice_gather_kernel(ForestDe
     }
 }
 
+// M at one frequency per scenario (index fidx[s], or f_all; scenarios with
+// an index < 0 are skipped): one thread per (scenario, iteration), one table
+// read.
+__global__ __launch_bounds__(kGatherThreads) void lattice_column_kernel(ForestDev f, LatticeDev L, GatherParams P,
+                                                                         const int32_t* fidx, int32_t f_all,
+                                                                         int32_t n_jb) {
+    const int64_t s = blockIdx.x / (uint32_t)n_jb;
+    const int32_t j = (int32_t)(blockIdx.x % (uint32_t)n_jb) * kGatherThreads + threadIdx.x;
+    if (j >= P.H) return;
+    const int32_t fi = fidx ? fidx[s] : f_all;
+    if (fi < 0 || fi >= L.F) return;
+    const int32_t kv = P.kv[s * P.H + j];
+    const int32_t b = P.batch[s * P.H + j];
+    const float xe = P.engine ? P.engine[s] : 0.0f;
+    int32_t e = 0;
+    if (L.nf == 4) {
+        e = -1;
+        for (int32_t q = 0; q < L.nE; ++q)
+            if (L.engines[q] == xe) { e = q; break; }
+    }
+    float v;
+    if (e >= 0 && kv >= 0 && kv <= L.kv_max && b >= 0 && b <= L.batch_max) {
+        v = L.table[((((int64_t)e * L.nB + b) * L.nC) * kLatticeChunk + kv) * L.F + fi];
+    } else {
+        const float x[4] = {L.freqs[fi], (float)kv, (float)b, xe};
+        v = walk_global(f, x);
+    }
+    P.out[s * P.H + j] = v;
+}
+
 }  // namespace
+
+hipError_t launch_lattice_column(const ForestDev& f, const LatticeDev& L, const GatherParams& p,
+                                 const int32_t* fidx, int32_t f_all, hipStream_t stream) {
+    if (p.S == 0) return hipSuccess;
+    const int32_t n_jb = (p.H + kGatherThreads - 1) / kGatherThreads;
+    const int64_t blocks = p.S * n_jb;
+    if (!grid_fits(blocks)) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(lattice_column_kernel, dim3((unsigned)blocks), dim3(kGatherThreads), 0, stream, f, L, p, fidx,
+                       f_all, n_jb);
+    return hipGetLastError();
+}
 
 hipError_t launch_lattice_inputs(const LatticeDev& L, int64_t s0, int64_t count, int32_t* kv, int32_t* batch,
                                  float* engine, hipStream_t stream) {

@@ -205,6 +205,9 @@ hipError_t launch_lattice_inputs(const LatticeDev& L, int64_t s0, int64_t count,
 hipError_t launch_lattice_transpose(const float* src, float* table, int64_t s0, int64_t count, int32_t F,
                                     hipStream_t stream);
 hipError_t launch_lattice_gather(const ForestDev& f, const LatticeDev& L, const GatherParams& p, hipStream_t stream);
+// M at one frequency per scenario from the table: out [S][H]
+hipError_t launch_lattice_column(const ForestDev& f, const LatticeDev& L, const GatherParams& p,
+                                 const int32_t* fidx, int32_t f_all, hipStream_t stream);
 
 // A launch of `blocks` workgroups fits the grid (at most 2^31 - 1 in x).
 inline bool grid_fits(int64_t blocks) { return blocks >= 0 && blocks <= 0x7fffffffll; }

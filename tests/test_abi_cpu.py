@@ -135,7 +135,7 @@ def test_adjust_lengths_rejects_bad_arguments():
 def test_binary_search_rejects_bad_arguments():
     L = _lib.lib()
     d = ctypes.c_void_p(16)
-    args = [d, 1, 4, 8] + [d] * 12 + [None]
+    args = [d, 1, 4, 8] + [d] * 12 + [None, None]
     for pos, bad, needle in ((0, None, "forest is NULL"), (1, -1, "n_scenarios"), (2, 0, "n_freqs"),
                              (2, 4097, "n_freqs"), (3, 0, "horizon"), (4, None, "NULL required pointer")):
         a = list(args)

@@ -63,3 +63,42 @@ def test_lattice_scaled_c3(gpu):
     torch.cuda.synchronize()
     assert torch.equal(got, ctl.ips)
     lat.close()
+
+
+@pytest.mark.parametrize("ci,over", [(1, dict(n_scenarios=12)), (3, dict(n_scenarios=8, forest_n_trees=200))])
+def test_lattice_in_admission_and_binary_search(gpu, ci, over):
+    """Admission what-ifs and the binary search read M from a lattice with
+    the same decisions, indices and IPS as with walks; a lattice of another
+    forest is refused."""
+    import torch
+    from paper_2408_05235_amd import api, _lib
+    cfg = synth.scaled(configs.get_config(ci), **over)
+    inp = synth.make_inputs(cfg)
+    d = api.upload(inp)
+    ctl = api.Controller(d, api.Forest.from_dict(inp["forest"]))
+    ctl.project()
+    engines = [1.0, 2.0, 4.0, 8.0] if inp["n_features"] == 4 else None
+    # bounds smaller than the workload: rows past them are walked, also exactly
+    lat = api.Lattice(ctl.forest, d["freqs_mhz"], 20000, 140, engines)
+    i0, s0 = [x.clone() for x in ctl.select_binary()]
+    i1, s1 = ctl.select_binary(lat)
+    torch.cuda.synchronize()
+    assert torch.equal(i0, i1) and torch.equal(s0, s1)
+    cand = synth.make_candidates(cfg, inp)
+    t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a, dt).view(np.int64 if dt == np.uint64 else dt)).cuda()
+    fmax = float(inp["freqs_mhz"][-1])
+    args = (ctl.forest, fmax, d["tbt_slo_ns"], t(cand["cand_prompt"], np.int32), t(cand["cand_len"], np.int32),
+            d["req_offset"], d["prompt"], d["generated"], d["remaining"], d["arrival"], d["kv_capacity"],
+            d["horizon"], d["block_tokens"], d["deadline_ns"], d["lost"], d["batch_cap"], d["engine_size"],
+            t(cand["cand_deadline_ns"], np.uint64))
+    a0 = api.tl_admit(*args)
+    a0 = {k: v.clone() for k, v in a0.items()}
+    a1 = api.tl_admit(*args, lattice=lat)
+    torch.cuda.synchronize()
+    for k in ("decision", "ips", "kv", "batch", "flags"):
+        assert torch.equal(a0[k], a1[k]), k
+    other = api.Forest.from_dict(random_forest(np.random.default_rng(5), 4, 3, inp["n_features"]))
+    with pytest.raises(_lib.TLError):
+        api.tl_admit(other, *args[1:], lattice=lat)
+    lat.close()
+    other.close()
