@@ -215,7 +215,7 @@ __device__ __forceinline__ bool in_box(const float4& b, float kv, float bs) {
 constexpr int kLdsWaves = TL_LDS_WAVES;  // wavefronts per workgroup
 constexpr int kLdsThreads = kLdsWaves * kWave;
 #ifndef TL_STAGE_REGS
-#define TL_STAGE_REGS (6 * 16 / TL_LDS_WAVES)
+#define TL_STAGE_REGS (5 * 16 / TL_LDS_WAVES)
 #endif
 constexpr int kStageRegs = TL_STAGE_REGS;  // staged 16-byte words per thread per block
 
