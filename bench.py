@@ -206,6 +206,54 @@ def adjust_lengths_bench(inp, dev_in, steps, copy_gbs):
             "frac_of_copy": byt / (ms / 1e3) / 1e9 / copy_gbs, "frac_of_hbm_peak": byt / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}
 
 
+def materialized_rows_bench(inp, dev_in, forest, ctl, steps, copy_gbs, sample_rows=1 << 20):
+    """The path that writes the feature rows out (a separate mode, not the
+    headline): tl_project with rows, HBM-write-bound at 4·n_features bytes
+    per (s, f, j) row on top of its curve bytes, against the HBM peak and the
+    measured copy; then the generic row kernel (tl_forest_predict, every tree
+    walked from the root for every row) on the first `sample_rows` rows,
+    checked against the grid path's IPS of the same rows."""
+    import torch
+
+    from paper_2408_05235_amd import api
+    S, H, F, nf = inp["n_scenarios"], inp["horizon"], inp["n_freqs"], inp["n_features"]
+    rows = S * F * H
+    mctl = api.Controller(dev_in, forest, materialize_rows=True)
+    mctl.project()
+    torch.cuda.synchronize()
+    ev = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        mctl.project()
+        e1.record()
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    byt = algorithmic_bytes(inp, F, rows)["project"] + rows * nf * 4
+    n = min(sample_rows, rows)
+    x = mctl.buf["rows"].view(-1, nf)[:n]
+    out = torch.empty(n, dtype=torch.float32, device="cuda:0")
+    forest.tl_forest_predict(x, out)
+    torch.cuda.synchronize()
+    same = bool(torch.equal(out, ctl.ips.view(-1)[:n]))
+    ev = []
+    for _ in range(max(1, steps // 2)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        forest.tl_forest_predict(x, out)
+        e1.record()
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    pms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    del mctl, x, out
+    torch.cuda.empty_cache()
+    gbs = byt / (ms / 1e3) / 1e9
+    return {"rows_bytes": rows * nf * 4, "project_ms": ms, "project_gbs": gbs, "frac_of_hbm_peak": gbs / HBM_PEAK_GBS,
+            "frac_of_copy": gbs / copy_gbs,
+            "row_kernel": {"rows": n, "ms": pms, "rows_per_s": n / (pms / 1e3), "same_ips_as_grid": same}}
+
+
 LATTICE_FILE = os.path.join(ROOT, "profiles", "lattice_{}_traffic.json")
 
 
@@ -504,6 +552,7 @@ def main():
     }
     out["results_d2h_ms"] = d2h_results_ms(ctl)
     out["adjust_lengths"] = adjust_lengths_bench(inp, dev_in, args.steps, copy_gbs)
+    out["materialized_rows"] = materialized_rows_bench(inp, dev_in, forest, ctl, args.steps, copy_gbs)
     out["lattice"] = lattice_bench(inp, cfg, ctl, args.steps, args.warmup,
                                    lambda lat: admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup, lat))
     out["binary_search"] = binary_search_bench(ctl, args.steps, args.warmup)

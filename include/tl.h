@@ -258,7 +258,9 @@ tl_status tl_forest_predict_grid(const tl_forest* forest, int64_t n_scenarios, i
  *   size not in the list) are walked.
  * freqs_mhz: device [n_freqs], copied.  engine_values: host
  * [n_engines <= 16], required for 4-feature forests (ignored otherwise).
- * The build is enqueued on `stream`; the forest must outlive the lattice.
+ * The build is enqueued on `stream`, which the call synchronizes once (to
+ * keep a host copy of the frequency list); the forest must outlive the
+ * lattice.
  * Errors: TL_EINVAL, TL_EUNSUPPORTED (table too large), TL_ENOMEM,
  * TL_EDEVICE.
  * ---------------------------------------------------------------------- */
@@ -307,8 +309,11 @@ tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs,
  * freqs_mhz [F] ascending; engine_size [S] for 4-feature forests.
  * Work arrays of the caller: ips_work [S][H] fp32 (left holding M at the
  * final probe) and search_work [3][S] int32.  Allocates nothing.
- * lattice (nullable): a table of the same forest built for freqs_mhz
- * (tl_lattice_create); M at the probes is then read from it (same values).
+ * lattice (nullable): a table of the same forest and frequency count
+ * (tl_lattice_create; TL_EINVAL otherwise); M at the probes is then read
+ * from it, at the lattice's own frequencies (the same values when it was
+ * built for freqs_mhz, which is the caller's to ensure: the list itself is
+ * not compared).
  * ---------------------------------------------------------------------- */
 tl_status tl_select_freq_binary(const tl_forest* forest, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
                                 const float* freqs_mhz, const int32_t* kv, const int32_t* batch,

@@ -341,6 +341,8 @@ tl_status tl_admit(const tl_admit_args* a, void* stream) {
     if (f->dev.n_features != 3 && f->dev.n_features != 4)
         return fail(TL_EINVAL, "tl_admit: the forest has %d features, admission needs 3 or 4", f->dev.n_features);
     if (f->dev.n_features == 4 && !a->engine_size) return fail(TL_EINVAL, "tl_admit: 4 features need engine_size");
+    if (a->lattice && a->lattice->forest != f)
+        return fail(TL_EINVAL, "tl_admit: the lattice was built from another forest");
     const int64_t S = a->proj.n_scenarios;
     if (S == 0) return ok();
     const hipStream_t st_h = (hipStream_t)stream;
@@ -358,7 +360,6 @@ tl_status tl_admit(const tl_admit_args* a, void* stream) {
     c.out = a->ips;
     int32_t lat_f = -1;
     if (a->lattice) {
-        if (a->lattice->forest != f) return fail(TL_EINVAL, "tl_admit: the lattice was built from another forest");
         const std::vector<float>& hf = a->lattice->host_freqs;
         for (size_t q = 0; q < hf.size(); ++q)
             if (hf[q] == a->max_freq_mhz) { lat_f = (int32_t)q; break; }

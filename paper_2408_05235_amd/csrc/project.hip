@@ -446,16 +446,19 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
             outB[t] = b;
             outKV[t] = k;
             if (P.rows) {
+                // one 16- or 12-byte store per row; consecutive lanes write
+                // consecutive rows of one frequency
                 const float kf = (float)k, bf = (float)b;
-                for (int32_t f = 0; f < P.F; ++f) {
-                    float* row = P.rows + (((int64_t)s * P.F + f) * H + t) * P.nf;
-                    if (P.nf == 4) {
-                        *(float4*)row = make_float4(P.freqs[f], kf, bf, eng);
-                    } else {
-                        row[0] = P.freqs[f];
-                        row[1] = kf;
-                        row[2] = bf;
-                    }
+                float* row = P.rows + ((int64_t)s * P.F * H + t) * P.nf;
+                const int64_t f_stride = (int64_t)H * P.nf;
+                if (P.nf == 4) {
+#pragma unroll 4
+                    for (int32_t f = 0; f < P.F; ++f)
+                        *(float4*)(row + f * f_stride) = make_float4(P.freqs[f], kf, bf, eng);
+                } else {
+#pragma unroll 4
+                    for (int32_t f = 0; f < P.F; ++f)
+                        *(float3*)(row + f * f_stride) = make_float3(P.freqs[f], kf, bf);
                 }
             }
         }

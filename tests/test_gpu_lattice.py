@@ -98,7 +98,14 @@ def test_lattice_in_admission_and_binary_search(gpu, ci, over):
     for k in ("decision", "ips", "kv", "batch", "flags"):
         assert torch.equal(a0[k], a1[k]), k
     other = api.Forest.from_dict(random_forest(np.random.default_rng(5), 4, 3, inp["n_features"]))
+    # refused on the host before anything is enqueued: the outputs keep
+    # what they held
+    sentinel = {k: v.clone().fill_(-7) for k, v in a1.items()}
+    out = {k: v.clone() for k, v in sentinel.items()}
     with pytest.raises(_lib.TLError):
-        api.tl_admit(other, *args[1:], lattice=lat)
+        api.tl_admit(other, *args[1:], out=out, lattice=lat)
+    torch.cuda.synchronize()
+    for k in sentinel:
+        assert torch.equal(out[k], sentinel[k]), k
     lat.close()
     other.close()
