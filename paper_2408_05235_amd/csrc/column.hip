@@ -16,6 +16,11 @@
 // order and rounded once, as everywhere in the library.
 //
 // Forests too deep for LDS records are walked from global memory.
+//
+// Rows mode (P.rows): the same kernel on arbitrary feature rows, lane l of
+// item i taking rows i*64*RPL + l + 64 r; every row carries its own
+// frequency and engine size.  tl_forest_predict uses it for 3- and
+// 4-feature forests with LDS records.
 #include <algorithm>
 
 #include "device_util.h"
@@ -66,8 +71,8 @@ __device__ __forceinline__ float column_freq(const ColumnParams& P, int64_t s) {
 // interleaved, and adds the leaves to each row's sum in tree order.
 template <int NF, int NT, int RPL>
 __device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, uint32_t vals_off, int32_t depth,
-                                           float xf, const float (&kv)[RPL], const float (&bs)[RPL], float xe,
-                                           double (&acc)[RPL]) {
+                                           const float (&xf)[RPL], const float (&kv)[RPL], const float (&bs)[RPL],
+                                           const float (&xe)[RPL], double (&acc)[RPL]) {
     uint32_t a[RPL][NT], cl[NT], cr[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -89,7 +94,7 @@ __device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, ui
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const uint4 nd = make_uint4(w[r][t].x, w[r][t].y, w[r][t].z, w[r][t].w);
-                const bool left = node_feature<NF>(nd, xf, kv[r], bs[r], xe) < __uint_as_float(nd.x);
+                const bool left = node_feature<NF>(nd, xf[r], kv[r], bs[r], xe[r]) < __uint_as_float(nd.x);
                 a[r][t] = 2u * a[r][t] + (left ? cl[t] : cr[t]);
             }
     }
@@ -104,7 +109,7 @@ __device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, ui
         }
 }
 
-template <int NF, int RPL>
+template <int NF, int RPL, bool ROWS>
 __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const uint4* __restrict__ records,
                                                                        int32_t n_trees, int32_t depth, int32_t tb,
                                                                        float base, ColumnParams P) {
@@ -114,18 +119,42 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     const uint32_t buf_bytes = (uint32_t)tb * R.bytes;
     const int wave = threadIdx.x / kWave;
     const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kColWaves + wave);
-    const ColumnItem<RPL> c = column_item<RPL>(P, item);
-    const float xf = column_freq(P, c.s);
-    const float xe = NF == 4 ? P.engine[c.s] : 0.0f;
-    float kv[RPL], bs[RPL];
+    float xf[RPL], kv[RPL], bs[RPL], xe[RPL];
     double acc[RPL];
+    int64_t o[RPL];     // output index of each row, < 0: none
+    bool valid;         // the wavefront has rows (uniform)
+    if (ROWS) {
+        const int64_t first = item * (kWave * RPL);
+        valid = first < P.n_rows;
+#pragma unroll
+        for (int r = 0; r < RPL; ++r) {
+            const int64_t i = first + lane_id() + r * kWave;
+            o[r] = i < P.n_rows ? i : -1;
+            const float* x = P.rows + (valid ? min(i, P.n_rows - 1) : 0) * NF;
+            xf[r] = x[0];
+            kv[r] = x[1];
+            bs[r] = x[2];
+            xe[r] = NF == 4 ? x[3] : 0.0f;
+        }
+    } else {
+        const ColumnItem<RPL> c = column_item<RPL>(P, item);
+        valid = c.valid;
+        const float f_s = column_freq(P, c.s);
+        const float e_s = NF == 4 ? P.engine[c.s] : 0.0f;
+#pragma unroll
+        for (int r = 0; r < RPL; ++r) {
+            xf[r] = f_s;
+            xe[r] = e_s;
+            kv[r] = (float)P.kv[c.s * P.H + c.j[r]];
+            bs[r] = (float)P.batch[c.s * P.H + c.j[r]];
+            o[r] = c.row[r] ? c.s * P.H + c.j[r] : -1;
+        }
+    }
 #pragma unroll
     for (int r = 0; r < RPL; ++r) {
-        kv[r] = (float)P.kv[c.s * P.H + c.j[r]];
-        bs[r] = (float)P.batch[c.s * P.H + c.j[r]];
         acc[r] = (double)base;
         // the rows are complete before any staging load is in flight
-        asm volatile("" ::"v"(kv[r]), "v"(bs[r]));
+        asm volatile("" ::"v"(xf[r]), "v"(kv[r]), "v"(bs[r]), "v"(xe[r]));
     }
 
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
@@ -161,7 +190,6 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
         TL_COL_STORE_WORD(4, st4) TL_COL_STORE_WORD(5, st5)                    \
         TL_COL_STORE_WORD(6, st6) TL_COL_STORE_WORD(7, st7)                    \
     }
-    asm volatile("" ::"v"(xf), "v"(xe));
     if (n_blocks > 0) {
         TL_COL_FETCH(0)
         TL_COL_STORE(0, 0)
@@ -170,7 +198,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     for (int32_t b = 0; b < n_blocks; ++b) {
         const int cur = b & 1;
         if (b + 1 < n_blocks) TL_COL_FETCH(b + 1)
-        if (c.valid) {
+        if (valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
             const uint32_t first = lds_addr(smem) + cur * buf_bytes;
             int32_t t = 0;
@@ -190,7 +218,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
 #undef TL_COL_FETCH_WORD
 #pragma unroll
     for (int r = 0; r < RPL; ++r)
-        if (c.row[r]) P.out[c.s * P.H + c.j[r]] = (float)acc[r];
+        if (o[r] >= 0) P.out[o[r]] = (float)acc[r];
 }
 
 // Global-memory walks for forests without LDS records.
@@ -235,12 +263,12 @@ int32_t column_trees_per_block(const ForestDev& f, size_t* lds) {
     return tb;
 }
 
-template <int NF, int RPL>
+template <int NF, int RPL, bool ROWS = false>
 hipError_t launch_column_lds(const ForestDev& f, const ColumnParams& c, int32_t tb, size_t lds, hipStream_t stream) {
-    const int64_t n_cols = (c.H + kWave * RPL - 1) / (kWave * RPL);
-    const int64_t items = c.S * n_cols;
+    const int64_t span = kWave * RPL;
+    const int64_t items = ROWS ? (c.n_rows + span - 1) / span : c.S * ((c.H + span - 1) / span);
     if (!grid_fits((items + kColWaves - 1) / kColWaves)) return hipErrorInvalidConfiguration;
-    const auto kern = forest_column_lds_kernel<NF, RPL>;
+    const auto kern = forest_column_lds_kernel<NF, RPL, ROWS>;
     const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3((unsigned)((items + kColWaves - 1) / kColWaves)), dim3(kColThreads), lds, stream,
@@ -271,6 +299,20 @@ hipError_t launch_column(const ForestDev& f, const ColumnParams& c, hipStream_t 
 hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream) {
     if (c.S == 0) return hipSuccess;
     return f.n_features == 4 ? launch_column<4>(f, c, stream) : launch_column<3>(f, c, stream);
+}
+
+hipError_t launch_forest_rows_lds(const ForestDev& f, const float* rows, int64_t n_rows, float* out,
+                                  hipStream_t stream) {
+    size_t lds = 0;
+    const int32_t tb = (f.n_features == 3 || f.n_features == 4) ? column_trees_per_block(f, &lds) : 0;
+    if (tb <= 0) return hipErrorNotSupported;
+    if (n_rows == 0) return hipSuccess;
+    ColumnParams c{};
+    c.rows = rows;
+    c.n_rows = n_rows;
+    c.out = out;
+    return f.n_features == 4 ? launch_column_lds<4, 4, true>(f, c, tb, lds, stream)
+                             : launch_column_lds<3, 4, true>(f, c, tb, lds, stream);
 }
 
 }  // namespace tl

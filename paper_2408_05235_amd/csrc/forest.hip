@@ -38,7 +38,8 @@
 // kernel.
 //
 // forest_rows_kernel evaluates arbitrary rows: each thread walks RPT
-// consecutive rows through every tree.
+// consecutive rows through every tree (forests without LDS records; the
+// others take the column kernel's staged walks).
 #include <hipcub/hipcub.hpp>
 
 #include "device_util.h"
@@ -657,6 +658,10 @@ hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g_in, hipStr
 
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,
                               hipStream_t stream) {
+    // 3- and 4-feature forests with LDS records: the staged walks of the
+    // column kernel; otherwise walks from global memory
+    const hipError_t e = launch_forest_rows_lds(f, rows, n_rows, out, stream);
+    if (e != hipErrorNotSupported) return e;
     switch (f.n_features) {
         case 1: return launch_nf<1>(f, rows, n_rows, out, stream);
         case 2: return launch_nf<2>(f, rows, n_rows, out, stream);

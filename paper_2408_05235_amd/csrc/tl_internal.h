@@ -52,6 +52,10 @@ struct ColumnParams {
     const int32_t* fidx;            // nullable
     const float* engine;            // 4-feature forests
     float* out;
+    // rows mode (rows != NULL): out[i] = M(rows[i][0 .. n_features - 1]) for
+    // i < n_rows; the fields above except `out` are not used
+    const float* rows;
+    int64_t n_rows;
 };
 
 // Admission decision from the IPS at the maximum frequency.
@@ -219,6 +223,10 @@ hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_r
 hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, hipStream_t stream);
 hipError_t launch_select(const SelectParams& p, hipStream_t stream);
 hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream);
+// The same kernel on arbitrary rows [n_rows][n_features] (3 or 4 features,
+// LDS records present); hipErrorNotSupported when the forest has no records.
+hipError_t launch_forest_rows_lds(const ForestDev& f, const float* rows, int64_t n_rows, float* out,
+                                  hipStream_t stream);
 hipError_t launch_admit(const AdmitParams& p, hipStream_t stream);
 // mode 0: init, 1: one search step, 3: probe lo, 2: final check
 hipError_t launch_search_step(const SearchParams& p, int mode, hipStream_t stream);

@@ -259,8 +259,11 @@ def random_rows(rng, n, nf, kvmax=5000, bmax=300):
     return x
 
 
+# 3- and 4-feature forests up to depth 11 take the LDS-staged row walks
+# (odd tree counts end on a single tree), the others the global-memory walks
 @pytest.mark.parametrize("T,d,nf,n", [(0, 3, 3, 100), (1, 0, 3, 77), (5, 1, 1, 1000), (50, 6, 3, 12345),
-                                      (20, 10, 4, 4099), (7, 14, 2, 513), (300, 8, 3, 65537)])
+                                      (20, 10, 4, 4099), (7, 14, 2, 513), (300, 8, 3, 65537),
+                                      (33, 11, 4, 3001), (9, 9, 4, 100003), (3, 12, 3, 999)])
 def test_forest_random(gpu, T, d, nf, n):
     import torch
     api = _api()
