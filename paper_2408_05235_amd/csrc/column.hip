@@ -15,6 +15,12 @@
 // room for only two trees per block).  Leaves are accumulated in fp64 in tree
 // order and rounded once, as everywhere in the library.
 //
+// On horizons of at least 512 iterations and grids of at least one
+// workgroup per CU, forest_column_reuse_kernel gives each lane 8
+// consecutive iterations instead and reuses leaves along them (the grid
+// kernel's box test, per lane), unless the wavefront's batch changes on
+// most row-to-row steps.
+//
 // Forests too deep for LDS records are walked from global memory.
 //
 // Rows mode (P.rows): the same kernel on arbitrary feature rows, lane l of
@@ -32,7 +38,7 @@ namespace {
 
 constexpr int kColWaves = 16;
 constexpr int kColThreads = kColWaves * kWave;
-constexpr int kColStage = 8;                       // staged 16-byte words per thread per block
+constexpr int kColStage = 6;                       // staged 16-byte words per thread per block
 constexpr size_t kColLdsBudget = 152 * 1024;
 
 template <int RPL>
@@ -160,10 +166,10 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
     // block b: trees [b*tb, b*tb + cnt), one contiguous range of words; each
     // thread moves word threadIdx.x + r * kColThreads through register st<r>
-    static_assert(kColStage == 8, "staging below names eight registers");
+    static_assert(kColStage >= 1 && kColStage <= 8, "staging below names up to eight registers");
     uint4 st0 = make_uint4(0, 0, 0, 0), st1 = st0, st2 = st0, st3 = st0, st4 = st0, st5 = st0, st6 = st0, st7 = st0;
 #define TL_COL_FETCH_WORD(r, reg)                                              \
-    {                                                                          \
+    if ((r) < kColStage) {                                                     \
         const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
         reg = src[i < words ? i : 0];                                          \
     }
@@ -177,7 +183,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
         TL_COL_FETCH_WORD(6, st6) TL_COL_FETCH_WORD(7, st7)                    \
     }
 #define TL_COL_STORE_WORD(r, reg)                                              \
-    {                                                                          \
+    if ((r) < kColStage) {                                                     \
         const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
         if (i < words) dst[i] = reg;                                           \
     }
@@ -219,6 +225,213 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
 #pragma unroll
     for (int r = 0; r < RPL; ++r)
         if (o[r] >= 0) P.out[o[r]] = (float)acc[r];
+}
+
+// Whether (kv, batch) lies in a leaf box (kv_lo, kv_hi, batch_lo, batch_hi).
+__device__ __forceinline__ bool col_in_box(const float4& b, float kv, float bs) {
+    return (kv >= b.x) & (kv < b.y) & (bs >= b.z) & (bs < b.w);
+}
+
+// A leaf box read from LDS (byte address).
+__device__ __forceinline__ float4 lds_box(uint32_t addr) {
+    const u32x4 w = *(lds_u32x4*)(uintptr_t)addr;
+    return make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
+}
+
+__device__ __forceinline__ float4 col_box_meet(const float4& a, const float4& b) {
+    return make_float4(a.x > b.x ? a.x : b.x, a.y < b.y ? a.y : b.y, a.z > b.z ? a.z : b.z, a.w < b.w ? a.w : b.w);
+}
+
+// Leaf reuse along a lane's rows: a lane takes RPL consecutive iterations of
+// the scenario and keeps, for NT (1 or 2) consecutive staged trees, the
+// leaves its last walk reached and the intersection of their KV / batch
+// boxes (a row inside it reaches the same leaves: the frequency and engine
+// size are the scenario's).  A row outside walks only the tree(s) whose own
+// box it left, both in one interleaved pass when the wavefront needs both.
+template <int NF, int NT, int RPL>
+__device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayout& R, int32_t depth, float xf,
+                                                 const float (&kv)[RPL], const float (&bs)[RPL], float xe,
+                                                 double (&acc)[RPL]) {
+    typedef __attribute__((address_space(3))) const float lds_f32;
+    const uint32_t vals0 = tree + R.vals, boxes0 = tree + R.boxes;
+    const uint32_t vals1 = vals0 + R.bytes, boxes1 = boxes0 + R.bytes;
+    float4 box = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
+    int32_t leaf[NT];
+    double v[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        leaf[t] = 0;
+        v[t] = 0.0;
+    }
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) {
+        bool moved = true;   // this lane reached other leaves: reload values and box
+        if (r == 0) {
+            // first row: every tree, every lane
+            int32_t k[NT];
+            walk<NF, NT>(tree, R.bytes, depth, xf, kv[0], bs[0], xe, k);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) leaf[t] = k[t];
+        } else if (!col_in_box(box, kv[r], bs[r])) {
+            if (NT == 1) {
+                int32_t k[1];
+                walk<NF, 1>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
+                leaf[0] = k[0];
+            } else {
+                const bool n0 = !col_in_box(lds_box(boxes0 + 16u * leaf[0]), kv[r], bs[r]);
+                const bool n1 = !col_in_box(lds_box(boxes1 + 16u * leaf[NT - 1]), kv[r], bs[r]);
+                if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
+                    int32_t k[2];
+                    walk<NF, 2>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
+                    leaf[0] = k[0];
+                    leaf[NT - 1] = k[1];
+                } else {
+                    if (n0) {
+                        int32_t k[1];
+                        walk<NF, 1>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
+                        leaf[0] = k[0];
+                    }
+                    if (n1) {
+                        int32_t k[1];
+                        walk<NF, 1>(tree + R.bytes, R.bytes, depth, xf, kv[r], bs[r], xe, k);
+                        leaf[NT - 1] = k[0];
+                    }
+                }
+            }
+        } else {
+            moved = false;
+        }
+        if (moved) {
+            v[0] = (double)*(lds_f32*)(uintptr_t)(vals0 + 4u * leaf[0]);
+            box = lds_box(boxes0 + 16u * leaf[0]);
+            if (NT == 2) {
+                v[NT - 1] = (double)*(lds_f32*)(uintptr_t)(vals1 + 4u * leaf[NT - 1]);
+                box = col_box_meet(box, lds_box(boxes1 + 16u * leaf[NT - 1]));
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[r] += v[t];
+        asm volatile("" ::"v"(acc[r]));
+    }
+}
+
+// M at one frequency per scenario with leaf reuse along each lane's RPL
+// consecutive iterations (a wavefront takes 64 x RPL consecutive
+// iterations of one scenario); staging as in forest_column_lds_kernel.
+// Reuse pays where the rows move slowly; a wavefront whose batch changes
+// on more than half of its row-to-row steps (arrivals and completions at
+// most iterations) walks every row instead, four rows x two trees
+// interleaved, as forest_column_lds_kernel does.
+template <int NF, int RPL>
+__global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const uint4* __restrict__ records,
+                                                                         int32_t n_trees, int32_t depth,
+                                                                         int32_t tb, float base, ColumnParams P) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const RecordLayout R = record_layout(depth);
+    const uint32_t rec_words = R.bytes / 16u;
+    const uint32_t buf_bytes = (uint32_t)tb * R.bytes;
+    const int wave = threadIdx.x / kWave;
+    const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kColWaves + wave);
+    const int32_t span = kWave * RPL;
+    const int32_t n_cols = (P.H + span - 1) / span;
+    bool valid = item < P.S * n_cols;
+    const int64_t s = valid ? item / n_cols : 0;
+    if (P.fidx && P.fidx[s] < 0) valid = false;
+    const int32_t j0 = (int32_t)(item % n_cols) * span + lane_id() * RPL;
+    const float xf = column_freq(P, s);
+    const float xe = NF == 4 ? P.engine[s] : 0.0f;
+    float kv[RPL], bs[RPL];
+    double acc[RPL];
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) {
+        const int32_t j = min(j0 + r, P.H - 1);
+        kv[r] = (float)P.kv[s * P.H + j];
+        bs[r] = (float)P.batch[s * P.H + j];
+        acc[r] = (double)base;
+        asm volatile("" ::"v"(kv[r]), "v"(bs[r]));
+    }
+    asm volatile("" ::"v"(xf), "v"(xe));
+    // how often the batch changes from one row to the next, over the wavefront
+    int32_t steps_changed = 0;
+#pragma unroll
+    for (int r = 1; r < RPL; ++r) steps_changed += __builtin_popcountll(__builtin_amdgcn_ballot_w64(bs[r] != bs[r - 1]));
+    const bool reuse = 2 * steps_changed <= kWave * (RPL - 1);   // wavefront-uniform
+    static_assert(RPL % 4 == 0, "the walk-every-row path takes four rows at a time");
+    const int32_t n_blocks = (n_trees + tb - 1) / tb;
+    static_assert(kColStage >= 1 && kColStage <= 8, "staging below names up to eight registers");
+    uint4 st0 = make_uint4(0, 0, 0, 0), st1 = st0, st2 = st0, st3 = st0, st4 = st0, st5 = st0, st6 = st0, st7 = st0;
+#define TL_COL_FETCH_WORD(r, reg)                                              \
+    if ((r) < kColStage) {                                                     \
+        const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
+        reg = src[i < words ? i : 0];                                          \
+    }
+#define TL_COL_FETCH(b)                                                        \
+    {                                                                          \
+        const uint32_t words = (uint32_t)min(tb, n_trees - (b) * tb) * rec_words; \
+        const uint4* src = records + (int64_t)(b) * tb * rec_words;            \
+        TL_COL_FETCH_WORD(0, st0) TL_COL_FETCH_WORD(1, st1)                    \
+        TL_COL_FETCH_WORD(2, st2) TL_COL_FETCH_WORD(3, st3)                    \
+        TL_COL_FETCH_WORD(4, st4) TL_COL_FETCH_WORD(5, st5)                    \
+        TL_COL_FETCH_WORD(6, st6) TL_COL_FETCH_WORD(7, st7)                    \
+    }
+#define TL_COL_STORE_WORD(r, reg)                                              \
+    if ((r) < kColStage) {                                                     \
+        const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
+        if (i < words) dst[i] = reg;                                           \
+    }
+#define TL_COL_STORE(b, buf)                                                   \
+    {                                                                          \
+        const uint32_t words = (uint32_t)min(tb, n_trees - (b) * tb) * rec_words; \
+        uint4* dst = (uint4*)(smem + (buf) * buf_bytes);                       \
+        TL_COL_STORE_WORD(0, st0) TL_COL_STORE_WORD(1, st1)                    \
+        TL_COL_STORE_WORD(2, st2) TL_COL_STORE_WORD(3, st3)                    \
+        TL_COL_STORE_WORD(4, st4) TL_COL_STORE_WORD(5, st5)                    \
+        TL_COL_STORE_WORD(6, st6) TL_COL_STORE_WORD(7, st7)                    \
+    }
+    if (n_blocks > 0) {
+        TL_COL_FETCH(0)
+        TL_COL_STORE(0, 0)
+    }
+    __syncthreads();
+    for (int32_t b = 0; b < n_blocks; ++b) {
+        const int cur = b & 1;
+        if (b + 1 < n_blocks) TL_COL_FETCH(b + 1)
+        if (valid) {
+            const int32_t cnt = min(tb, n_trees - b * tb);
+            const uint32_t first = lds_addr(smem) + cur * buf_bytes;
+            int32_t t = 0;
+            if (reuse) {
+                for (; t + 2 <= cnt; t += 2)
+                    add_leaves_reuse<NF, 2, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
+                if (t < cnt) add_leaves_reuse<NF, 1, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
+            } else {
+                const float xf4[4] = {xf, xf, xf, xf}, xe4[4] = {xe, xe, xe, xe};
+#pragma unroll
+                for (int h = 0; h < RPL / 4; ++h) {
+                    const float kv4[4] = {kv[4 * h], kv[4 * h + 1], kv[4 * h + 2], kv[4 * h + 3]};
+                    const float bs4[4] = {bs[4 * h], bs[4 * h + 1], bs[4 * h + 2], bs[4 * h + 3]};
+                    double a4[4] = {acc[4 * h], acc[4 * h + 1], acc[4 * h + 2], acc[4 * h + 3]};
+                    int32_t u = 0;
+                    for (; u + 2 <= cnt; u += 2)
+                        add_leaves<NF, 2, 4>(first + u * R.bytes, R.bytes, R.vals, depth, xf4, kv4, bs4, xe4, a4);
+                    if (u < cnt) add_leaves<NF, 1, 4>(first + u * R.bytes, R.bytes, R.vals, depth, xf4, kv4, bs4, xe4, a4);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[4 * h + i] = a4[i];
+                }
+            }
+        }
+        if (b + 1 < n_blocks) TL_COL_STORE(b + 1, cur ^ 1)
+        __syncthreads();
+    }
+#undef TL_COL_STORE
+#undef TL_COL_STORE_WORD
+#undef TL_COL_FETCH
+#undef TL_COL_FETCH_WORD
+    if (valid) {
+#pragma unroll
+        for (int r = 0; r < RPL; ++r)
+            if (j0 + r < P.H) P.out[s * P.H + j0 + r] = (float)acc[r];
+    }
 }
 
 // Global-memory walks for forests without LDS records.
@@ -276,10 +489,35 @@ hipError_t launch_column_lds(const ForestDev& f, const ColumnParams& c, int32_t 
     return hipGetLastError();
 }
 
+#ifndef TL_COLUMN_REUSE_RPL
+#define TL_COLUMN_REUSE_RPL 8
+#endif
+
 template <int NF>
 hipError_t launch_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream) {
     size_t lds = 0;
     const int32_t tb = column_trees_per_block(f, &lds);
+    if constexpr (TL_COLUMN_REUSE_RPL > 0) {
+        // leaf reuse along RPL consecutive rows a lane, on horizons that
+        // fill a wavefront's 64 x RPL rows and grids that still give every
+        // CU a workgroup (the reuse kernel has half the wavefronts)
+        constexpr int RPL = TL_COLUMN_REUSE_RPL;
+        const int64_t items = c.S * ((c.H + kWave * RPL - 1) / (kWave * RPL));
+        int dev = 0, cus = 0;
+        hipError_t e0 = hipGetDevice(&dev);
+        if (e0 == hipSuccess) e0 = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e0 != hipSuccess) return e0;
+        if (tb > 0 && c.H >= kWave * RPL && items >= (int64_t)kColWaves * cus) {
+            if (!grid_fits((items + kColWaves - 1) / kColWaves)) return hipErrorInvalidConfiguration;
+            const auto kern = forest_column_reuse_kernel<NF, RPL>;
+            const hipError_t e =
+                hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL(kern, dim3((unsigned)((items + kColWaves - 1) / kColWaves)), dim3(kColThreads), lds,
+                               stream, f.records, f.n_trees, f.depth, tb, f.base_score, c);
+            return hipGetLastError();
+        }
+    }
     if (tb > 0) {
         // rows per lane: enough chains to overlap, without idle stripes on
         // short horizons

@@ -152,16 +152,6 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
 
     if (bad_range || bound > 0x7fffffffull) {
         for (int32_t t = lane; t < H; t += kWave) { outB[t] = 0; outKV[t] = 0; }
-        if (P.rows) {
-            for (int32_t f = 0; f < P.F; ++f)
-                for (int32_t t = lane; t < H; t += kWave) {
-                    float* row = P.rows + (((int64_t)s * P.F + f) * H + t) * P.nf;
-                    row[0] = P.freqs[f];
-                    row[1] = 0.0f;
-                    row[2] = 0.0f;
-                    if (P.nf == 4) row[3] = P.engine[s];
-                }
-        }
         if (lane == 0) {
             P.n_iters[s] = 0;
             P.flags[s] = bad_range ? TL_FLAG_OVERFLOW : ((fl & TL_FLAG_BAD_REQUEST) | TL_FLAG_OVERFLOW);
@@ -432,10 +422,9 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     }
     __syncthreads();
 
-    // outputs: curves (batch = prefix sum of BD), optional feature rows, scalars
+    // outputs: curves (batch = prefix sum of BD), scalars
     {
         int32_t carry_b = 0;
-        const float eng = (P.rows && P.nf == 4) ? P.engine[s] : 0.0f;
         for (int32_t t0 = 0; t0 < H; t0 += kWave) {
             const int32_t t = t0 + lane;
             const bool in = t < H;
@@ -445,27 +434,37 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
             const int32_t k = KV[t];
             outB[t] = b;
             outKV[t] = k;
-            if (P.rows) {
-                // one 16- or 12-byte store per row; consecutive lanes write
-                // consecutive rows of one frequency
-                const float kf = (float)k, bf = (float)b;
-                float* row = P.rows + ((int64_t)s * P.F * H + t) * P.nf;
-                const int64_t f_stride = (int64_t)H * P.nf;
-                if (P.nf == 4) {
-#pragma unroll 4
-                    for (int32_t f = 0; f < P.F; ++f)
-                        *(float4*)(row + f * f_stride) = make_float4(P.freqs[f], kf, bf, eng);
-                } else {
-#pragma unroll 4
-                    for (int32_t f = 0; f < P.F; ++f)
-                        *(float3*)(row + f * f_stride) = make_float3(P.freqs[f], kf, bf);
-                }
-            }
         }
     }
     if (lane == 0) {
         P.n_iters[s] = n_end;
         P.flags[s] = fl;
+    }
+}
+
+// Feature rows of the grid, written out when requested: row (s, f, j) =
+// (freq[f], KV[s][j], B[s][j] [, engine[s]]) from the curves project_kernel
+// wrote.  One thread per (s, j) writes its F rows with one 16- or 12-byte
+// store each; consecutive threads write consecutive rows of one frequency.
+constexpr int kRowsThreads = 256;
+
+template <int NF>
+__global__ __launch_bounds__(kRowsThreads) void expand_rows_kernel(ProjectParams P) {
+    const int32_t H = P.H;
+    const int32_t n_jb = (H + kRowsThreads - 1) / kRowsThreads;
+    const int64_t s = blockIdx.x / (uint32_t)n_jb;
+    const int32_t t = (int32_t)(blockIdx.x % (uint32_t)n_jb) * kRowsThreads + threadIdx.x;
+    if (t >= H) return;
+    const float kf = (float)P.kv[s * H + t], bf = (float)P.batch[s * H + t];
+    const float eng = NF == 4 ? P.engine[s] : 0.0f;
+    float* row = P.rows + ((int64_t)s * P.F * H + t) * NF;
+    const int64_t f_stride = (int64_t)H * NF;
+#pragma unroll 4
+    for (int32_t f = 0; f < P.F; ++f) {
+        if (NF == 4)
+            *(float4*)(row + f * f_stride) = make_float4(P.freqs[f], kf, bf, eng);
+        else
+            *(float3*)(row + f * f_stride) = make_float3(P.freqs[f], kf, bf);
     }
 }
 
@@ -518,6 +517,14 @@ hipError_t launch_project(const ProjectParams& p, hipStream_t stream) {
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(project_kernel, dim3((unsigned)p.n_scenarios), dim3(64), lds, stream, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !p.rows) return e;
+    const int64_t blocks = p.n_scenarios * ((p.H + kRowsThreads - 1) / kRowsThreads);
+    if (!grid_fits(blocks)) return hipErrorInvalidConfiguration;
+    if (p.nf == 4)
+        hipLaunchKernelGGL(expand_rows_kernel<4>, dim3((unsigned)blocks), dim3(kRowsThreads), 0, stream, p);
+    else
+        hipLaunchKernelGGL(expand_rows_kernel<3>, dim3((unsigned)blocks), dim3(kRowsThreads), 0, stream, p);
     return hipGetLastError();
 }
 

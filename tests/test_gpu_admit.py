@@ -155,6 +155,26 @@ def test_admit_scaled_configs(gpu, ci, over):
     check_admit(inp, inp["forest"], float(inp["freqs_mhz"][-1]), cand, cfg["name"])
 
 
+@pytest.mark.parametrize("ci,S", [(3, 2048), (4, 1024)])
+def test_admit_model_at_reuse_sizes(gpu, ci, S):
+    """Grids large enough for the column kernel with leaf reuse along each
+    lane's rows: c3's slowly changing rows take its reuse path, c4's batch
+    (arrivals and completions at most iterations) its walk-every-row path.
+    The model at the maximum frequency equals the oracle's on every
+    iteration of the projection the GPU returned (the projection itself is
+    checked against the oracle in the tests above)."""
+    cfg = synth.scaled(configs.get_config(ci), n_scenarios=S, forest_n_trees=60)
+    inp = synth.make_inputs(cfg)
+    cand = synth.make_candidates(cfg, inp)
+    fmax = float(inp["freqs_mhz"][-1])
+    g = gpu_admit(inp, inp["forest"], fmax, cand["cand_prompt"], cand["cand_len"], cand["cand_deadline_ns"])
+    nf = int(inp["n_features"])
+    eng = None if nf == 3 else np.asarray(inp["engine_size"], np.float32)
+    want = oracle.forest_predict(inp["forest"], oracle.rows(np.array([fmax], np.float32), g["batch"], g["kv"],
+                                                            eng, nf))[:, 0]
+    assert assert_ips_close(g["ips"], want, cfg["name"]) == want.size
+
+
 # (config, scenarios checked against the oracle at full size)
 PLAN_FULL = {0: [0], 1: [0, 517, 1023], 2: [0, 128, 255], 3: [0, 2048, 4095], 4: [0, 9000, 16383]}
 

@@ -91,6 +91,30 @@ def test_binary_search_random(gpu, S, F, H, T, d, nf, mono, seed):
     assert len(set(st.tolist())) >= 2
 
 
+def test_binary_search_at_reuse_sizes(gpu):
+    """A grid large enough for the column kernel with leaf reuse along each
+    lane's rows (4096 scenarios x 512 iterations); half of the scenarios have
+    a batch that changes at every iteration, which takes that kernel's
+    walk-every-row path.  Indices and statuses equal the oracle's."""
+    rng = np.random.default_rng(777)
+    S, F, H, T, d, nf = 4096, 5, 512, 20, 6, 4
+    fd = random_forest(rng, T, d, nf, kvmax=3000, bmax=200)
+    fd["base_score"] = np.float32(45.0)
+    kv, bs = random_curves(rng, S, H, kvmax=3000, bmax=200)
+    fast = np.arange(S) % 2 == 1
+    nfast = int(fast.sum())
+    bs[fast] = np.clip(rng.integers(20, 180, (nfast, 1)) + np.cumsum(rng.choice([-1, 1], (nfast, H)), axis=1),
+                       0, None).astype(np.int32)
+    freqs = synth.frequency_grid(F)
+    eng = rng.choice([1.0, 2.0, 4.0, 8.0], S).astype(np.float32)
+    dl, n, tbt, flags = random_checks(rng, S, H, kv)
+    idx, st = gpu_binary(fd, freqs, kv, bs, dl, n, tbt, flags, eng)
+    ips = oracle.forest_predict(fd, oracle.rows(freqs, bs, kv, eng, nf))
+    oi, os_ = oracle.select_binary(ips, dl, n, tbt, flags)
+    assert np.array_equal(idx, oi) and np.array_equal(st, os_), np.nonzero((idx != oi) | (st != os_))[0][:5]
+    assert len(set(st.tolist())) >= 2
+
+
 SCALED = [
     (0, dict()),
     (1, dict(n_scenarios=10)),
