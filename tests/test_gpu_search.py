@@ -91,13 +91,15 @@ def test_binary_search_random(gpu, S, F, H, T, d, nf, mono, seed):
     assert len(set(st.tolist())) >= 2
 
 
-def test_binary_search_at_reuse_sizes(gpu):
-    """A grid large enough for the column kernel with leaf reuse along each
-    lane's rows (4096 scenarios x 512 iterations); half of the scenarios have
-    a batch that changes at every iteration, which takes that kernel's
-    walk-every-row path.  Indices and statuses equal the oracle's."""
-    rng = np.random.default_rng(777)
-    S, F, H, T, d, nf = 4096, 5, 512, 20, 6, 4
+@pytest.mark.parametrize("S,H", [(4096, 512), (2048, 1000)])
+def test_binary_search_at_reuse_sizes(gpu, S, H):
+    """Grids large enough for the column kernel with leaf reuse along each
+    lane's rows (a whole and a ragged last wavefront of iterations); half of
+    the scenarios have a batch that changes at every iteration, which takes
+    that kernel's walk-every-row path.  Indices and statuses equal the
+    oracle's."""
+    rng = np.random.default_rng(777 + H)
+    F, T, d, nf = 5, 20, 6, 4
     fd = random_forest(rng, T, d, nf, kvmax=3000, bmax=200)
     fd["base_score"] = np.float32(45.0)
     kv, bs = random_curves(rng, S, H, kvmax=3000, bmax=200)
