@@ -278,6 +278,26 @@ def test_forest_random(gpu, T, d, nf, n):
     assert exact == n      # tree-order fp64 accumulation on both sides
 
 
+def test_forest_rows_at_an_offset(gpu):
+    """4-feature rows that start 4 bytes into their buffer (not 16-byte
+    aligned) through the LDS-staged row walks."""
+    import torch
+    api = _api()
+    rng = np.random.default_rng(4343)
+    fd = random_forest(rng, 37, 8, 4)
+    n = 3001
+    x = random_rows(rng, n, 4)
+    buf = torch.zeros(n * 4 + 1, dtype=torch.float32)
+    buf[1:] = torch.from_numpy(x.reshape(-1))
+    dev = buf.cuda()[1:].view(n, 4)
+    assert dev.data_ptr() % 16 == 4
+    f = api.Forest.from_dict(fd)
+    got = _np(f.tl_forest_predict(dev))
+    torch.cuda.synchronize()
+    exp = oracle.forest_predict(fd, x)
+    assert assert_ips_close(got, exp, "offset rows") == n
+
+
 def random_curves(rng, S, H, kvmax=5000, bmax=300):
     """Slowly varying KV / batch curves with jumps, like projections."""
     kv = np.clip(rng.integers(0, kvmax, (S, 1)) + np.cumsum(rng.integers(-12, 10, (S, H)), axis=1), 0, None)
