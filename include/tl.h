@@ -50,10 +50,10 @@ typedef enum tl_status {
     TL_EINVAL = 1,          /* invalid argument; nothing was enqueued          */
     TL_ENOMEM = 2,          /* device allocation failed                        */
     TL_EDEVICE = 3,         /* a HIP runtime call or kernel launch failed      */
-    TL_EUNSUPPORTED = 4     /* valid but beyond this build's limits            */
+    TL_EUNSUPPORTED = 4     /* valid but beyond the library's limits          */
 } tl_status;
 
-/* Limits of this build. */
+/* Limits of the library. */
 #define TL_MAX_HORIZON 8192         /* H: future iterations per scenario      */
 #define TL_MAX_BLOCK_TOKENS 65536   /* N: tokens per KV block                 */
 #define TL_MAX_FREQS 4096           /* F: candidate frequencies               */
