@@ -1,5 +1,12 @@
-"""Seeded random sweep of the model kernels against the oracle, through the
-C ABI: the grid kernel (random S, F up to 129, H up to 700), the LDS-staged
+"""Seeded random sweeps against the oracle, through the C ABI.
+
+Projection and admission: random scoreboards (1-119 scenarios, H up to
+3000, block sizes 1-100, 0-1000 requests per scenario, any queued
+fraction, sorted or unsorted arrivals, loose or binding KV and batch caps,
+malformed and lost entries), every third case as an admission what-if with
+a small random forest; curves, checkpoints, flags and decisions bit-exact.
+
+Models: the grid kernel (random S, F up to 129, H up to 700), the LDS-staged
 row walks (up to 20 000 rows, NaN features) and the column query at one
 frequency per scenario (the binary search's final probe; half of the cases
 at the sizes that take the leaf-reuse column kernel, half of the scenarios
@@ -10,7 +17,8 @@ import pytest
 
 import oracle
 from paper_2408_05235_amd import synth
-from test_gpu_parity import random_curves, random_forest, random_rows
+from test_gpu_admit import check_admit, random_candidates
+from test_gpu_parity import assert_projection_equal, gpu_project, random_boards, random_curves, random_forest, random_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -82,3 +90,29 @@ def test_random_sweep(gpu):
     for seed in range(N_CASES):
         what, bad = _case(seed)
         assert bad.size == 0, f"seed {seed} ({what}): {bad.size} outputs differ, first at {bad[:5].tolist()}"
+
+
+N_BOARD_CASES = 300
+
+
+def test_random_projection_and_admission_sweep(gpu):
+    for seed in range(N_BOARD_CASES):
+        rng = np.random.default_rng(50_000 + seed)
+        S, H = int(rng.integers(1, 120)), int(rng.integers(1, 3000))
+        N = int(rng.choice([1, 3, 7, 16, 64, 100]))
+        rmax = int(rng.choice([0, 5, 40, 300, 1000]))
+        qfrac = float(rng.random())
+        tight = rng.random() < 0.5
+        cap = rng.integers(max(1, N), N * 10 + 50, S).astype(np.int32) if tight else None
+        inp = random_boards(rng, S, H, N, rmax=rmax, qfrac=qfrac, unsorted=bool(rng.random() < 0.3), cap=cap)
+        where = f"seed {seed} S={S} H={H} N={N} rmax={rmax} q={qfrac:.2f} tight={tight}"
+        if seed % 3 == 2:
+            nf = int(rng.choice([3, 4]))
+            inp["tbt_slo_ns"] = rng.integers(5_000_000, 60_000_000, S).astype(np.uint64)
+            if nf == 4:
+                inp["engine_size"] = rng.choice([1.0, 2.0, 4.0, 8.0], S).astype(np.float32)
+            fd = random_forest(rng, int(rng.integers(0, 20)), int(rng.integers(0, 9)), nf, kvmax=4000, bmax=300)
+            fd["base_score"] = np.float32(60.0)
+            check_admit(inp, fd, 2000.0, random_candidates(rng, inp), "admission " + where)
+        else:
+            assert_projection_equal(gpu_project(inp), oracle.project(inp), where)
