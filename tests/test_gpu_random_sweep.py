@@ -6,6 +6,10 @@ fraction, sorted or unsorted arrivals, loose or binding KV and batch caps,
 malformed and lost entries), every third case as an admission what-if with
 a small random forest; curves, checkpoints, flags and decisions bit-exact.
 
+Selection: random IPS (scaled per case, special values, increasing in the
+frequency on half of the scenarios), deadlines, SLO budgets and flags over
+random shapes; index and status bit-exact.
+
 Models: the grid kernel (random S, F up to 129, H up to 700), the LDS-staged
 row walks (up to 20 000 rows, NaN features) and the column query at one
 frequency per scenario (the binary search's final probe; half of the cases
@@ -18,7 +22,8 @@ import pytest
 import oracle
 from paper_2408_05235_amd import synth
 from test_gpu_admit import check_admit, random_candidates
-from test_gpu_parity import assert_projection_equal, gpu_project, random_boards, random_curves, random_forest, random_rows
+from test_gpu_parity import (assert_projection_equal, gpu_project, gpu_select, random_boards, random_curves,
+                             random_forest, random_rows, random_selection)
 
 pytestmark = pytest.mark.gpu
 
@@ -116,3 +121,21 @@ def test_random_projection_and_admission_sweep(gpu):
             check_admit(inp, fd, 2000.0, random_candidates(rng, inp), "admission " + where)
         else:
             assert_projection_equal(gpu_project(inp), oracle.project(inp), where)
+
+
+N_SELECT_CASES = 300
+
+
+def test_random_selection_sweep(gpu):
+    for seed in range(N_SELECT_CASES):
+        rng = np.random.default_rng(90_000 + seed)
+        S, F, H = int(rng.integers(1, 80)), int(rng.integers(1, 130)), int(rng.integers(1, 1500))
+        ips, dl, n, tbt, flags = random_selection(rng, S, F, H)
+        ips *= np.float32(rng.uniform(0.2, 5.0))
+        mono = rng.random(S) < 0.5
+        ips[mono] = np.sort(ips[mono], axis=1)
+        fl = flags if rng.random() < 0.7 else None
+        gi, gs = gpu_select(ips, dl, n, tbt, fl)
+        oi, os_ = oracle.select(ips, dl, n, tbt, fl)
+        assert np.array_equal(gi, oi) and np.array_equal(gs.view(np.uint32), os_), \
+            f"seed {seed} S={S} F={F} H={H}: scenarios {np.nonzero((gi != oi) | (gs.view(np.uint32) != os_))[0][:5]}"
