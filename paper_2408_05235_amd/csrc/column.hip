@@ -227,19 +227,10 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
         if (o[r] >= 0) P.out[o[r]] = (float)acc[r];
 }
 
-// Whether (kv, batch) lies in a leaf box (kv_lo, kv_hi, batch_lo, batch_hi).
-__device__ __forceinline__ bool col_in_box(const float4& b, float kv, float bs) {
-    return (kv >= b.x) & (kv < b.y) & (bs >= b.z) & (bs < b.w);
-}
-
 // A leaf box read from LDS (byte address).
 __device__ __forceinline__ float4 lds_box(uint32_t addr) {
     const u32x4 w = *(lds_u32x4*)(uintptr_t)addr;
     return make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
-}
-
-__device__ __forceinline__ float4 col_box_meet(const float4& a, const float4& b) {
-    return make_float4(a.x > b.x ? a.x : b.x, a.y < b.y ? a.y : b.y, a.z > b.z ? a.z : b.z, a.w < b.w ? a.w : b.w);
 }
 
 // Leaf reuse along a lane's rows: a lane takes RPL consecutive iterations of
@@ -272,14 +263,14 @@ __device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayo
             walk<NF, NT>(tree, R.bytes, depth, xf, kv[0], bs[0], xe, k);
 #pragma unroll
             for (int t = 0; t < NT; ++t) leaf[t] = k[t];
-        } else if (!col_in_box(box, kv[r], bs[r])) {
+        } else if (!in_box(box, kv[r], bs[r])) {
             if (NT == 1) {
                 int32_t k[1];
                 walk<NF, 1>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
                 leaf[0] = k[0];
             } else {
-                const bool n0 = !col_in_box(lds_box(boxes0 + 16u * leaf[0]), kv[r], bs[r]);
-                const bool n1 = !col_in_box(lds_box(boxes1 + 16u * leaf[NT - 1]), kv[r], bs[r]);
+                const bool n0 = !in_box(lds_box(boxes0 + 16u * leaf[0]), kv[r], bs[r]);
+                const bool n1 = !in_box(lds_box(boxes1 + 16u * leaf[NT - 1]), kv[r], bs[r]);
                 if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
                     int32_t k[2];
                     walk<NF, 2>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
@@ -306,7 +297,7 @@ __device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayo
             box = lds_box(boxes0 + 16u * leaf[0]);
             if (NT == 2) {
                 v[NT - 1] = (double)*(lds_f32*)(uintptr_t)(vals1 + 4u * leaf[NT - 1]);
-                box = col_box_meet(box, lds_box(boxes1 + 16u * leaf[NT - 1]));
+                box = box_meet(box, lds_box(boxes1 + 16u * leaf[NT - 1]));
             }
         }
 #pragma unroll

@@ -208,11 +208,6 @@ __global__ __launch_bounds__(kCostThreads) void grid_cost_kernel(const float* __
 
 // ---------------------------------------------------------------- LDS-staged
 
-// Whether (kv, batch) lies in a leaf box (kv_lo, kv_hi, batch_lo, batch_hi).
-__device__ __forceinline__ bool in_box(const float4& b, float kv, float bs) {
-    return (kv >= b.x) & (kv < b.y) & (bs >= b.z) & (bs < b.w);
-}
-
 constexpr int kLdsWaves = TL_LDS_WAVES;  // wavefronts per workgroup
 constexpr int kLdsThreads = kLdsWaves * kWave;
 #ifndef TL_STAGE_REGS
@@ -235,10 +230,6 @@ __device__ __forceinline__ float to_sgpr(float x) {
 #define TL_ROW_GROUP 4
 #endif
 constexpr int kRowGroup = TL_ROW_GROUP;   // rows whose (KV, batch) hull is tested as one
-
-__device__ __forceinline__ float4 box_meet(const float4& a, const float4& b) {
-    return make_float4(a.x > b.x ? a.x : b.x, a.y < b.y ? a.y : b.y, a.z > b.z ? a.z : b.z, a.w < b.w ? a.w : b.w);
-}
 
 // Adds the leaves of NT (1 or 2) consecutive staged trees (records R.bytes
 // apart, the first at `tree`) to the J row sums of a wavefront, in tree

@@ -1,4 +1,5 @@
-// Node walks over tree records staged in LDS, shared by the forest kernels.
+// Node walks over tree records staged in LDS and leaf-box tests, shared by
+// the forest kernels.
 // A record node is (threshold, sel1, sel2, sel3): the byte-permute selectors
 // that pick the tested feature out of the row (see node_feature); internal
 // nodes sit in heap order 16 bytes apart from the record's start.
@@ -20,6 +21,16 @@ __device__ __forceinline__ float node_feature(const uint4& nd, float xf, float k
     const uint32_t x23 = NF == 4 ? __builtin_amdgcn_perm(__float_as_uint(xe), __float_as_uint(bs), nd.z)
                                  : __float_as_uint(bs);
     return __uint_as_float(__builtin_amdgcn_perm(x23, x01, nd.w));
+}
+
+// Whether (kv, batch) lies in a leaf box (kv_lo, kv_hi, batch_lo, batch_hi).
+__device__ __forceinline__ bool in_box(const float4& b, float kv, float bs) {
+    return (kv >= b.x) & (kv < b.y) & (bs >= b.z) & (bs < b.w);
+}
+
+// The intersection of two leaf boxes.
+__device__ __forceinline__ float4 box_meet(const float4& a, const float4& b) {
+    return make_float4(a.x > b.x ? a.x : b.x, a.y < b.y ? a.y : b.y, a.z > b.z ? a.z : b.z, a.w < b.w ? a.w : b.w);
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
