@@ -439,6 +439,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="c3")
+    ap.add_argument("--lattice-max-gib", type=float, default=24,
+                    help="largest model table the lattice mode builds (larger ones are reported as skipped)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-procs", type=int, default=min(16, len(os.sched_getaffinity(0))),
                     help="processes for the sharded oracle run (0 or 1: single thread only)")
@@ -554,7 +556,8 @@ def main():
     out["adjust_lengths"] = adjust_lengths_bench(inp, dev_in, args.steps, copy_gbs)
     out["materialized_rows"] = materialized_rows_bench(inp, dev_in, forest, ctl, args.steps, copy_gbs)
     out["lattice"] = lattice_bench(inp, cfg, ctl, args.steps, args.warmup,
-                                   lambda lat: admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup, lat))
+                                   lambda lat: admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup, lat),
+                                   max_gib=args.lattice_max_gib)
     out["binary_search"] = binary_search_bench(ctl, args.steps, args.warmup)
     out["admission"] = admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup)
     if args.copy_calibration_mib:
