@@ -83,16 +83,22 @@ __device__ __forceinline__ void inflight_jumps(int32_t c, int32_t e, int32_t H, 
     }
 }
 
+// BD_LDS: the batch difference array lives in LDS beside the KV curve, as a
+// batch cap needs (the admission loop reads its running sums).  Without a
+// cap it is only added to and finally prefix-summed, so it accumulates with
+// atomics in the scenario's own batch output row instead: half the LDS, twice
+// the scenario wavefronts per CU.
+template <bool BD_LDS>
 __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     extern __shared__ int32_t lds[];
     const int32_t H = P.H;
     const int32_t N = P.N;
     const DivU32 divN{(uint32_t)N, P.div_m, P.div_l};
-    int32_t* KV = lds;            // comb diff, comb prefix, + jumps, then KV values
-    int32_t* BI = lds + H;        // batch difference array
     const int lane = lane_id();
     const int64_t s = blockIdx.x;
     int32_t* outB = P.batch + s * H;
+    int32_t* KV = lds;                      // comb diff, comb prefix, + jumps, then KV values
+    int32_t* BI = BD_LDS ? lds + H : outB;  // batch difference array
     int32_t* outKV = P.kv + s * H;
     uint64_t* outDL = P.deadline_at + s * H;
 
@@ -205,7 +211,8 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     kv0 = wave_sum(kv0);
     n_end = wave_max(n_end);
     if (lane == 0) {
-        BI[0] += n_in;
+        if (BD_LDS) BI[0] += n_in;
+        else atomicAdd(&BI[0], n_in);
         KV[0] += kv0;
     }
     __syncthreads();
@@ -229,7 +236,7 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
         }
     }
     last_over = wave_max(last_over);
-    const bool has_bcap = P.batch_cap != nullptr;
+    const bool has_bcap = BD_LDS && P.batch_cap != nullptr;   // (the host takes BD_LDS with a cap)
     const int32_t bcap = has_bcap ? P.batch_cap[s] : 0;
     if (last_over >= 0 || (has_bcap && n_in > bcap)) fl |= TL_FLAG_OVERCOMMIT;
 
@@ -409,8 +416,13 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 if (t < lim) KV[t] += (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN);
             }
             if (lane == 0) {
-                BD[j] += 1;
-                if (e < H) BD[e] -= 1;
+                if (BD_LDS) {
+                    BD[j] += 1;
+                    if (e < H) BD[e] -= 1;
+                } else {
+                    atomicAdd(&BD[j], 1);
+                    if (e < H) atomicAdd(&BD[e], -1);
+                }
                 if (e <= H && !h_lost && h_dl != kNoDeadline)
                     atomicMin((unsigned long long*)&outDL[e - 1], (unsigned long long)h_dl);
             }
@@ -423,7 +435,7 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     __syncthreads();
 
     // outputs: curves (batch = prefix sum of BD), scalars
-    {
+    if (BD_LDS) {
         int32_t carry_b = 0;
         for (int32_t t0 = 0; t0 < H; t0 += kWave) {
             const int32_t t = t0 + lane;
@@ -434,6 +446,29 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
             const int32_t k = KV[t];
             outB[t] = b;
             outKV[t] = k;
+        }
+    } else {
+        // the differences were added at L2 by atomics: read them there,
+        // eight 64-iteration chunks in flight at a time, then scan
+        constexpr int kChunks = 8;
+        int32_t carry_b = 0;
+        for (int32_t g0 = 0; g0 < H; g0 += kChunks * kWave) {
+            int32_t d[kChunks];
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) {
+                const int32_t t = g0 + c * kWave + lane;
+                d[c] = t < H ? __hip_atomic_load(&BD[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+            }
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) {
+                const int32_t t = g0 + c * kWave + lane;
+                const int32_t b = wave_incl_scan(d[c]) + carry_b;
+                carry_b = __builtin_amdgcn_readlane(b, kWave - 1);
+                if (t < H) {
+                    outB[t] = b;
+                    outKV[t] = KV[t];
+                }
+            }
         }
     }
     if (lane == 0) {
@@ -510,13 +545,20 @@ hipError_t launch_adjust(const AdjustParams& p, hipStream_t stream) {
 }
 
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream) {
-    const size_t lds = (size_t)2 * p.H * sizeof(int32_t);
+    // The batch differences go to global memory where occupancy pays: no
+    // batch cap and long FIFO loops (on average 1024 or more requests per
+    // scenario); otherwise the LDS array is faster.
+    const bool bd_lds = p.batch_cap != nullptr || p.n_requests < (int64_t)1024 * p.n_scenarios;
+    const size_t lds = (size_t)(bd_lds ? 2 : 1) * p.H * sizeof(int32_t);
+    const void* kern = bd_lds ? (const void*)project_kernel<true> : (const void*)project_kernel<false>;
     if (lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)project_kernel,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(project_kernel, dim3((unsigned)p.n_scenarios), dim3(64), lds, stream, p);
+    if (bd_lds)
+        hipLaunchKernelGGL(project_kernel<true>, dim3((unsigned)p.n_scenarios), dim3(64), lds, stream, p);
+    else
+        hipLaunchKernelGGL(project_kernel<false>, dim3((unsigned)p.n_scenarios), dim3(64), lds, stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !p.rows) return e;
     const int64_t blocks = p.n_scenarios * ((p.H + kRowsThreads - 1) / kRowsThreads);

@@ -134,6 +134,19 @@ def random_boards(rng, S, H, N, rmax=40, qfrac=0.3, bad=0.03, lost=0.02, unsorte
                 batch_cap=rng.integers(1, 30, S).astype(np.int32) if rng.random() < 0.5 else None)
 
 
+@pytest.mark.parametrize("H,N,seed,rmax,qfrac", [(2048, 16, 20, 4000, 0.7), (700, 5, 21, 2500, 0.95),
+                                                 (4096, 64, 22, 3000, 0.5)])
+def test_project_many_requests(gpu, H, N, seed, rmax, qfrac):
+    """Boards with thousands of requests per scenario and no batch cap: the
+    projection keeps its batch differences in global memory (long FIFO
+    loops); everything still equals the oracle."""
+    rng = np.random.default_rng(seed)
+    inp = random_boards(rng, 40, H, N, rmax=rmax, qfrac=qfrac, unsorted=(seed % 2 == 1))
+    inp["batch_cap"] = None
+    assert int(inp["req_offset"][-1]) >= 1024 * 40
+    assert_projection_equal(gpu_project(inp), oracle.project(inp), f"H={H} N={N} rmax={rmax}")
+
+
 @pytest.mark.parametrize("H,N,seed", [(1, 16, 0), (7, 1, 1), (64, 16, 2), (100, 3, 3), (513, 16, 4),
                                       (1000, 64, 5), (257, 100, 6), (2048, 16, 7), (130, 7, 8)])
 def test_project_random_boards(gpu, H, N, seed):

@@ -1,7 +1,7 @@
 """Seeded random sweeps against the oracle, through the C ABI.
 
 Projection and admission: random scoreboards (1-119 scenarios, H up to
-3000, block sizes 1-100, 0-1000 requests per scenario, any queued
+3000, block sizes 1-100, 0-3000 requests per scenario, any queued
 fraction, sorted or unsorted arrivals, loose or binding KV and batch caps,
 malformed and lost entries), every third case as an admission what-if with
 a small random forest; curves, checkpoints, flags and decisions bit-exact.
@@ -105,7 +105,7 @@ def test_random_projection_and_admission_sweep(gpu):
         rng = np.random.default_rng(50_000 + seed)
         S, H = int(rng.integers(1, 120)), int(rng.integers(1, 3000))
         N = int(rng.choice([1, 3, 7, 16, 64, 100]))
-        rmax = int(rng.choice([0, 5, 40, 300, 1000]))
+        rmax = int(rng.choice([0, 5, 40, 300, 1000, 3000]))   # 3000: the projection's global-memory batch array
         qfrac = float(rng.random())
         tight = rng.random() < 0.5
         cap = rng.integers(max(1, N), N * 10 + 50, S).astype(np.int32) if tight else None
