@@ -376,17 +376,22 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 bool ok = !has_bcap || run < bcap;
                 int32_t t_bad = -1;
                 if (ok) {
+                    // 4 x 64 iterations per round (their LDS reads in flight
+                    // together); the earliest overflowing iteration wins
                     const int32_t lim = (int32_t)min((int64_t)j + h_len, (int64_t)H);
-                    for (int32_t t0 = j; t0 < lim; t0 += kWave) {
-                        const int32_t t = t0 + lane;
-                        bool badt = false;
-                        if (t < lim)
-                            badt = KV[t] + (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN) > cap;
-                        const uint64_t m = __ballot(badt);
-                        if (m) {
-                            t_bad = t0 + __ffsll((unsigned long long)m) - 1;
-                            break;
+                    for (int32_t t0 = j; t0 < lim && t_bad < 0; t0 += 4 * kWave) {
+                        uint64_t m[4];
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            const int32_t t = t0 + k * kWave + lane;
+                            bool badt = false;
+                            if (t < lim)
+                                badt = KV[t] + (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN) > cap;
+                            m[k] = __ballot(badt);
                         }
+#pragma unroll
+                        for (int k = 3; k >= 0; --k)
+                            if (m[k]) t_bad = t0 + k * kWave + __ffsll((unsigned long long)m[k]) - 1;
                     }
                     ok = t_bad < 0;
                 }
@@ -411,6 +416,7 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
             if (!admitted) break;
             const int64_t e = (int64_t)j + h_len;
             const int32_t lim = (int32_t)min(e, (int64_t)H);
+#pragma unroll 4
             for (int32_t t0 = j; t0 < lim; t0 += kWave) {
                 const int32_t t = t0 + lane;
                 if (t < lim) KV[t] += (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN);
