@@ -396,6 +396,30 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                     ok = t_bad < 0;
                 }
                 if (ok) { admitted = true; break; }
+                if (has_bcap && run >= bcap) {
+                    // The batch is full: the next start to try is the first
+                    // later iteration with a free slot, found 64 iterations
+                    // at a time from the batch differences (what stepping
+                    // one iteration at a time reaches).
+                    int32_t base = j, r = run, found = -1;
+                    while (base + 1 < H) {
+                        const int32_t t = base + 1 + lane;
+                        const int32_t pre = wave_incl_scan(t < H ? BD[t] : 0) + r;   // batch size at t
+                        const uint64_t m = __ballot(t < H && pre < bcap);
+                        if (m) {
+                            const int l = __ffsll((unsigned long long)m) - 1;
+                            found = base + 1 + l;
+                            r = __builtin_amdgcn_readlane(pre, l);
+                            break;
+                        }
+                        r = __builtin_amdgcn_readlane(pre, kWave - 1);
+                        base += kWave;
+                    }
+                    if (found < 0) break;
+                    run = r;
+                    j = found;
+                    continue;
+                }
                 // Next start to try.  If iteration t_bad overflowed, every
                 // start j2 in (j, t_bad] whose own contribution there,
                 // ceil((c + t_bad - j2) / N), exceeds room = cap - KV[t_bad]
