@@ -221,6 +221,9 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     // a difference array: admissions add their +1 / -1 to it and the output
     // takes its prefix sum.
     const int32_t cap = P.kv_cap[s];
+    // bound (pass A) is at least the KV of every iteration: when it fits the
+    // capacity, no admission check can fail and the checks are skipped
+    const bool kv_fits = cap >= 0 && bound <= (uint64_t)cap;
     int32_t last_over = -1;
     {
         int32_t carry_kv = 0;
@@ -312,10 +315,11 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 }
                 const int32_t a_first = __builtin_amdgcn_readlane(a, __ffsll((unsigned long long)take) - 1);
                 bool bad = false;
-                for (int32_t t0 = a_first; t0 < r_end; t0 += kWave) {
-                    const int32_t t = t0 + lane;
-                    if (t < r_end && KV[t] > cap) bad = true;
-                }
+                if (!kv_fits)
+                    for (int32_t t0 = a_first; t0 < r_end; t0 += kWave) {
+                        const int32_t t = t0 + lane;
+                        if (t < r_end && KV[t] > cap) bad = true;
+                    }
                 const bool fits = __ballot(bad) == 0;
                 if (!fits) {
                     // take the batch's contributions out again
@@ -378,7 +382,7 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 if (ok) {
                     // 4 x 64 iterations per round (their LDS reads in flight
                     // together); the earliest overflowing iteration wins
-                    const int32_t lim = (int32_t)min((int64_t)j + h_len, (int64_t)H);
+                    const int32_t lim = kv_fits ? j : (int32_t)min((int64_t)j + h_len, (int64_t)H);
                     for (int32_t t0 = j; t0 < lim && t_bad < 0; t0 += 4 * kWave) {
                         uint64_t m[4];
 #pragma unroll

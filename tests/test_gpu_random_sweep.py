@@ -2,9 +2,10 @@
 
 Projection and admission: random scoreboards (1-119 scenarios, H up to
 3000, block sizes 1-100, 0-3000 requests per scenario, any queued
-fraction, sorted or unsorted arrivals, loose or binding KV and batch caps,
-malformed and lost entries), every third case as an admission what-if with
-a small random forest; curves, checkpoints, flags and decisions bit-exact.
+fraction, sorted or unsorted arrivals, binding, loose or unreachable KV
+caps, batch caps or none, malformed and lost entries), every third case as
+an admission what-if with a small random forest; curves, checkpoints, flags
+and decisions bit-exact.
 
 Selection: random IPS (scaled per case, special values, increasing in the
 frequency on half of the scenarios), deadlines, SLO budgets and flags over
@@ -107,8 +108,10 @@ def test_random_projection_and_admission_sweep(gpu):
         N = int(rng.choice([1, 3, 7, 16, 64, 100]))
         rmax = int(rng.choice([0, 5, 40, 300, 1000, 3000]))   # 3000: the projection's global-memory batch array
         qfrac = float(rng.random())
-        tight = rng.random() < 0.5
-        cap = rng.integers(max(1, N), N * 10 + 50, S).astype(np.int32) if tight else None
+        u = rng.random()
+        tight = u < 0.4
+        cap = (rng.integers(max(1, N), N * 10 + 50, S).astype(np.int32) if tight
+               else np.full(S, 1 << 30, np.int32) if u > 0.75 else None)   # binding, never binding, generated
         inp = random_boards(rng, S, H, N, rmax=rmax, qfrac=qfrac, unsorted=bool(rng.random() < 0.3), cap=cap)
         where = f"seed {seed} S={S} H={H} N={N} rmax={rmax} q={qfrac:.2f} tight={tight}"
         if seed % 3 == 2:
