@@ -39,3 +39,23 @@ def forest(g):
                 feature=np.array(f["feature"], np.uint8).reshape(f["n_trees"], -1),
                 threshold=np.array(f["threshold"], np.float32).reshape(f["n_trees"], -1),
                 leaf=np.array(f["leaf"], np.float32).reshape(f["n_trees"], -1))
+
+
+def scoreboard_multi(g, sigma_ns, lost=None):
+    """Several scenarios from one fixture: CSR offsets, per-scenario
+    capacities and engine sizes; deadlines sigma_s * r_i per request."""
+    off = np.array(g["req_offset"], np.int64)
+    S = off.size - 1
+    rem = np.array(g["remaining"], np.int64)
+    sig = np.repeat(np.array(sigma_ns, np.uint64), np.diff(off))
+    return dict(
+        n_scenarios=S, horizon=g["horizon"], block_tokens=g["block_tokens"], req_offset=off,
+        prompt=np.array(g["prompt"], np.int32), generated=np.array(g["generated"], np.int32),
+        remaining=rem.astype(np.int32), arrival=np.array(g["arrival"], np.int32),
+        deadline_ns=(rem.astype(np.uint64) * sig).astype(np.uint64),
+        lost=None if lost is None else np.array(lost, np.uint8),
+        kv_capacity=np.array(g.get("kv_capacity", [1 << 30] * S), np.int32),
+        batch_cap=None,
+        engine_size=np.array(g["engine_size"], np.float32),
+        tbt_slo_ns=np.array(sigma_ns, np.uint64),
+    )

@@ -52,6 +52,40 @@ def test_golden_selection():
         assert (int(idx[0]), int(stt[0])) == (case["freq_idx"], case["status"]), case
 
 
+def test_golden_engine_size_two_scenarios():
+    """Four-feature rows of several scenarios: the row (s, f, j) must carry
+    scenario s's own curves and engine size at frequency f, in [S][F][H]
+    order, through prediction and selection (hand-computed)."""
+    g = goldens.load("e2e_engine_size_two_scenarios.json")
+    forest = goldens.forest(g)
+    freqs = np.array(g["freqs_mhz"], np.float32)
+    for case in g["cases"]:
+        inp = goldens.scoreboard_multi(g, case["sigma_ns"], lost=case["lost"])
+        proj = oracle.project(inp)
+        assert proj["batch"].tolist() == g["expect_batch"]
+        assert proj["kv"].tolist() == g["expect_kv"]
+        assert proj["n_iters"].tolist() == g["expect_n_iters"]
+        x = oracle.rows(freqs, proj["batch"], proj["kv"], inp["engine_size"], 4)
+        assert x.tolist() == g["expect_rows"]
+        ips = oracle.forest_predict(forest, x)
+        assert ips.tolist() == g["expect_ips"]
+        idx, stt = oracle.select(ips, proj["deadline_at"], proj["n_iters"], inp["tbt_slo_ns"],
+                                 proj["flags"])
+        assert idx.tolist() == case["freq_idx"] and stt.tolist() == case["status"], case["note"]
+        full = oracle.end_to_end(dict(inp, freqs_mhz=freqs, n_features=4, forest=forest))
+        assert full["ips"].tolist() == g["expect_ips"]
+        assert full["freq_idx"].tolist() == case["freq_idx"], case["note"]
+
+
+def test_rows_three_features_several_scenarios():
+    """Without the engine-size column the rows keep the same [S][F][H]
+    order (the same hand-computed curves as the four-feature fixture)."""
+    g = goldens.load("e2e_engine_size_two_scenarios.json")
+    proj = oracle.project(goldens.scoreboard_multi(g, [1, 1]))
+    x = oracle.rows(np.array(g["freqs_mhz"], np.float32), proj["batch"], proj["kv"], None, 3)
+    assert x.tolist() == [[[r[:3] for r in rf] for rf in rs] for rs in g["expect_rows"]]
+
+
 # ------------------------------------------------ engine simulation (Eq. 1, 2)
 
 def simulate_engine(H, N, reqs):
@@ -582,6 +616,25 @@ def test_golden_admission():
             assert out["kv"][0].tolist() == ex["kv"]
             assert out["batch"][0].tolist() == ex["batch"]
             assert out["ips"][0].tolist() == ex["ips"]
+
+
+def test_golden_admission_engine_size_two_scenarios():
+    """Admission on several scenarios with a four-feature model: check 2
+    queries M with each scenario's own engine size (hand-computed)."""
+    g = goldens.load("admit_engine_size_two_scenarios.json")
+    forest = goldens.forest(g)
+    for case in g["cases"]:
+        inp = goldens.scoreboard_multi(dict(g, kv_capacity=case["kv_capacity"]), case["sigma_ns"])
+        inp["forest"] = forest
+        d = case["cand_deadline"]
+        out = oracle.admit(inp, g["cand_prompt"], g["cand_len"],
+                           None if d is None else np.array(d, np.uint64), g["max_freq_mhz"])
+        assert out["decision"].tolist() == case["decision"], case["note"]
+        for s, dec in enumerate(case["decision"]):
+            assert out["batch"][s].tolist() == g["expect_batch"][s]
+            assert out["kv"][s].tolist() == g["expect_kv"][s]
+            if dec != oracle.QUEUE_CAPACITY:
+                assert out["ips"][s].tolist() == g["expect_ips"][s]
 
 
 def _random_admission(rng, queued):
