@@ -232,9 +232,15 @@ tl_status tl_forest_predict(const tl_forest* forest, const float* rows, int64_t 
  * features in the order (frequency, KV, batch[, engine size]).
  * 1 <= F <= TL_MAX_FREQS, 1 <= H <= TL_MAX_HORIZON.
  * Work is ordered by an estimate of its cost (results do not depend on the
- * order); the ordering takes about 16 bytes per (scenario, 32-iteration
- * chunk) of device scratch from the stream-ordered allocator, released on
- * the stream when the call's work is done.  TL_ENOMEM if that fails.
+ * order).  The ordering needs 16 bytes per (scenario, 32-iteration chunk)
+ * plus a radix sort's temporary storage of device scratch, which the forest
+ * handle owns: it is allocated
+ * on the first call, kept, and replaced only when a larger grid comes, so
+ * repeated calls of one size allocate nothing.  If that allocation fails the
+ * call runs without the ordering (same results).  Calls with one forest
+ * share its scratch: a call on another stream than the previous one first
+ * waits (on the device) for the previous call's work.  The forest's device
+ * must be the current device.
  * ---------------------------------------------------------------------- */
 tl_status tl_forest_predict_grid(const tl_forest* forest, int64_t n_scenarios, int32_t n_freqs,
                                  int32_t horizon, const float* freqs_mhz, const int32_t* kv,

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -22,6 +23,16 @@ struct tl_forest {
     void* box_mem;
     void* records_mem;
     void* cuts_mem;   // [kMaxCuts] KV cuts, then [kMaxCuts] batch cuts
+    // Work-order scratch of the grid kernel, on the forest's device: kept
+    // from call to call and only replaced by a larger one when a larger grid
+    // comes.  ws_done is recorded on the stream of the last call that used
+    // it; a call on another stream waits for it first.
+    mutable std::mutex ws_mutex;
+    mutable void* ws = nullptr;
+    mutable size_t ws_bytes = 0;
+    mutable hipEvent_t ws_done = nullptr;
+    mutable hipStream_t ws_stream = nullptr;
+    mutable bool ws_used = false;
 };
 
 struct tl_lattice {
@@ -177,10 +188,12 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     if (!f) return fail(TL_ENOMEM, "tl_forest_create: host allocation failed");
     hipError_t e = hipGetDevice(&f->device);
     if (e != hipSuccess) { delete f; return from_hip(e, "tl_forest_create: hipGetDevice"); }
+    e = hipEventCreateWithFlags(&f->ws_done, hipEventDisableTiming);
+    if (e != hipSuccess) { delete f; return from_hip(e, "tl_forest_create: hipEventCreate"); }
     e = hipMalloc(&f->nodes_mem, nodes.size() * sizeof(uint2));
-    if (e != hipSuccess) { delete f; return from_hip(e, "tl_forest_create: hipMalloc(nodes)"); }
+    if (e != hipSuccess) { (void)hipEventDestroy(f->ws_done); delete f; return from_hip(e, "tl_forest_create: hipMalloc(nodes)"); }
     e = hipMalloc(&f->leaves_mem, leaves.size() * sizeof(float));
-    if (e != hipSuccess) { (void)hipFree(f->nodes_mem); delete f; return from_hip(e, "tl_forest_create: hipMalloc(leaves)"); }
+    if (e != hipSuccess) { (void)hipFree(f->nodes_mem); (void)hipEventDestroy(f->ws_done); delete f; return from_hip(e, "tl_forest_create: hipMalloc(leaves)"); }
     f->box_mem = nullptr;
     f->records_mem = nullptr;
     f->cuts_mem = nullptr;
@@ -194,6 +207,7 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
         if (f->box_mem) (void)hipFree(f->box_mem);
         if (f->records_mem) (void)hipFree(f->records_mem);
         if (f->cuts_mem) (void)hipFree(f->cuts_mem);
+        (void)hipEventDestroy(f->ws_done);
         delete f;
         return from_hip(e, "tl_forest_create: hipMalloc");
     }
@@ -216,6 +230,7 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
         if (f->box_mem) (void)hipFree(f->box_mem);
         if (f->records_mem) (void)hipFree(f->records_mem);
         if (f->cuts_mem) (void)hipFree(f->cuts_mem);
+        (void)hipEventDestroy(f->ws_done);
         delete f;
         return from_hip(e, "tl_forest_create: hipMemcpy");
     }
@@ -246,6 +261,8 @@ void tl_forest_destroy(tl_forest* f) {
     if (f->box_mem) (void)hipFree(f->box_mem);
     if (f->records_mem) (void)hipFree(f->records_mem);
     if (f->cuts_mem) (void)hipFree(f->cuts_mem);
+    if (f->ws) (void)hipFree(f->ws);
+    (void)hipEventDestroy(f->ws_done);
     (void)hipSetDevice(cur);
     delete f;
 }
@@ -253,6 +270,49 @@ void tl_forest_destroy(tl_forest* f) {
 }  // extern "C"
 
 namespace {
+
+// The grid kernel with the forest's cached work-order workspace.  In the
+// steady state nothing is allocated; a larger grid than any before replaces
+// the workspace (after the last call that used it is done).  Without a
+// workspace (allocation failed) the kernel runs without the order, which
+// changes only its speed.
+hipError_t grid_with_workspace(const tl_forest* f, const tl::GridParams& g, hipStream_t st) {
+    size_t need = 0;
+    hipError_t e = tl::grid_order_bytes(f->dev, g, &need);
+    if (e != hipSuccess) return e;
+    if (need == 0) return tl::launch_forest_grid(f->dev, g, nullptr, 0, st);
+    std::lock_guard<std::mutex> lock(f->ws_mutex);
+    if (need > f->ws_bytes) {
+        if (f->ws) {
+            if (f->ws_used) {
+                e = hipEventSynchronize(f->ws_done);
+                if (e != hipSuccess) return e;
+            }
+            (void)hipFree(f->ws);
+            f->ws = nullptr;
+            f->ws_bytes = 0;
+            f->ws_used = false;
+        }
+        if (hipMalloc(&f->ws, need) == hipSuccess) {
+            f->ws_bytes = need;
+        } else {
+            f->ws = nullptr;
+            (void)hipGetLastError();   // clear the allocation error before the launches check theirs
+        }
+    }
+    if (!f->ws) return tl::launch_forest_grid(f->dev, g, nullptr, 0, st);
+    if (f->ws_used && f->ws_stream != st) {
+        e = hipStreamWaitEvent(st, f->ws_done, 0);
+        if (e != hipSuccess) return e;
+    }
+    e = tl::launch_forest_grid(f->dev, g, f->ws, f->ws_bytes, st);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(f->ws_done, st);
+    if (e != hipSuccess) return e;
+    f->ws_stream = st;
+    f->ws_used = true;
+    return hipSuccess;
+}
 
 // Host checks of a projection request and its translation to kernel
 // parameters; `who` prefixes messages.  Rows are only looked at when
@@ -421,6 +481,10 @@ tl_status tl_forest_predict_grid(const tl_forest* f, int64_t n_scenarios, int32_
     if (n_scenarios > 0 && f->dev.n_features == 4 && !engine_size)
         return fail(TL_EINVAL, "tl_forest_predict_grid: a 4-feature forest needs engine_size");
     if (n_scenarios == 0) return ok();
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur != f->device)
+        return fail(TL_EINVAL, "tl_forest_predict_grid: the forest lives on device %d, the current device is %d",
+                    f->device, cur);
     tl::GridParams g{};
     g.S = n_scenarios;
     g.F = n_freqs;
@@ -430,7 +494,7 @@ tl_status tl_forest_predict_grid(const tl_forest* f, int64_t n_scenarios, int32_
     g.batch = batch;
     g.engine = f->dev.n_features == 4 ? engine_size : nullptr;
     g.out = out;
-    return from_hip(tl::launch_forest_grid(f->dev, g, (hipStream_t)stream), "tl_forest_predict_grid: launch");
+    return from_hip(grid_with_workspace(f, g, (hipStream_t)stream), "tl_forest_predict_grid: launch");
 }
 
 tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
@@ -537,7 +601,7 @@ tl_status tl_lattice_create(const tl_forest* f, int32_t n_freqs, const float* fr
                 g.batch = batch;
                 g.engine = nf == 4 ? eng : nullptr;
                 g.out = grid_out;
-                e = tl::launch_forest_grid(f->dev, g, st);
+                e = grid_with_workspace(f, g, st);
             }
             if (e == hipSuccess)
                 e = tl::launch_lattice_transpose(grid_out, (float*)L.table, (int64_t)s0, cnt, n_freqs, st);

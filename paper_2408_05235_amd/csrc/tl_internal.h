@@ -220,7 +220,14 @@ hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
 hipError_t launch_adjust(const AdjustParams& p, hipStream_t stream);
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,
                               hipStream_t stream);
-hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, hipStream_t stream);
+// Scratch bytes the grid kernel's work order needs for this grid (0 when no
+// order applies: small grids, deep trees, forests without cuts).
+hipError_t grid_order_bytes(const ForestDev& f, const GridParams& g, size_t* bytes);
+// ws (nullable): device workspace of ws_bytes for the work order; the order
+// is computed when ws_bytes >= grid_order_bytes, otherwise items keep their
+// natural numbering (same results).  Nothing is allocated.
+hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
 hipError_t launch_select(const SelectParams& p, hipStream_t stream);
 hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream);
 // The same kernel on arbitrary rows [n_rows][n_features] (3 or 4 features,
