@@ -86,20 +86,23 @@ def _host_info():
     return dict(cpu_model=model, nproc=os.cpu_count(), affinity=len(os.sched_getaffinity(0)))
 
 
-def _oracle_scenarios(sub_inputs, budget_s):
+def _oracle_scenarios(sub_inputs, budget_s, keep=False):
     """Run the oracle on whole scenarios, one after another, until the budget
-    is spent; returns (scenarios done, rows done, seconds)."""
+    is spent; returns (scenarios done, rows done, seconds, results) where
+    results (with `keep`) holds each scenario's IPS, index and status."""
     import oracle
-    done, rows, t_used = 0, 0, 0.0
+    done, rows, t_used, kept = 0, 0, 0.0, []
     for sub in sub_inputs:
         t0 = time.perf_counter()
-        oracle.end_to_end(sub)
+        r = oracle.end_to_end(sub)
         t_used += time.perf_counter() - t0
         done += 1
         rows += sub["n_freqs"] * sub["horizon"]
+        if keep:
+            kept.append(dict(ips=r["ips"][0], freq_idx=int(r["freq_idx"][0]), status=int(r["status"][0])))
         if t_used >= budget_s:
             break
-    return done, rows, t_used
+    return done, rows, t_used, kept
 
 
 def cpu_baseline(inp, budget_s=12.0, max_scen=64, procs=0):
@@ -111,22 +114,24 @@ def cpu_baseline(inp, budget_s=12.0, max_scen=64, procs=0):
     S = inp["n_scenarios"]
     order = list(dict.fromkeys([0, S - 1] + list(np.random.default_rng(0).permutation(S))))
     done, rows, t_used = 0, 0, 0.0
-    F, H = inp["n_freqs"], inp["horizon"]
+    results = {}
     for s in order[:max_scen]:
-        d, r, t = _oracle_scenarios([synth.subset(inp, [s])], budget_s)
+        d, r, t, kept = _oracle_scenarios([synth.subset(inp, [s])], budget_s, keep=True)
         done, rows, t_used = done + d, rows + r, t_used + t
+        results[int(s)] = kept[0]
         if t_used >= budget_s:
             break
     out = dict(value=rows / t_used, unit="rows/s", cores=1, kind="oracle",
                sample=f"{done} of {S} scenarios (all stages, single thread), {t_used:.1f} s",
                scenarios_per_s=done / t_used, **_host_info())
+    out["_results"] = results
     if procs > 1 and S >= 2 * procs:
         import multiprocessing as mp
         per = max(2, (max_scen * 2) // procs)
         jobs = [[synth.subset(inp, [s]) for s in order[w::procs][:per]] for w in range(procs)]
         t0 = time.perf_counter()
         with mp.get_context("spawn").Pool(procs) as pool:
-            res = pool.starmap(_oracle_scenarios, [(j, budget_s) for j in jobs])
+            res = pool.starmap(_oracle_scenarios, [(j, budget_s, False) for j in jobs])
         wall = time.perf_counter() - t0
         n = sum(r[0] for r in res)
         tot_rows = sum(r[1] for r in res)
@@ -135,6 +140,21 @@ def cpu_baseline(inp, budget_s=12.0, max_scen=64, procs=0):
                               sample=f"{n} of {S} scenarios in {procs} single-threaded processes, "
                                      f"longest {t_max:.1f} s of oracle time ({wall:.1f} s wall with start-up)")
     return out
+
+
+def oracle_parity(ctl, results):
+    """The last timed step's IPS, frequency index and status against the
+    oracle's on the scenarios the CPU baseline ran (bit for bit)."""
+    idx = ctl.sel["freq_idx"].cpu().numpy()
+    st = ctl.sel["status"].cpu().numpy().view(np.uint32)
+    bad = []
+    for s, r in results.items():
+        ips = ctl.ips[s].cpu().numpy()
+        if not (np.array_equal(ips.view(np.uint32), r["ips"].view(np.uint32))
+                and int(idx[s]) == r["freq_idx"] and int(st[s]) == r["status"]):
+            bad.append(s)
+    return {"scenarios": len(results), "mismatched": bad[:16], "ok": not bad,
+            "compared": "IPS of every (frequency, iteration) row, frequency index, status"}
 
 
 def copy_bandwidth_gbs(mib=2048, reps=5):
@@ -569,10 +589,16 @@ def main():
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = n * 4
         del src, dst
+    parity_ok = True
     if cpu_base is not None:
         out["cpu_baseline"] = cpu_base
+        out["cpu_baseline"]["parity"] = oracle_parity(ctl, cpu_base.pop("_results"))
+        parity_ok = out["cpu_baseline"]["parity"]["ok"]
     forest.close()
     print(json.dumps(out), flush=True)
+    if not parity_ok:
+        log("the timed step's results differ from the oracle's on the baseline scenarios")
+        sys.exit(1)
 
 
 if __name__ == "__main__":
