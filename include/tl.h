@@ -248,6 +248,23 @@ tl_status tl_forest_predict_grid(const tl_forest* forest, int64_t n_scenarios, i
                                  void* stream);
 
 /* ------------------------------------------------------------------------
+ * tl_forest_predict_grid for callers that cannot allocate device memory
+ * (code under stream capture, tight serving loops, hosts that forbid
+ * allocation): same arguments, same results, no allocation of any kind.
+ * The work order's scratch is a fixed 32 MiB array of the library on each
+ * device (taken when the library is loaded); enough for 1,048,576
+ * (scenario, 32-iteration chunk) pairs, e.g. 16384 scenarios x 2048
+ * iterations.  A grid whose order needs more returns TL_EUNSUPPORTED and
+ * enqueues nothing.  Every call on one device shares that array: calls that
+ * overlap on one device (concurrent streams, other threads) race and must
+ * be serialized by the caller; tl_forest_predict_grid does not use it.
+ * ---------------------------------------------------------------------- */
+tl_status tl_forest_predict_grid_noalloc(const tl_forest* forest, int64_t n_scenarios, int32_t n_freqs,
+                                         int32_t horizon, const float* freqs_mhz, const int32_t* kv,
+                                         const int32_t* batch, const float* engine_size, float* out,
+                                         void* stream);
+
+/* ------------------------------------------------------------------------
  * Stage 2 through a table: the model compiled to its discrete input lattice.
  * The controller queries M only at a fixed list of frequencies, a few engine
  * sizes, integer batch sizes and integer KV blocks (Sec. 4.3.1 notes that

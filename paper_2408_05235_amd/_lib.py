@@ -24,7 +24,7 @@ MAX_HORIZON, MAX_BLOCK_TOKENS, MAX_FREQS, MAX_FEATURES, MAX_DEPTH = 8192, 65536,
 EXPORTED = ("tl_abi_version", "tl_last_error", "tl_forest_create", "tl_forest_destroy",
             "tl_project", "tl_forest_predict", "tl_forest_predict_grid", "tl_select_freq", "tl_admit",
             "tl_select_freq_binary", "tl_adjust_lengths", "tl_lattice_create", "tl_lattice_destroy",
-            "tl_lattice_bytes", "tl_lattice_predict_grid")
+            "tl_lattice_bytes", "tl_lattice_predict_grid", "tl_forest_predict_grid_noalloc")
 
 
 class ProjectArgs(ctypes.Structure):
@@ -80,6 +80,8 @@ def lib():
     L.tl_forest_predict.restype = ctypes.c_int
     L.tl_forest_predict_grid.argtypes = [P, i64, i32, i32, P, P, P, P, P, P]
     L.tl_forest_predict_grid.restype = ctypes.c_int
+    L.tl_forest_predict_grid_noalloc.argtypes = [P, i64, i32, i32, P, P, P, P, P, P]
+    L.tl_forest_predict_grid_noalloc.restype = ctypes.c_int
     L.tl_select_freq.argtypes = [P, i64, i32, i32, P, P, P, P, P, P, P]
     L.tl_select_freq.restype = ctypes.c_int
     L.tl_select_freq_binary.argtypes = [P, i64, i32, i32] + [P] * 14

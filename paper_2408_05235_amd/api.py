@@ -192,9 +192,11 @@ class Forest:
 
     predict = tl_forest_predict
 
-    def tl_forest_predict_grid(self, freqs_mhz, kv, batch, engine_size=None, out=None):
+    def tl_forest_predict_grid(self, freqs_mhz, kv, batch, engine_size=None, out=None, noalloc=False):
         """IPS on the projection grid: out[s, f, j] = M(freqs[f], kv[s, j],
-        batch[s, j] [, engine[s]]) without materializing the rows."""
+        batch[s, j] [, engine[s]]) without materializing the rows.  With
+        ``noalloc`` (and ``out`` given) the call goes to
+        tl_forest_predict_grid_noalloc, which allocates nothing."""
         _need(kv, torch.int32, "kv")
         if kv.dim() != 2:
             raise ValueError("kv must be [S, H]")
@@ -209,8 +211,8 @@ class Forest:
         if out is None:
             out = torch.empty((S, F, H), dtype=torch.float32, device=kv.device)
         _need(out, torch.float32, "out", (S, F, H))
-        check(lib().tl_forest_predict_grid(self._h, S, F, H, _p(freqs_mhz), _p(kv), _p(batch),
-                                           _p(engine_size), _p(out), _stream()))
+        fn = lib().tl_forest_predict_grid_noalloc if noalloc else lib().tl_forest_predict_grid
+        check(fn(self._h, S, F, H, _p(freqs_mhz), _p(kv), _p(batch), _p(engine_size), _p(out), _stream()))
         return out
 
     def close(self):

@@ -463,38 +463,83 @@ tl_status tl_forest_predict(const tl_forest* f, const float* rows, int64_t n_row
                     "tl_forest_predict: launch");
 }
 
-tl_status tl_forest_predict_grid(const tl_forest* f, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
-                                 const float* freqs_mhz, const int32_t* kv, const int32_t* batch,
-                                 const float* engine_size, float* out, void* stream) {
-    if (!f) return fail(TL_EINVAL, "tl_forest_predict_grid: forest is NULL");
+}  // extern "C"
+
+namespace {
+
+// Host checks of a grid prediction and its kernel parameters; TL_OK with
+// g->S == 0 means there is nothing to do.
+tl_status grid_params(const char* who, const tl_forest* f, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
+                      const float* freqs_mhz, const int32_t* kv, const int32_t* batch, const float* engine_size,
+                      float* out, tl::GridParams* g) {
+    *g = tl::GridParams{};
+    if (!f) return fail(TL_EINVAL, "%s: forest is NULL", who);
     if (f->dev.n_features != 3 && f->dev.n_features != 4)
-        return fail(TL_EINVAL, "tl_forest_predict_grid: the forest has %d features, the grid needs 3 or 4",
-                    f->dev.n_features);
+        return fail(TL_EINVAL, "%s: the forest has %d features, the grid needs 3 or 4", who, f->dev.n_features);
     if (n_scenarios < 0 || n_scenarios > 0x7fffffffll)
-        return fail(TL_EINVAL, "tl_forest_predict_grid: n_scenarios %lld outside [0, 2^31-1]", (long long)n_scenarios);
+        return fail(TL_EINVAL, "%s: n_scenarios %lld outside [0, 2^31-1]", who, (long long)n_scenarios);
     if (n_freqs < 1 || n_freqs > TL_MAX_FREQS)
-        return fail(TL_EINVAL, "tl_forest_predict_grid: n_freqs %d outside [1, %d]", n_freqs, TL_MAX_FREQS);
+        return fail(TL_EINVAL, "%s: n_freqs %d outside [1, %d]", who, n_freqs, TL_MAX_FREQS);
     if (horizon < 1 || horizon > TL_MAX_HORIZON)
-        return fail(TL_EINVAL, "tl_forest_predict_grid: horizon %d outside [1, %d]", horizon, TL_MAX_HORIZON);
+        return fail(TL_EINVAL, "%s: horizon %d outside [1, %d]", who, horizon, TL_MAX_HORIZON);
     if (n_scenarios > 0 && (!freqs_mhz || !kv || !batch || !out))
-        return fail(TL_EINVAL, "tl_forest_predict_grid: NULL required pointer");
+        return fail(TL_EINVAL, "%s: NULL required pointer", who);
     if (n_scenarios > 0 && f->dev.n_features == 4 && !engine_size)
-        return fail(TL_EINVAL, "tl_forest_predict_grid: a 4-feature forest needs engine_size");
+        return fail(TL_EINVAL, "%s: a 4-feature forest needs engine_size", who);
     if (n_scenarios == 0) return ok();
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess || cur != f->device)
-        return fail(TL_EINVAL, "tl_forest_predict_grid: the forest lives on device %d, the current device is %d",
-                    f->device, cur);
-    tl::GridParams g{};
-    g.S = n_scenarios;
-    g.F = n_freqs;
-    g.H = horizon;
-    g.freqs = freqs_mhz;
-    g.kv = kv;
-    g.batch = batch;
-    g.engine = f->dev.n_features == 4 ? engine_size : nullptr;
-    g.out = out;
+        return fail(TL_EINVAL, "%s: the forest lives on device %d, the current device is %d", who, f->device, cur);
+    g->S = n_scenarios;
+    g->F = n_freqs;
+    g->H = horizon;
+    g->freqs = freqs_mhz;
+    g->kv = kv;
+    g->batch = batch;
+    g->engine = f->dev.n_features == 4 ? engine_size : nullptr;
+    g->out = out;
+    return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+tl_status tl_forest_predict_grid(const tl_forest* f, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,
+                                 const float* freqs_mhz, const int32_t* kv, const int32_t* batch,
+                                 const float* engine_size, float* out, void* stream) {
+    tl::GridParams g;
+    const tl_status st = grid_params("tl_forest_predict_grid", f, n_scenarios, n_freqs, horizon, freqs_mhz, kv,
+                                     batch, engine_size, out, &g);
+    if (st != TL_OK || g.S == 0) return st;
     return from_hip(grid_with_workspace(f, g, (hipStream_t)stream), "tl_forest_predict_grid: launch");
+}
+
+tl_status tl_forest_predict_grid_noalloc(const tl_forest* f, int64_t n_scenarios, int32_t n_freqs,
+                                         int32_t horizon, const float* freqs_mhz, const int32_t* kv,
+                                         const int32_t* batch, const float* engine_size, float* out,
+                                         void* stream) {
+    const char* who = "tl_forest_predict_grid_noalloc";
+    tl::GridParams g;
+    const tl_status st = grid_params(who, f, n_scenarios, n_freqs, horizon, freqs_mhz, kv, batch, engine_size, out,
+                                     &g);
+    if (st != TL_OK || g.S == 0) return st;
+    size_t need = 0;
+    hipError_t e = tl::grid_order_bytes(f->dev, g, &need);
+    if (e != hipSuccess) return from_hip(e, "tl_forest_predict_grid_noalloc: sizing the work order");
+    if (need > tl::kNoAllocScratchBytes)
+        return fail(TL_EUNSUPPORTED,
+                    "%s: the work order of %lld scenarios x %d iterations needs %zu bytes of scratch, more than the "
+                    "fixed %zu (use tl_forest_predict_grid)",
+                    who, (long long)n_scenarios, horizon, need, tl::kNoAllocScratchBytes);
+    void* ws = nullptr;
+    if (need > 0) {
+        e = tl::noalloc_scratch(&ws);
+        if (e != hipSuccess) return from_hip(e, "tl_forest_predict_grid_noalloc: scratch address");
+    }
+    return from_hip(tl::launch_forest_grid(f->dev, g, ws, need > 0 ? tl::kNoAllocScratchBytes : 0,
+                                           (hipStream_t)stream),
+                    "tl_forest_predict_grid_noalloc: launch");
 }
 
 tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs, int32_t horizon,

@@ -42,6 +42,8 @@
 // others take the column kernel's staged walks).
 #include <hipcub/hipcub.hpp>
 
+#include <mutex>
+
 #include "device_util.h"
 #include "tl_internal.h"
 #include "forest_walk.h"
@@ -673,6 +675,36 @@ hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g_in, void* 
         if (e != hipSuccess) return e;
     }
     return f.n_features == 4 ? launch_grid_lds<4>(f, g, tb, lds, stream) : launch_grid_lds<3>(f, g, tb, lds, stream);
+}
+
+// Workspace of the grid kernel's work order for callers that cannot
+// allocate (tl_forest_predict_grid_noalloc): one fixed array per device,
+// shared by every such call on that device.  In host code `scratch` only
+// names the symbol; its device address comes from hipGetSymbolAddress, once
+// per device, and is kept in noalloc_ptr.
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex noalloc_mutex;
+void* noalloc_ptr[kMaxDevices];
+}  // namespace
+
+hipError_t noalloc_scratch(void** ptr) {
+    *ptr = nullptr;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(noalloc_mutex);
+    if (!noalloc_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        noalloc_ptr[dev] = p;
+    }
+    *ptr = noalloc_ptr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,

@@ -228,6 +228,10 @@ hipError_t grid_order_bytes(const ForestDev& f, const GridParams& g, size_t* byt
 // natural numbering (same results).  Nothing is allocated.
 hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g, void* ws, size_t ws_bytes,
                               hipStream_t stream);
+// The fixed work-order workspace of tl_forest_predict_grid_noalloc on the
+// current device (a device address; looked up once per device).
+constexpr size_t kNoAllocScratchBytes = (size_t)32 << 20;
+hipError_t noalloc_scratch(void** ptr);
 hipError_t launch_select(const SelectParams& p, hipStream_t stream);
 hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream);
 // The same kernel on arbitrary rows [n_rows][n_features] (3 or 4 features,
