@@ -83,6 +83,17 @@ void leaf_boxes(int32_t n_trees, int32_t depth, const uint8_t* feature, const fl
     }
 }
 
+// One bound of a leaf box for integer inputs, as stored in the records:
+// for integer x, x >= lo iff x >= ceil(lo) and x < hi iff x < ceil(hi);
+// the result is clamped to [0, maxv], which can only shrink the box (a row
+// outside the shrunk box walks the tree again).
+uint32_t box_bound(float x, uint32_t maxv) {
+    const double c = std::ceil((double)x);
+    if (!(c > 0.0)) return 0;
+    if (c >= (double)maxv) return maxv;
+    return (uint32_t)c;
+}
+
 // Up to kMaxCuts quantiles of the finite thresholds of one feature, ascending.
 std::vector<float> threshold_cuts(int64_t n_nodes, const uint8_t* feature, const float* threshold, int fi) {
     std::vector<float> t;
@@ -156,24 +167,30 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
     if (n_features >= 3) {
         leaf_boxes(n_trees, depth, feature, threshold, boxes);
         if (depth <= tl::kMaxRecordDepth) {
-            // per tree: nodes (threshold, then byte-permute selectors that
-            // pick the tested feature: sel1 frequency / KV, sel2 batch /
-            // engine size, sel3 between the two), leaf values, leaf boxes
+            // per tree: node slots (threshold, sel_lo, sel_hi, leaf value;
+            // sel_lo picks frequency / KV and batch / engine size by bit 0
+            // of the feature, sel_hi between the two by bit 1), then the
+            // leaf boxes as packed integer bounds
             constexpr uint32_t kLow = 0x03020100u, kHigh = 0x07060504u;
             const tl::RecordLayout R = tl::record_layout(depth);
             records.assign((size_t)n_trees * R.bytes + 64, 0);
             for (int64_t t = 0; t < n_trees; ++t) {
                 unsigned char* rec = records.data() + (size_t)t * R.bytes;
-                uint4* nd = (uint4*)rec;
+                uint32_t* slot = (uint32_t*)rec;
                 for (int64_t k = 0; k < n_int; ++k) {
                     const int64_t i = t * n_int + k;
                     const int fi = feature[i];
-                    uint32_t bits;
-                    std::memcpy(&bits, &threshold[i], 4);
-                    nd[k] = make_uint4(bits, fi == 1 ? kHigh : kLow, fi == 3 ? kHigh : kLow, fi >= 2 ? kHigh : kLow);
+                    std::memcpy(&slot[4 * k], &threshold[i], 4);
+                    slot[4 * k + 1] = (fi & 1) ? kHigh : kLow;
+                    slot[4 * k + 2] = (fi & 2) ? kHigh : kLow;
                 }
-                std::memcpy(rec + R.vals, leaf + t * n_leaf, (size_t)n_leaf * 4);
-                std::memcpy(rec + R.boxes, boxes.data() + t * n_leaf, (size_t)n_leaf * 16);
+                uint32_t* bw = (uint32_t*)(rec + R.boxes);
+                for (int64_t L = 0; L < n_leaf; ++L) {
+                    std::memcpy(&slot[4 * L + 3], &leaf[t * n_leaf + L], 4);
+                    const float4 b = boxes[(size_t)(t * n_leaf + L)];
+                    bw[2 * L] = box_bound(b.x, tl::kBoxKvMax) | box_bound(b.z, tl::kBoxBatchMax) << 20;
+                    bw[2 * L + 1] = box_bound(b.y, tl::kBoxKvMax) | box_bound(b.w, tl::kBoxBatchMax) << 20;
+                }
             }
         }
         boxes.resize(cells + 4, make_float4(0, 0, 0, 0));

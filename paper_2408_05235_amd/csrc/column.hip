@@ -76,7 +76,7 @@ __device__ __forceinline__ float column_freq(const ColumnParams& P, int64_t s) {
 // LDS byte address `tree`) for the RPL rows of a lane, all RPL x NT chains
 // interleaved, and adds the leaves to each row's sum in tree order.
 template <int NF, int NT, int RPL>
-__device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, uint32_t vals_off, int32_t depth,
+__device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, int32_t depth,
                                            const float (&xf)[RPL], const float (&kv)[RPL], const float (&bs)[RPL],
                                            const float (&xe)[RPL], double (&acc)[RPL]) {
     uint32_t a[RPL][NT], cl[NT], cr[NT];
@@ -90,16 +90,16 @@ __device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, ui
         for (int r = 0; r < RPL; ++r) a[r][t] = root;
     }
     for (int32_t level = 0; level < depth; ++level) {
-        u32x4 w[RPL][NT];
+        uint4 w[RPL][NT];
 #pragma unroll
         for (int r = 0; r < RPL; ++r)
 #pragma unroll
-            for (int t = 0; t < NT; ++t) w[r][t] = *(lds_u32x4*)(uintptr_t)a[r][t];
+            for (int t = 0; t < NT; ++t) w[r][t] = read_node(a[r][t]);
 #pragma unroll
         for (int r = 0; r < RPL; ++r)
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                const uint4 nd = make_uint4(w[r][t].x, w[r][t].y, w[r][t].z, w[r][t].w);
+                const uint4& nd = w[r][t];
                 const bool left = node_feature<NF>(nd, xf[r], kv[r], bs[r], xe[r]) < __uint_as_float(nd.x);
                 a[r][t] = 2u * a[r][t] + (left ? cl[t] : cr[t]);
             }
@@ -111,7 +111,7 @@ __device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, ui
         for (int t = 0; t < NT; ++t) {
             const uint32_t root = tree + t * rec_bytes;
             const int32_t k = (int32_t)((a[r][t] - root) >> 4) - n_int;
-            acc[r] += (double)*(__attribute__((address_space(3))) const float*)(uintptr_t)(root + vals_off + 4u * k);
+            acc[r] += (double)leaf_value(root, k);
         }
 }
 
@@ -210,10 +210,10 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
             int32_t t = 0;
             if (RPL == 1)
                 for (; t + 4 <= cnt; t += 4)
-                    add_leaves<NF, 4, RPL>(first + t * R.bytes, R.bytes, R.vals, depth, xf, kv, bs, xe, acc);
+                    add_leaves<NF, 4, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
             for (; t + 2 <= cnt; t += 2)
-                add_leaves<NF, 2, RPL>(first + t * R.bytes, R.bytes, R.vals, depth, xf, kv, bs, xe, acc);
-            if (t < cnt) add_leaves<NF, 1, RPL>(first + t * R.bytes, R.bytes, R.vals, depth, xf, kv, bs, xe, acc);
+                add_leaves<NF, 2, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
+            if (t < cnt) add_leaves<NF, 1, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
         }
         if (b + 1 < n_blocks) TL_COL_STORE(b + 1, cur ^ 1)
         __syncthreads();
@@ -227,12 +227,6 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
         if (o[r] >= 0) P.out[o[r]] = (float)acc[r];
 }
 
-// A leaf box read from LDS (byte address).
-__device__ __forceinline__ float4 lds_box(uint32_t addr) {
-    const u32x4 w = *(lds_u32x4*)(uintptr_t)addr;
-    return make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
-}
-
 // Leaf reuse along a lane's rows: a lane takes RPL consecutive iterations of
 // the scenario and keeps, for NT (1 or 2) consecutive staged trees, the
 // leaves its last walk reached and the intersection of their KV / batch
@@ -243,9 +237,7 @@ template <int NF, int NT, int RPL>
 __device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayout& R, int32_t depth, float xf,
                                                  const float (&kv)[RPL], const float (&bs)[RPL], float xe,
                                                  double (&acc)[RPL]) {
-    typedef __attribute__((address_space(3))) const float lds_f32;
-    const uint32_t vals0 = tree + R.vals, boxes0 = tree + R.boxes;
-    const uint32_t vals1 = vals0 + R.bytes, boxes1 = boxes0 + R.bytes;
+    const uint32_t tree1 = tree + R.bytes;
     float4 box = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
     int32_t leaf[NT];
     double v[NT];
@@ -269,8 +261,8 @@ __device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayo
                 walk<NF, 1>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
                 leaf[0] = k[0];
             } else {
-                const bool n0 = !in_box(lds_box(boxes0 + 16u * leaf[0]), kv[r], bs[r]);
-                const bool n1 = !in_box(lds_box(boxes1 + 16u * leaf[NT - 1]), kv[r], bs[r]);
+                const bool n0 = !in_box(leaf_box(tree, R, leaf[0]), kv[r], bs[r]);
+                const bool n1 = !in_box(leaf_box(tree1, R, leaf[NT - 1]), kv[r], bs[r]);
                 if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
                     int32_t k[2];
                     walk<NF, 2>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
@@ -284,7 +276,7 @@ __device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayo
                     }
                     if (n1) {
                         int32_t k[1];
-                        walk<NF, 1>(tree + R.bytes, R.bytes, depth, xf, kv[r], bs[r], xe, k);
+                        walk<NF, 1>(tree1, R.bytes, depth, xf, kv[r], bs[r], xe, k);
                         leaf[NT - 1] = k[0];
                     }
                 }
@@ -293,11 +285,11 @@ __device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayo
             moved = false;
         }
         if (moved) {
-            v[0] = (double)*(lds_f32*)(uintptr_t)(vals0 + 4u * leaf[0]);
-            box = lds_box(boxes0 + 16u * leaf[0]);
+            v[0] = (double)leaf_value(tree, leaf[0]);
+            box = leaf_box(tree, R, leaf[0]);
             if (NT == 2) {
-                v[NT - 1] = (double)*(lds_f32*)(uintptr_t)(vals1 + 4u * leaf[NT - 1]);
-                box = box_meet(box, lds_box(boxes1 + 16u * leaf[NT - 1]));
+                v[NT - 1] = (double)leaf_value(tree1, leaf[NT - 1]);
+                box = box_meet(box, leaf_box(tree1, R, leaf[NT - 1]));
             }
         }
 #pragma unroll
@@ -404,8 +396,8 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
                     double a4[4] = {acc[4 * h], acc[4 * h + 1], acc[4 * h + 2], acc[4 * h + 3]};
                     int32_t u = 0;
                     for (; u + 2 <= cnt; u += 2)
-                        add_leaves<NF, 2, 4>(first + u * R.bytes, R.bytes, R.vals, depth, xf4, kv4, bs4, xe4, a4);
-                    if (u < cnt) add_leaves<NF, 1, 4>(first + u * R.bytes, R.bytes, R.vals, depth, xf4, kv4, bs4, xe4, a4);
+                        add_leaves<NF, 2, 4>(first + u * R.bytes, R.bytes, depth, xf4, kv4, bs4, xe4, a4);
+                    if (u < cnt) add_leaves<NF, 1, 4>(first + u * R.bytes, R.bytes, depth, xf4, kv4, bs4, xe4, a4);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) acc[4 * h + i] = a4[i];
                 }

@@ -113,7 +113,7 @@ __global__ __launch_bounds__(256) void forest_rows_kernel(const uint2* __restric
 }
 
 #ifndef TL_LDS_J
-#define TL_LDS_J 32
+#define TL_LDS_J 44
 #endif
 #ifndef TL_LDS_WAVES
 #define TL_LDS_WAVES 16
@@ -212,10 +212,22 @@ __global__ __launch_bounds__(kCostThreads) void grid_cost_kernel(const float* __
 
 constexpr int kLdsWaves = TL_LDS_WAVES;  // wavefronts per workgroup
 constexpr int kLdsThreads = kLdsWaves * kWave;
-#ifndef TL_STAGE_REGS
-#define TL_STAGE_REGS (5 * 16 / TL_LDS_WAVES)
-#endif
-constexpr int kStageRegs = TL_STAGE_REGS;  // staged 16-byte words per thread per block
+// Tree blocks are copied into LDS in pieces of 64 lanes x 16 bytes; each of
+// the two block buffers is a whole number of pieces.
+constexpr uint32_t kStagePiece = kWave * 16;
+__host__ __device__ inline uint32_t stage_buffer_bytes(int32_t tb, const RecordLayout& R) {
+    return ((uint32_t)tb * R.bytes + kStagePiece - 1) / kStagePiece * kStagePiece;
+}
+// One piece: lane l copies the 16 bytes at its `src` to LDS byte address
+// lds + 16 l (lds the same in every lane).  Issued as an instruction the compiler does not track, so it
+// does not make the evaluation's LDS reads wait for the copy (they read
+// other buffers); the kernel waits for it (vmcnt) before the block barrier
+// that hands the buffer over.  No other vector-memory load is in flight
+// inside the block loop.
+__device__ __forceinline__ void stage_piece(const uint4* src, uint32_t lds) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds);   // wavefront-uniform by construction
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(base), "v"(src) : "memory", "m0");
+}
 
 // A wavefront-uniform value read into a scalar register: the compiler's lane
 // read, with the empty asm statements hiding how x was computed and pinning
@@ -235,13 +247,14 @@ constexpr int kRowGroup = TL_ROW_GROUP;   // rows whose (KV, batch) hull is test
 
 // Adds the leaves of NT (1 or 2) consecutive staged trees (records R.bytes
 // apart, the first at `tree`) to the J row sums of a wavefront, in tree
-// order.  hull[g] = (min KV, max KV, min batch, max batch) over rows
-// g*8 .. g*8+7; kv4 holds the rows' (KV, batch) pairs, two per 16 bytes.
-// A lane keeps the leaves its walks reached and the intersection of their
-// boxes.  A group whose hull lies inside that box on every lane needs only
-// its adds; other groups test row by row.  A lane whose row leaves the
-// intersection re-reads both leaf boxes and walks only the trees whose own
-// box it left (both in one pass when the wavefront needs both).
+// order.  hull[g] = (min KV, max KV, min batch, max batch) over the rows of
+// group g; kv4 holds the rows' (KV, batch) pairs, two per 16 bytes.  A lane
+// keeps the values of the leaves its walks reached, their boxes and the
+// intersection of the boxes.  A group whose hull lies inside that
+// intersection on every lane needs only its adds; other groups test row by
+// row.  A lane whose row leaves the intersection walks only the trees whose
+// own box it left (both in one pass when the wavefront needs both) and reads
+// the new leaves' values and boxes.
 template <int NF, int J, int NT>
 __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tree_off, const RecordLayout& R,
                                            int32_t depth,
@@ -254,18 +267,14 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
     asm volatile("" ::: "memory");
     const unsigned char* tree = lds + tree_off;
     const uint32_t tree_addr = lds_addr(tree);
-    const float* vals0 = (const float*)(tree + R.vals);
-    const float4* boxes0 = (const float4*)(tree + R.boxes);
-    const float* vals1 = (const float*)(tree + R.bytes + R.vals);
-    const float4* boxes1 = (const float4*)(tree + R.bytes + R.boxes);
+    const uint32_t tree1 = tree_addr + R.bytes;
     float4 box = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);   // empty: first row walks
-    int32_t leaf[NT];
+    // a pair's own leaf boxes, decoded, beside their intersection: after a
+    // walk only the walked tree's box is read again
+    float4 b0 = box, b1 = box;
     double v[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        leaf[t] = 0;
-        v[t] = 0.0;
-    }
+    for (int t = 0; t < NT; ++t) v[t] = 0.0;
 #pragma unroll
     for (int gi = 0; gi < J / kRowGroup; ++gi) {
         const uint64_t inside = __builtin_amdgcn_fcmpf(hull[gi][0], box.x, 3) &   // min KV >= kv_lo
@@ -289,38 +298,38 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
                     if (NT == 1) {
                         int32_t k[1];
                         walk<NF, 1>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
-                        leaf[0] = k[0];
-                    } else if (gi == 0 && i == 0) {
-                        int32_t k[2];       // first row: both trees, every lane
-                        walk<NF, 2>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
-                        leaf[0] = k[0];
-                        leaf[NT - 1] = k[1];
+                        v[0] = (double)leaf_value(tree_addr, k[0]);
+                        box = leaf_box(tree_addr, R, k[0]);
                     } else {
-                        const bool n0 = !in_box(boxes0[leaf[0]], kv, bs);
-                        const bool n1 = !in_box(boxes1[leaf[NT - 1]], kv, bs);
+                        // first row: both trees, every lane
+                        const bool n0 = (gi == 0 && i == 0) || !in_box(b0, kv, bs);
+                        const bool n1 = (gi == 0 && i == 0) || !in_box(b1, kv, bs);
                         if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
                             int32_t k[2];
                             walk<NF, 2>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
-                            leaf[0] = k[0];
-                            leaf[NT - 1] = k[1];
+                            if (n0) {
+                                v[0] = (double)leaf_value(tree_addr, k[0]);
+                                b0 = leaf_box(tree_addr, R, k[0]);
+                            }
+                            if (n1) {
+                                v[NT - 1] = (double)leaf_value(tree1, k[1]);
+                                b1 = leaf_box(tree1, R, k[1]);
+                            }
                         } else {
                             if (n0) {
                                 int32_t k[1];
                                 walk<NF, 1>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
-                                leaf[0] = k[0];
+                                v[0] = (double)leaf_value(tree_addr, k[0]);
+                                b0 = leaf_box(tree_addr, R, k[0]);
                             }
                             if (n1) {
                                 int32_t k[1];
-                                walk<NF, 1>(tree_addr + R.bytes, R.bytes, depth, xf, kv, bs, xe, k);
-                                leaf[NT - 1] = k[0];
+                                walk<NF, 1>(tree1, R.bytes, depth, xf, kv, bs, xe, k);
+                                v[NT - 1] = (double)leaf_value(tree1, k[0]);
+                                b1 = leaf_box(tree1, R, k[0]);
                             }
                         }
-                    }
-                    v[0] = (double)vals0[leaf[0]];
-                    box = boxes0[leaf[0]];
-                    if (NT == 2) {
-                        v[NT - 1] = (double)vals1[leaf[NT - 1]];
-                        box = box_meet(box, boxes1[leaf[NT - 1]]);
+                        box = box_meet(b0, b1);
                     }
                 }
             }
@@ -342,7 +351,7 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
     const int32_t n_leaf = 1 << depth;
     const RecordLayout R = record_layout(depth);
     const uint32_t rec_words = R.bytes / 16u;
-    const uint32_t buf_bytes = (uint32_t)tb * R.bytes;
+    const uint32_t buf_bytes = stage_buffer_bytes(tb, R);
 
     const int wave = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -363,61 +372,34 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
     }
 
     // staging: block b is trees [b*tb, b*tb + cnt), one contiguous range of
-    // 16-byte words in global memory and in LDS.  Each thread moves up to
-    // kStageRegs words: one load per word straight into its own register, so
-    // the loads stay in flight while the current block is evaluated.
+    // 16-byte words in global memory and in LDS.  The wavefronts copy it in
+    // 1 KiB pieces (64 lanes x 16 bytes) straight from global memory into LDS
+    // (global_load_lds_dwordx4, no registers), wavefront w taking pieces w,
+    // w + 16, ...  The copy of the next block runs while the current one is
+    // evaluated and is waited for (vmcnt) before the block barrier.  Lanes
+    // past the block's last word copy its first word into the buffer's
+    // padding (buffers are whole pieces), so no lane writes outside its
+    // buffer.
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
-    static_assert(kStageRegs >= 1 && kStageRegs <= 12, "staging code below moves up to twelve words");
-    uint4 rw0 = make_uint4(0, 0, 0, 0), rw1 = rw0, rw2 = rw0, rw3 = rw0;
-    uint4 rw4 = rw0, rw5 = rw0, rw6 = rw0, rw7 = rw0, rw8 = rw0, rw9 = rw0, rw10 = rw0, rw11 = rw0;
     double acc[J];
 #pragma unroll
     for (int jj = 0; jj < J; ++jj) acc[jj] = (double)base;
-
-#define TL_BLOCK_WORDS(b) ((uint32_t)min(tb, n_trees - (b) * tb) * rec_words)
-#define TL_FETCH_WORD(r, reg)                                                  \
-    if ((r) < kStageRegs) {                                                    \
-        /* unconditional (threads past the block re-read word 0), so the   */ \
-        /* loads issue back to back without waits between them             */ \
-        const uint32_t i0 = threadIdx.x + (r) * kLdsThreads;                   \
-        reg = src[i0 < wt ? i0 : 0];                                           \
-    }
-#define TL_FETCH(b)                                                            \
-    {                                                                          \
-        const uint32_t wt = TL_BLOCK_WORDS(b);                                 \
-        const uint4* src = records + (int64_t)(b) * tb * rec_words;            \
-        TL_FETCH_WORD(0, rw0) TL_FETCH_WORD(1, rw1)                            \
-        TL_FETCH_WORD(2, rw2) TL_FETCH_WORD(3, rw3)                            \
-        TL_FETCH_WORD(4, rw4) TL_FETCH_WORD(5, rw5)                            \
-        TL_FETCH_WORD(6, rw6) TL_FETCH_WORD(7, rw7)                            \
-        TL_FETCH_WORD(8, rw8) TL_FETCH_WORD(9, rw9)                            \
-        TL_FETCH_WORD(10, rw10) TL_FETCH_WORD(11, rw11)                        \
-    }
-#define TL_STORE_WORD(r, reg)                                                  \
-    if ((r) < kStageRegs) {                                                    \
-        const uint32_t i = threadIdx.x + (r) * kLdsThreads;                    \
-        if (i < wt) dst[i] = reg;                                              \
-    }
-#define TL_STORE(b, buf)                                                       \
-    {                                                                          \
-        const uint32_t wt = TL_BLOCK_WORDS(b);                                 \
-        uint4* dst = (uint4*)(smem + (buf) * buf_bytes);                       \
-        TL_STORE_WORD(0, rw0) TL_STORE_WORD(1, rw1)                            \
-        TL_STORE_WORD(2, rw2) TL_STORE_WORD(3, rw3)                            \
-        TL_STORE_WORD(4, rw4) TL_STORE_WORD(5, rw5)                            \
-        TL_STORE_WORD(6, rw6) TL_STORE_WORD(7, rw7)                            \
-        TL_STORE_WORD(8, rw8) TL_STORE_WORD(9, rw9)                            \
-        TL_STORE_WORD(10, rw10) TL_STORE_WORD(11, rw11)                        \
-    }
+    auto stage = [&](int32_t b, int buf) {
+        const uint32_t wt = (uint32_t)min(tb, n_trees - b * tb) * rec_words;
+        const uint4* src = records + (int64_t)b * tb * rec_words;
+        const uint32_t n_pieces = (wt + kWave - 1) / kWave;
+        for (uint32_t pc = (uint32_t)wave; pc < n_pieces; pc += kLdsWaves) {
+            const uint32_t i = pc * kWave + lane;
+            stage_piece(src + (i < wt ? i : 0u), lds_addr(smem + buf * buf_bytes + pc * kStagePiece));
+        }
+    };
 
     // Make the lane's frequency / engine size complete here, before any
-    // staging load is in flight: otherwise the walks inside the loop would
-    // each wait for all outstanding loads, including the prefetch.
+    // staging copy is in flight: otherwise the walks inside the loop would
+    // each wait for all outstanding copies, including the prefetch.
     asm volatile("" ::"v"(xf), "v"(xe));
-    if (n_blocks > 0) {
-        TL_FETCH(0)
-        TL_STORE(0, 0)
-    }
+    if (n_blocks > 0) stage(0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     // per row group, the (KV, batch) hull of its rows (wavefront-uniform)
     const float4* kvb4 = (const float4*)kvb;
@@ -440,7 +422,7 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
     }
     for (int32_t b = 0; b < n_blocks; ++b) {
         const int cur = b & 1;
-        if (b + 1 < n_blocks) TL_FETCH(b + 1)
+        if (b + 1 < n_blocks) stage(b + 1, cur ^ 1);
         if (g.valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
             const uint32_t bp = cur * buf_bytes;
@@ -453,14 +435,9 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
                 eval_trees<NF, J, 2>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
             if (tt < cnt) eval_trees<NF, J, 1>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
         }
-        if (b + 1 < n_blocks) TL_STORE(b + 1, cur ^ 1)
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     }
-#undef TL_STORE
-#undef TL_STORE_WORD
-#undef TL_FETCH
-#undef TL_FETCH_WORD
-#undef TL_BLOCK_WORDS
     if (active) {
         float* o = P.out + ((int64_t)g.s * F + g.f) * H + g.j0;
 #pragma unroll
@@ -553,16 +530,14 @@ hipError_t launch_nf(const ForestDev& f, const float* rows, int64_t n_rows, floa
 // registers.  0 = the LDS kernel cannot run.
 int32_t lds_trees_per_block(const ForestDev& f, size_t* lds_bytes) {
     if (!f.records || f.depth > kMaxRecordDepth) return 0;
-    const size_t rec = record_layout(f.depth).bytes;
+    const RecordLayout R = record_layout(f.depth);
     const size_t head = (size_t)kLdsWaves * kLdsJ * sizeof(float2);
     const size_t budget = (size_t)TL_LDS_BUDGET_KIB * 1024;
-    auto fits = [&](int32_t tb) {
-        return 2 * (size_t)tb * rec + head <= budget && (size_t)tb * rec / 16 <= (size_t)kStageRegs * kLdsThreads;
-    };
+    auto fits = [&](int32_t tb) { return 2 * (size_t)stage_buffer_bytes(tb, R) + head <= budget; };
     int32_t tb = 64;
     while (tb > 1 && !fits(tb)) --tb;
     if (!fits(tb)) return 0;
-    *lds_bytes = 2 * (size_t)tb * rec + head;
+    *lds_bytes = 2 * (size_t)stage_buffer_bytes(tb, R) + head;
     return tb;
 }
 

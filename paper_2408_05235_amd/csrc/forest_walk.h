@@ -12,15 +12,16 @@ namespace tl {
 namespace {
 
 // The value of the feature a record node tests, picked with byte permutes:
-// node = (threshold, sel1, sel2, sel3); sel1 picks frequency or KV, sel2
-// batch or engine size, sel3 between the two picks (v_perm_b32: selector
-// 0x03020100 keeps the second operand, 0x07060504 takes the first).
+// node = (threshold, sel_lo, sel_hi, leaf value); sel_lo picks frequency or
+// KV and, with the same selector, batch or engine size; sel_hi picks between
+// the two (v_perm_b32: selector 0x03020100 keeps the second operand,
+// 0x07060504 takes the first).
 template <int NF>
 __device__ __forceinline__ float node_feature(const uint4& nd, float xf, float kv, float bs, float xe) {
     const uint32_t x01 = __builtin_amdgcn_perm(__float_as_uint(kv), __float_as_uint(xf), nd.y);
-    const uint32_t x23 = NF == 4 ? __builtin_amdgcn_perm(__float_as_uint(xe), __float_as_uint(bs), nd.z)
+    const uint32_t x23 = NF == 4 ? __builtin_amdgcn_perm(__float_as_uint(xe), __float_as_uint(bs), nd.y)
                                  : __float_as_uint(bs);
-    return __uint_as_float(__builtin_amdgcn_perm(x23, x01, nd.w));
+    return __uint_as_float(__builtin_amdgcn_perm(x23, x01, nd.z));
 }
 
 // Whether (kv, batch) lies in a leaf box (kv_lo, kv_hi, batch_lo, batch_hi).
@@ -34,11 +35,36 @@ __device__ __forceinline__ float4 box_meet(const float4& a, const float4& b) {
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
+typedef __attribute__((address_space(3))) const float lds_f32;
 
 // LDS byte address of a location in the kernel's dynamic LDS.
 __device__ __forceinline__ uint32_t lds_addr(const unsigned char* p) {
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const unsigned char*)p;
+}
+
+// The node slot at LDS byte address `a`, (threshold, sel_lo, sel_hi, leaf
+// value), read whole (a 12-byte read of the node alone measured slower).
+__device__ __forceinline__ uint4 read_node(uint32_t a) {
+    const u32x4 w = *(lds_u32x4*)(uintptr_t)a;
+    return make_uint4(w.x, w.y, w.z, w.w);
+}
+
+// The value of leaf L of the staged tree whose record starts at LDS byte
+// address `tree` (word 3 of node slot L).
+__device__ __forceinline__ float leaf_value(uint32_t tree, int32_t L) {
+    return *(lds_f32*)(uintptr_t)(tree + 16u * (uint32_t)L + 12u);
+}
+
+// The KV / batch box of leaf L of a staged tree, decoded from its packed
+// integer bounds into (kv_lo, kv_hi, batch_lo, batch_hi) as floats (exact:
+// all bounds are below 2^24).
+__device__ __forceinline__ float4 leaf_box(uint32_t tree, const RecordLayout& R, int32_t L) {
+    const u32x2 w = *(lds_u32x2*)(uintptr_t)(tree + R.boxes + 8u * (uint32_t)L);
+    return make_float4((float)(w.x & kBoxKvMax), (float)(w.y & kBoxKvMax), (float)(w.x >> 20),
+                       (float)(w.y >> 20));
 }
 
 // Walks NT consecutive staged trees (records rec_bytes apart, the first at
@@ -63,8 +89,7 @@ __device__ __forceinline__ void walk(uint32_t tree, uint32_t rec_bytes, int32_t 
     for (int32_t level = 0; level < depth; ++level) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            const u32x4 w = *(lds_u32x4*)(uintptr_t)a[t];
-            const uint4 nd = make_uint4(w.x, w.y, w.z, w.w);
+            const uint4 nd = read_node(a[t]);
             const bool left = node_feature<NF>(nd, xf, kv, bs, xe) < __uint_as_float(nd.x);
             a[t] = 2u * a[t] + (left ? cl[t] : cr[t]);
         }
