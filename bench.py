@@ -15,7 +15,6 @@ to its input lattice (a separate mode with a one-time build), and the
 admission-control what-ifs (one new query per scenario) on the same workload.
 """
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -61,15 +60,15 @@ def algorithmic_bytes(inp, F, rows, sel=None):
     return dict(project=k1, predict=k2, select=k3)
 
 
-def traffic_record(cfg_name):
-    """HBM bytes per forest launch from committed rocprofv3 counters, if they
-    were taken on the current forest kernel source."""
-    path = os.path.join(ROOT, "profiles", f"forest_{cfg_name.split('_')[0]}_traffic.json")
+def traffic_record(path):
+    """HBM bytes per launch from a committed rocprofv3 traffic record, if it
+    was taken on the current sources of its kernel."""
     if not os.path.exists(path):
         return None
+    from paper_2408_05235_amd import prof_summary
     rec = json.load(open(path))
-    src = open(os.path.join(ROOT, "paper_2408_05235_amd", "csrc", "forest.hip"), "rb").read()
-    if rec.get("forest_hip_sha256") != hashlib.sha256(src).hexdigest():
+    names = rec.get("sources")
+    if not names or rec.get("sources_sha256") != prof_summary.sources_sha256(names):
         return None
     return rec.get("bytes_per_launch")
 
@@ -329,13 +328,7 @@ def lattice_bench(inp, cfg, ctl, steps, warmup, admission=None, max_gib=24):
     rows = S * F * H
     byt = 8 * rows + 8 * S * H
     achieved = byt / (look_ms / 1e3) / 1e9
-    traffic = None
-    path = LATTICE_FILE.format(cfg["name"].split("_")[0])
-    if os.path.exists(path):
-        rec = json.load(open(path))
-        src = open(os.path.join(ROOT, "paper_2408_05235_amd", "csrc", "lattice.hip"), "rb").read()
-        if rec.get("lattice_hip_sha256") == hashlib.sha256(src).hexdigest():
-            traffic = rec.get("bytes_per_launch")
+    traffic = traffic_record(LATTICE_FILE.format(cfg["name"].split("_")[0]))
     # the binary search with M read from the table
     for _ in range(max(1, warmup)):
         ctl.select_binary(lat)
@@ -535,7 +528,7 @@ def main():
     ops_per_row = f["n_trees"]
     forest_s = stage_ms[1] / 1e3
     achieved = ops_per_row * rows / forest_s / 1e12
-    traffic = traffic_record(cfg["name"])
+    traffic = traffic_record(os.path.join(ROOT, "profiles", f"forest_{cfg['name'].split('_')[0]}_traffic.json"))
 
     out = {
         "metric": METRIC,
@@ -574,12 +567,17 @@ def main():
     }
     out["results_d2h_ms"] = d2h_results_ms(ctl)
     out["adjust_lengths"] = adjust_lengths_bench(inp, dev_in, args.steps, copy_gbs)
+    log("length stage done")
     out["materialized_rows"] = materialized_rows_bench(inp, dev_in, forest, ctl, args.steps, copy_gbs)
+    log("materialized rows done")
     out["lattice"] = lattice_bench(inp, cfg, ctl, args.steps, args.warmup,
                                    lambda lat: admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup, lat),
                                    max_gib=args.lattice_max_gib)
+    log("lattice mode done")
     out["binary_search"] = binary_search_bench(ctl, args.steps, args.warmup)
+    log("binary search done")
     out["admission"] = admission_bench(inp, cfg, dev_in, forest, args.steps, args.warmup)
+    log("admission done")
     if args.copy_calibration_mib:
         n = args.copy_calibration_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda:0")

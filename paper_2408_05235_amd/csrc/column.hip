@@ -38,7 +38,6 @@ namespace {
 
 constexpr int kColWaves = 16;
 constexpr int kColThreads = kColWaves * kWave;
-constexpr int kColStage = 6;                       // staged 16-byte words per thread per block
 constexpr size_t kColLdsBudget = 152 * 1024;
 
 template <int RPL>
@@ -122,7 +121,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     extern __shared__ __align__(16) unsigned char smem[];
     const RecordLayout R = record_layout(depth);
     const uint32_t rec_words = R.bytes / 16u;
-    const uint32_t buf_bytes = (uint32_t)tb * R.bytes;
+    const uint32_t buf_bytes = stage_buffer_bytes(tb, R);
     const int wave = threadIdx.x / kWave;
     const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kColWaves + wave);
     float xf[RPL], kv[RPL], bs[RPL], xe[RPL];
@@ -164,46 +163,14 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     }
 
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
-    // block b: trees [b*tb, b*tb + cnt), one contiguous range of words; each
-    // thread moves word threadIdx.x + r * kColThreads through register st<r>
-    static_assert(kColStage >= 1 && kColStage <= 8, "staging below names up to eight registers");
-    uint4 st0 = make_uint4(0, 0, 0, 0), st1 = st0, st2 = st0, st3 = st0, st4 = st0, st5 = st0, st6 = st0, st7 = st0;
-#define TL_COL_FETCH_WORD(r, reg)                                              \
-    if ((r) < kColStage) {                                                     \
-        const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
-        reg = src[i < words ? i : 0];                                          \
-    }
-#define TL_COL_FETCH(b)                                                        \
-    {                                                                          \
-        const uint32_t words = (uint32_t)min(tb, n_trees - (b) * tb) * rec_words; \
-        const uint4* src = records + (int64_t)(b) * tb * rec_words;            \
-        TL_COL_FETCH_WORD(0, st0) TL_COL_FETCH_WORD(1, st1)                    \
-        TL_COL_FETCH_WORD(2, st2) TL_COL_FETCH_WORD(3, st3)                    \
-        TL_COL_FETCH_WORD(4, st4) TL_COL_FETCH_WORD(5, st5)                    \
-        TL_COL_FETCH_WORD(6, st6) TL_COL_FETCH_WORD(7, st7)                    \
-    }
-#define TL_COL_STORE_WORD(r, reg)                                              \
-    if ((r) < kColStage) {                                                     \
-        const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
-        if (i < words) dst[i] = reg;                                           \
-    }
-#define TL_COL_STORE(b, buf)                                                   \
-    {                                                                          \
-        const uint32_t words = (uint32_t)min(tb, n_trees - (b) * tb) * rec_words; \
-        uint4* dst = (uint4*)(smem + (buf) * buf_bytes);                       \
-        TL_COL_STORE_WORD(0, st0) TL_COL_STORE_WORD(1, st1)                    \
-        TL_COL_STORE_WORD(2, st2) TL_COL_STORE_WORD(3, st3)                    \
-        TL_COL_STORE_WORD(4, st4) TL_COL_STORE_WORD(5, st5)                    \
-        TL_COL_STORE_WORD(6, st6) TL_COL_STORE_WORD(7, st7)                    \
-    }
-    if (n_blocks > 0) {
-        TL_COL_FETCH(0)
-        TL_COL_STORE(0, 0)
-    }
+    // staging (stage_block): the next block's copy runs during evaluation
+    if (n_blocks > 0) stage_block(records, n_trees, tb, rec_words, 0, lds_addr(smem), wave, kColWaves);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     for (int32_t b = 0; b < n_blocks; ++b) {
         const int cur = b & 1;
-        if (b + 1 < n_blocks) TL_COL_FETCH(b + 1)
+        if (b + 1 < n_blocks)
+            stage_block(records, n_trees, tb, rec_words, b + 1, lds_addr(smem) + (cur ^ 1) * buf_bytes, wave, kColWaves);
         if (valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
             const uint32_t first = lds_addr(smem) + cur * buf_bytes;
@@ -215,13 +182,9 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
                 add_leaves<NF, 2, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
             if (t < cnt) add_leaves<NF, 1, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
         }
-        if (b + 1 < n_blocks) TL_COL_STORE(b + 1, cur ^ 1)
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     }
-#undef TL_COL_STORE
-#undef TL_COL_STORE_WORD
-#undef TL_COL_FETCH
-#undef TL_COL_FETCH_WORD
 #pragma unroll
     for (int r = 0; r < RPL; ++r)
         if (o[r] >= 0) P.out[o[r]] = (float)acc[r];
@@ -229,67 +192,70 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
 
 // Leaf reuse along a lane's rows: a lane takes RPL consecutive iterations of
 // the scenario and keeps, for NT (1 or 2) consecutive staged trees, the
-// leaves its last walk reached and the intersection of their KV / batch
-// boxes (a row inside it reaches the same leaves: the frequency and engine
-// size are the scenario's).  A row outside walks only the tree(s) whose own
-// box it left, both in one interleaved pass when the wavefront needs both.
+// values of the leaves its last walks reached, their KV / batch boxes and
+// the intersection of the boxes (a row inside it reaches the same leaves:
+// the frequency and engine size are the scenario's).  A row outside walks
+// only the tree(s) whose own box it left, both in one interleaved pass when
+// the wavefront needs both.
 template <int NF, int NT, int RPL>
 __device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayout& R, int32_t depth, float xf,
                                                  const float (&kv)[RPL], const float (&bs)[RPL], float xe,
                                                  double (&acc)[RPL]) {
     const uint32_t tree1 = tree + R.bytes;
     float4 box = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
-    int32_t leaf[NT];
+    float4 b0 = box, b1 = box;   // the trees' own leaf boxes, decoded
     double v[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        leaf[t] = 0;
-        v[t] = 0.0;
-    }
+    for (int t = 0; t < NT; ++t) v[t] = 0.0;
 #pragma unroll
     for (int r = 0; r < RPL; ++r) {
-        bool moved = true;   // this lane reached other leaves: reload values and box
         if (r == 0) {
             // first row: every tree, every lane
             int32_t k[NT];
             walk<NF, NT>(tree, R.bytes, depth, xf, kv[0], bs[0], xe, k);
-#pragma unroll
-            for (int t = 0; t < NT; ++t) leaf[t] = k[t];
+            v[0] = (double)leaf_value(tree, k[0]);
+            b0 = leaf_box(tree, R, k[0]);
+            box = b0;
+            if (NT == 2) {
+                v[NT - 1] = (double)leaf_value(tree1, k[NT - 1]);
+                b1 = leaf_box(tree1, R, k[NT - 1]);
+                box = box_meet(b0, b1);
+            }
         } else if (!in_box(box, kv[r], bs[r])) {
             if (NT == 1) {
                 int32_t k[1];
                 walk<NF, 1>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
-                leaf[0] = k[0];
+                v[0] = (double)leaf_value(tree, k[0]);
+                box = leaf_box(tree, R, k[0]);
             } else {
-                const bool n0 = !in_box(leaf_box(tree, R, leaf[0]), kv[r], bs[r]);
-                const bool n1 = !in_box(leaf_box(tree1, R, leaf[NT - 1]), kv[r], bs[r]);
+                const bool n0 = !in_box(b0, kv[r], bs[r]);
+                const bool n1 = !in_box(b1, kv[r], bs[r]);
                 if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
                     int32_t k[2];
                     walk<NF, 2>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
-                    leaf[0] = k[0];
-                    leaf[NT - 1] = k[1];
+                    if (n0) {
+                        v[0] = (double)leaf_value(tree, k[0]);
+                        b0 = leaf_box(tree, R, k[0]);
+                    }
+                    if (n1) {
+                        v[NT - 1] = (double)leaf_value(tree1, k[1]);
+                        b1 = leaf_box(tree1, R, k[1]);
+                    }
                 } else {
                     if (n0) {
                         int32_t k[1];
                         walk<NF, 1>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
-                        leaf[0] = k[0];
+                        v[0] = (double)leaf_value(tree, k[0]);
+                        b0 = leaf_box(tree, R, k[0]);
                     }
                     if (n1) {
                         int32_t k[1];
                         walk<NF, 1>(tree1, R.bytes, depth, xf, kv[r], bs[r], xe, k);
-                        leaf[NT - 1] = k[0];
+                        v[NT - 1] = (double)leaf_value(tree1, k[0]);
+                        b1 = leaf_box(tree1, R, k[0]);
                     }
                 }
-            }
-        } else {
-            moved = false;
-        }
-        if (moved) {
-            v[0] = (double)leaf_value(tree, leaf[0]);
-            box = leaf_box(tree, R, leaf[0]);
-            if (NT == 2) {
-                v[NT - 1] = (double)leaf_value(tree1, leaf[NT - 1]);
-                box = box_meet(box, leaf_box(tree1, R, leaf[NT - 1]));
+                box = box_meet(b0, b1);
             }
         }
 #pragma unroll
@@ -312,7 +278,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
     extern __shared__ __align__(16) unsigned char smem[];
     const RecordLayout R = record_layout(depth);
     const uint32_t rec_words = R.bytes / 16u;
-    const uint32_t buf_bytes = (uint32_t)tb * R.bytes;
+    const uint32_t buf_bytes = stage_buffer_bytes(tb, R);
     const int wave = threadIdx.x / kWave;
     const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kColWaves + wave);
     const int32_t span = kWave * RPL;
@@ -341,44 +307,13 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
     const bool reuse = 2 * steps_changed <= kWave * (RPL - 1);   // wavefront-uniform
     static_assert(RPL % 4 == 0, "the walk-every-row path takes four rows at a time");
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
-    static_assert(kColStage >= 1 && kColStage <= 8, "staging below names up to eight registers");
-    uint4 st0 = make_uint4(0, 0, 0, 0), st1 = st0, st2 = st0, st3 = st0, st4 = st0, st5 = st0, st6 = st0, st7 = st0;
-#define TL_COL_FETCH_WORD(r, reg)                                              \
-    if ((r) < kColStage) {                                                     \
-        const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
-        reg = src[i < words ? i : 0];                                          \
-    }
-#define TL_COL_FETCH(b)                                                        \
-    {                                                                          \
-        const uint32_t words = (uint32_t)min(tb, n_trees - (b) * tb) * rec_words; \
-        const uint4* src = records + (int64_t)(b) * tb * rec_words;            \
-        TL_COL_FETCH_WORD(0, st0) TL_COL_FETCH_WORD(1, st1)                    \
-        TL_COL_FETCH_WORD(2, st2) TL_COL_FETCH_WORD(3, st3)                    \
-        TL_COL_FETCH_WORD(4, st4) TL_COL_FETCH_WORD(5, st5)                    \
-        TL_COL_FETCH_WORD(6, st6) TL_COL_FETCH_WORD(7, st7)                    \
-    }
-#define TL_COL_STORE_WORD(r, reg)                                              \
-    if ((r) < kColStage) {                                                     \
-        const uint32_t i = threadIdx.x + (r) * kColThreads;                    \
-        if (i < words) dst[i] = reg;                                           \
-    }
-#define TL_COL_STORE(b, buf)                                                   \
-    {                                                                          \
-        const uint32_t words = (uint32_t)min(tb, n_trees - (b) * tb) * rec_words; \
-        uint4* dst = (uint4*)(smem + (buf) * buf_bytes);                       \
-        TL_COL_STORE_WORD(0, st0) TL_COL_STORE_WORD(1, st1)                    \
-        TL_COL_STORE_WORD(2, st2) TL_COL_STORE_WORD(3, st3)                    \
-        TL_COL_STORE_WORD(4, st4) TL_COL_STORE_WORD(5, st5)                    \
-        TL_COL_STORE_WORD(6, st6) TL_COL_STORE_WORD(7, st7)                    \
-    }
-    if (n_blocks > 0) {
-        TL_COL_FETCH(0)
-        TL_COL_STORE(0, 0)
-    }
+    if (n_blocks > 0) stage_block(records, n_trees, tb, rec_words, 0, lds_addr(smem), wave, kColWaves);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     for (int32_t b = 0; b < n_blocks; ++b) {
         const int cur = b & 1;
-        if (b + 1 < n_blocks) TL_COL_FETCH(b + 1)
+        if (b + 1 < n_blocks)
+            stage_block(records, n_trees, tb, rec_words, b + 1, lds_addr(smem) + (cur ^ 1) * buf_bytes, wave, kColWaves);
         if (valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
             const uint32_t first = lds_addr(smem) + cur * buf_bytes;
@@ -403,13 +338,9 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
                 }
             }
         }
-        if (b + 1 < n_blocks) TL_COL_STORE(b + 1, cur ^ 1)
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
     }
-#undef TL_COL_STORE
-#undef TL_COL_STORE_WORD
-#undef TL_COL_FETCH
-#undef TL_COL_FETCH_WORD
     if (valid) {
 #pragma unroll
         for (int r = 0; r < RPL; ++r)
@@ -447,15 +378,14 @@ __global__ __launch_bounds__(256) void forest_column_global_kernel(const uint2* 
     P.out[c.s * P.H + c.j[0]] = (float)acc;
 }
 
-// Trees per staged block: double buffers within the LDS budget, and no more
-// words per block than the staging registers of one workgroup hold.
+// Trees per staged block: double buffers within the LDS budget.
 int32_t column_trees_per_block(const ForestDev& f, size_t* lds) {
     if (!f.records || f.n_trees == 0) return 0;
     const RecordLayout R = record_layout(f.depth);
-    const int64_t by_lds = (int64_t)(kColLdsBudget / (2 * (size_t)R.bytes));
-    const int64_t by_regs = (int64_t)kColStage * kColThreads / (R.bytes / 16);
-    const int32_t tb = (int32_t)std::min<int64_t>(std::min<int64_t>(by_lds, by_regs), f.n_trees);
-    *lds = (size_t)2 * tb * R.bytes;
+    int32_t tb = std::min<int32_t>(f.n_trees, 64);
+    while (tb > 1 && 2 * (size_t)stage_buffer_bytes(tb, R) > kColLdsBudget) --tb;
+    if (2 * (size_t)stage_buffer_bytes(tb, R) > kColLdsBudget) return 0;
+    *lds = (size_t)2 * stage_buffer_bytes(tb, R);
     return tb;
 }
 

@@ -212,23 +212,6 @@ __global__ __launch_bounds__(kCostThreads) void grid_cost_kernel(const float* __
 
 constexpr int kLdsWaves = TL_LDS_WAVES;  // wavefronts per workgroup
 constexpr int kLdsThreads = kLdsWaves * kWave;
-// Tree blocks are copied into LDS in pieces of 64 lanes x 16 bytes; each of
-// the two block buffers is a whole number of pieces.
-constexpr uint32_t kStagePiece = kWave * 16;
-__host__ __device__ inline uint32_t stage_buffer_bytes(int32_t tb, const RecordLayout& R) {
-    return ((uint32_t)tb * R.bytes + kStagePiece - 1) / kStagePiece * kStagePiece;
-}
-// One piece: lane l copies the 16 bytes at its `src` to LDS byte address
-// lds + 16 l (lds the same in every lane).  Issued as an instruction the compiler does not track, so it
-// does not make the evaluation's LDS reads wait for the copy (they read
-// other buffers); the kernel waits for it (vmcnt) before the block barrier
-// that hands the buffer over.  No other vector-memory load is in flight
-// inside the block loop.
-__device__ __forceinline__ void stage_piece(const uint4* src, uint32_t lds) {
-    const uint32_t base = __builtin_amdgcn_readfirstlane(lds);   // wavefront-uniform by construction
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(base), "v"(src) : "memory", "m0");
-}
-
 // A wavefront-uniform value read into a scalar register: the compiler's lane
 // read, with the empty asm statements hiding how x was computed and pinning
 // the result to the scalar register file (the compiler would otherwise
@@ -371,27 +354,15 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
         kvb[lane] = make_float2((float)P.kv[g.s * H + j], (float)P.batch[g.s * H + j]);
     }
 
-    // staging: block b is trees [b*tb, b*tb + cnt), one contiguous range of
-    // 16-byte words in global memory and in LDS.  The wavefronts copy it in
-    // 1 KiB pieces (64 lanes x 16 bytes) straight from global memory into LDS
-    // (global_load_lds_dwordx4, no registers), wavefront w taking pieces w,
-    // w + 16, ...  The copy of the next block runs while the current one is
-    // evaluated and is waited for (vmcnt) before the block barrier.  Lanes
-    // past the block's last word copy its first word into the buffer's
-    // padding (buffers are whole pieces), so no lane writes outside its
-    // buffer.
+    // staging (stage_block): the copy of the next block runs while the
+    // current one is evaluated and is waited for (vmcnt) before the block
+    // barrier.
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
     double acc[J];
 #pragma unroll
     for (int jj = 0; jj < J; ++jj) acc[jj] = (double)base;
     auto stage = [&](int32_t b, int buf) {
-        const uint32_t wt = (uint32_t)min(tb, n_trees - b * tb) * rec_words;
-        const uint4* src = records + (int64_t)b * tb * rec_words;
-        const uint32_t n_pieces = (wt + kWave - 1) / kWave;
-        for (uint32_t pc = (uint32_t)wave; pc < n_pieces; pc += kLdsWaves) {
-            const uint32_t i = pc * kWave + lane;
-            stage_piece(src + (i < wt ? i : 0u), lds_addr(smem + buf * buf_bytes + pc * kStagePiece));
-        }
+        stage_block(records, n_trees, tb, rec_words, b, lds_addr(smem + buf * buf_bytes), wave, kLdsWaves);
     };
 
     // Make the lane's frequency / engine size complete here, before any

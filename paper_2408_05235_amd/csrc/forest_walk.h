@@ -67,6 +67,43 @@ __device__ __forceinline__ float4 leaf_box(uint32_t tree, const RecordLayout& R,
                        (float)(w.y >> 20));
 }
 
+// Staging of tree blocks: block b is trees [b*tb, b*tb + cnt), one
+// contiguous range of 16-byte words in global memory and in LDS.  The
+// wavefronts of a workgroup copy it in pieces of 64 lanes x 16 bytes
+// straight from global memory into LDS (global_load_lds_dwordx4, no
+// registers), wavefront w of n taking pieces w, w + n, ...  Lanes past the
+// block's last word copy its first word into the buffer's padding (buffers
+// are whole pieces), so no lane writes outside its buffer.
+constexpr uint32_t kStagePiece = kWave * 16;
+
+__host__ __device__ inline uint32_t stage_buffer_bytes(int32_t tb, const RecordLayout& R) {
+    return ((uint32_t)tb * R.bytes + kStagePiece - 1) / kStagePiece * kStagePiece;
+}
+
+// One piece: lane l copies the 16 bytes at its `src` to LDS byte address
+// lds + 16 l (lds the same in every lane).  Issued as an instruction the
+// compiler does not track, so it does not make the evaluation's LDS reads
+// wait for the copy (they read other buffers); a kernel waits for its copies
+// (vmcnt) before the block barrier that hands the buffer over, and has no
+// other vector-memory load in flight inside its block loop.
+__device__ __forceinline__ void stage_piece(const uint4* src, uint32_t lds) {
+    const uint32_t base = __builtin_amdgcn_readfirstlane(lds);   // wavefront-uniform by construction
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(base), "v"(src) : "memory", "m0");
+}
+
+// Enqueues this wavefront's pieces of block b (rec_words 16-byte words per
+// tree) into the LDS buffer at byte address dst.
+__device__ __forceinline__ void stage_block(const uint4* records, int32_t n_trees, int32_t tb, uint32_t rec_words,
+                                            int32_t b, uint32_t dst, int wave, int n_waves) {
+    const uint32_t words = (uint32_t)min(tb, n_trees - b * tb) * rec_words;
+    const uint4* src = records + (int64_t)b * tb * rec_words;
+    const uint32_t n_pieces = (words + kWave - 1) / kWave;
+    for (uint32_t pc = (uint32_t)wave; pc < n_pieces; pc += (uint32_t)n_waves) {
+        const uint32_t i = pc * kWave + lane_id();
+        stage_piece(src + (i < words ? i : 0u), dst + pc * kStagePiece);
+    }
+}
+
 // Walks NT consecutive staged trees (records rec_bytes apart, the first at
 // LDS byte address `tree`) from the root for one row; k[t] = leaf index of
 // tree t.  The walks of two trees interleave, so their chains of dependent

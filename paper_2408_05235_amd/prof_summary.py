@@ -3,7 +3,7 @@
     python -m paper_2408_05235_amd.prof_summary stats  <kernel_stats.csv> <out.md> <command>
     python -m paper_2408_05235_amd.prof_summary trace  <kernel_trace.csv> <out.md> <command>
     python -m paper_2408_05235_amd.prof_summary traffic <fetch_counter_collection.csv> \
-        <write_counter_collection.csv> <kernel substring> <copy bytes> <out.json> <command> [source file]
+        <write_counter_collection.csv> <kernel substring> <copy bytes> <out.json> <command>
 
     python -m paper_2408_05235_amd.prof_summary counters <out.md> <kernel substring> <command> \
         <counter_collection.csv> [<counter_collection.csv> ...]
@@ -85,7 +85,23 @@ def _per_dispatch(csv_path, counter):
     return [(d, k, v) for d, (k, v) in sorted(agg.items())]
 
 
-def traffic(fetch_csv, write_csv, kernel, copy_bytes, out_json, command, source="forest.hip"):
+# the sources each profiled kernel is built from: a traffic record is used
+# only while all of them still hash the same
+KERNEL_SOURCES = {
+    "forest_grid_lds": ["forest.hip", "forest_walk.h", "tl_internal.h", "device_util.h", "api.cpp"],
+    "lattice_gather": ["lattice.hip", "tl_internal.h", "device_util.h", "api.cpp"],
+}
+
+
+def sources_sha256(names):
+    h = hashlib.sha256()
+    for n in names:
+        h.update(n.encode())
+        h.update(open(os.path.join(PKG, "csrc", n), "rb").read())
+    return h.hexdigest()
+
+
+def traffic(fetch_csv, write_csv, kernel, copy_bytes, out_json, command):
     res = {}
     for name, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
         disp = _per_dispatch(path, counter)
@@ -100,11 +116,11 @@ def traffic(fetch_csv, write_csv, kernel, copy_bytes, out_json, command, source=
         # of the same kernel, such as building a lattice table)
         res[name] = dict(kib_per_launch=vals[0], copy_kib=copies[-1], scale=scale,
                          bytes_per_launch=vals[0] * 1024.0 * scale)
-    src = open(os.path.join(PKG, "csrc", source), "rb").read()
+    names = KERNEL_SOURCES[kernel]
     rec = dict(kernel=kernel, command=command, copy_bytes=copy_bytes,
                fetch=res["fetch"], write=res["write"],
-               bytes_per_launch=res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"])
-    rec[source.replace(".", "_") + "_sha256"] = hashlib.sha256(src).hexdigest()
+               bytes_per_launch=res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"],
+               sources=names, sources_sha256=sources_sha256(names))
     json.dump(rec, open(out_json, "w"), indent=1)
     return rec
 
@@ -160,7 +176,7 @@ if __name__ == "__main__":
         kernel_stats(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5] if len(sys.argv) > 5 else "")
     elif sys.argv[1] == "traffic":
         print(json.dumps(traffic(sys.argv[2], sys.argv[3], sys.argv[4], int(sys.argv[5]), sys.argv[6],
-                                 sys.argv[7], *(sys.argv[8:9])), indent=1))
+                                 sys.argv[7]), indent=1))
     elif sys.argv[1] == "counters":
         print(counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5:]))
     else:
