@@ -15,8 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_DIR = os.path.join(PKG, "lib")
 LIB_PATH = os.path.join(LIB_DIR, "libtl.so")
-SOURCES = ["api.cpp", "project.hip", "forest.hip", "column.hip", "lattice.hip", "select.hip"]
-HEADERS = ["device_util.h", "tl_internal.h", "forest_walk.h"]
+SOURCES = ["api.cpp", "host_forest.cpp", "project.hip", "forest.hip", "column.hip", "lattice.hip", "select.hip"]
+HEADERS = ["device_util.h", "tl_internal.h", "forest_walk.h", "record_format.h", "host_forest.h"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

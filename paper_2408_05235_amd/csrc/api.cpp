@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "device_util.h"
+#include "host_forest.h"
 #include "tl.h"
 #include "tl_internal.h"
 
@@ -47,64 +48,6 @@ struct tl_lattice {
 namespace {
 
 thread_local char g_err[512] = "";
-
-// KV / batch box of every leaf: the constraints that its path puts on
-// features 1 and 2.  Going to 2k+1 means x < thr (an upper bound); going to
-// 2k+2 means !(x < thr), i.e. x >= thr for non-NaN x (a lower bound).  A NaN
-// threshold sends every row to 2k+2: no constraint there, and nothing reaches
-// the 2k+1 side, whose leaves get an empty box.
-void leaf_boxes(int32_t n_trees, int32_t depth, const uint8_t* feature, const float* threshold,
-                std::vector<float4>& out) {
-    const int64_t n_int = (1ll << depth) - 1;
-    const int64_t n_leaf = 1ll << depth;
-    out.assign((size_t)(n_trees * n_leaf), make_float4(0, 0, 0, 0));
-    for (int64_t t = 0; t < n_trees; ++t) {
-        const uint8_t* ft = feature + t * n_int;
-        const float* th = threshold + t * n_int;
-        for (int64_t L = 0; L < n_leaf; ++L) {
-            float lo[2] = {-INFINITY, -INFINITY}, hi[2] = {INFINITY, INFINITY};
-            bool empty = false;
-            int64_t k = 0;
-            for (int32_t l = 0; l < depth; ++l) {
-                const int bit = (int)((L >> (depth - 1 - l)) & 1);   // 0: to 2k+1, 1: to 2k+2
-                const float thr = th[k];
-                const int f = ft[k];
-                if (bit == 0) {
-                    if (std::isnan(thr)) empty = true;
-                    else if (f == 1 || f == 2) hi[f - 1] = std::fmin(hi[f - 1], thr);
-                } else if (!std::isnan(thr) && (f == 1 || f == 2)) {
-                    lo[f - 1] = std::fmax(lo[f - 1], thr);
-                }
-                k = 2 * k + 1 + bit;
-            }
-            out[(size_t)(t * n_leaf + L)] = empty ? make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY)
-                                                  : make_float4(lo[0], hi[0], lo[1], hi[1]);
-        }
-    }
-}
-
-// One bound of a leaf box for integer inputs, as stored in the records:
-// for integer x, x >= lo iff x >= ceil(lo) and x < hi iff x < ceil(hi);
-// the result is clamped to [0, maxv], which can only shrink the box (a row
-// outside the shrunk box walks the tree again).
-uint32_t box_bound(float x, uint32_t maxv) {
-    const double c = std::ceil((double)x);
-    if (!(c > 0.0)) return 0;
-    if (c >= (double)maxv) return maxv;
-    return (uint32_t)c;
-}
-
-// Up to kMaxCuts quantiles of the finite thresholds of one feature, ascending.
-std::vector<float> threshold_cuts(int64_t n_nodes, const uint8_t* feature, const float* threshold, int fi) {
-    std::vector<float> t;
-    for (int64_t i = 0; i < n_nodes; ++i)
-        if (feature[i] == fi && std::isfinite(threshold[i])) t.push_back(threshold[i]);
-    std::sort(t.begin(), t.end());
-    if ((int64_t)t.size() <= tl::kMaxCuts) return t;
-    std::vector<float> c(tl::kMaxCuts);
-    for (int64_t i = 0; i < tl::kMaxCuts; ++i) c[(size_t)i] = t[(size_t)(i * (int64_t)t.size() / tl::kMaxCuts)];
-    return c;
-}
 
 tl_status fail(tl_status st, const char* fmt, ...) {
     va_list ap;
@@ -162,43 +105,20 @@ tl_status tl_forest_create(int32_t n_trees, int32_t depth, int32_t n_features, f
             nodes[(size_t)(t * n_leaf + k)] = make_uint2(bits, feature[i]);
         }
     for (size_t i = 0; i < cells; ++i) leaves[i] = leaf[i];
+    std::vector<tl::host::Box> leaf_box;
     std::vector<float4> boxes;
     std::vector<unsigned char> records;
     if (n_features >= 3) {
-        leaf_boxes(n_trees, depth, feature, threshold, boxes);
-        if (depth <= tl::kMaxRecordDepth) {
-            // per tree: node slots (threshold, sel_lo, sel_hi, leaf value;
-            // sel_lo picks frequency / KV and batch / engine size by bit 0
-            // of the feature, sel_hi between the two by bit 1), then the
-            // leaf boxes as packed integer bounds
-            constexpr uint32_t kLow = 0x03020100u, kHigh = 0x07060504u;
-            const tl::RecordLayout R = tl::record_layout(depth);
-            records.assign((size_t)n_trees * R.bytes + 64, 0);
-            for (int64_t t = 0; t < n_trees; ++t) {
-                unsigned char* rec = records.data() + (size_t)t * R.bytes;
-                uint32_t* slot = (uint32_t*)rec;
-                for (int64_t k = 0; k < n_int; ++k) {
-                    const int64_t i = t * n_int + k;
-                    const int fi = feature[i];
-                    std::memcpy(&slot[4 * k], &threshold[i], 4);
-                    slot[4 * k + 1] = (fi & 1) ? kHigh : kLow;
-                    slot[4 * k + 2] = (fi & 2) ? kHigh : kLow;
-                }
-                uint32_t* bw = (uint32_t*)(rec + R.boxes);
-                for (int64_t L = 0; L < n_leaf; ++L) {
-                    std::memcpy(&slot[4 * L + 3], &leaf[t * n_leaf + L], 4);
-                    const float4 b = boxes[(size_t)(t * n_leaf + L)];
-                    bw[2 * L] = box_bound(b.x, tl::kBoxKvMax) | box_bound(b.z, tl::kBoxBatchMax) << 20;
-                    bw[2 * L + 1] = box_bound(b.y, tl::kBoxKvMax) | box_bound(b.w, tl::kBoxBatchMax) << 20;
-                }
-            }
-        }
-        boxes.resize(cells + 4, make_float4(0, 0, 0, 0));
+        tl::host::leaf_boxes(n_trees, depth, feature, threshold, leaf_box);
+        if (depth <= tl::kMaxRecordDepth) tl::host::build_records(n_trees, depth, feature, threshold, leaf, leaf_box, records);
+        boxes.assign(cells + 4, make_float4(0, 0, 0, 0));
+        for (size_t i = 0; i < leaf_box.size(); ++i)
+            boxes[i] = make_float4(leaf_box[i].kv_lo, leaf_box[i].kv_hi, leaf_box[i].batch_lo, leaf_box[i].batch_hi);
     }
     std::vector<float> cuts_kv, cuts_bs;
     if (n_features >= 3 && n_int > 0) {
-        cuts_kv = threshold_cuts(n_trees * n_int, feature, threshold, 1);
-        cuts_bs = threshold_cuts(n_trees * n_int, feature, threshold, 2);
+        cuts_kv = tl::host::threshold_cuts(n_trees * n_int, feature, threshold, 1);
+        cuts_bs = tl::host::threshold_cuts(n_trees * n_int, feature, threshold, 2);
     }
 
     tl_forest* f = new (std::nothrow) tl_forest();

@@ -88,8 +88,9 @@ def _per_dispatch(csv_path, counter):
 # the sources each profiled kernel is built from: a traffic record is used
 # only while all of them still hash the same
 KERNEL_SOURCES = {
-    "forest_grid_lds": ["forest.hip", "forest_walk.h", "tl_internal.h", "device_util.h", "api.cpp"],
-    "lattice_gather": ["lattice.hip", "tl_internal.h", "device_util.h", "api.cpp"],
+    "forest_grid_lds": ["forest.hip", "forest_walk.h", "tl_internal.h", "record_format.h", "device_util.h",
+                        "host_forest.cpp", "api.cpp"],
+    "lattice_gather": ["lattice.hip", "tl_internal.h", "record_format.h", "device_util.h", "api.cpp"],
 }
 
 
