@@ -134,11 +134,9 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
             // queue order: each queued arrival must be >= every earlier one
             const int32_t v = queued ? a : -1;
             const int32_t incl = wave_incl_max(v);
-            int32_t excl = __shfl_up(incl, 1);
-            if (lane == 0) excl = -1;
-            excl = max(excl, arr_carry);
+            const int32_t excl = max(wave_shift_up1(incl, -1), arr_carry);
             if (queued && a < excl) fl |= TL_FLAG_UNSORTED;
-            arr_carry = max(arr_carry, __shfl(incl, kWave - 1));
+            arr_carry = max(arr_carry, lane63(incl));
         }
     }
     // the appended query (admission control): one more request that starts

@@ -60,7 +60,7 @@ __device__ __forceinline__ bool feasible_wave(const float* ips, const uint64_t* 
                 bad |= d != kNoDeadline && !(before + p[k] < d);
             }
         }
-        carry = __shfl(before + run, kWave - 1);
+        carry = lane63_u64(before + run);
         if (__ballot(bad)) return false;
     }
     return carry <= budget;
@@ -135,7 +135,7 @@ __device__ __forceinline__ uint64_t wave_times(const float* ips, const uint64_t*
         const uint64_t d = in ? dl[j] : kNoDeadline;
         m |= in && d != kNoDeadline && !(tr < d);
         mo |= in && j == own_at && !(tr < d_own);
-        carry = __shfl(tr, kWave - 1);
+        carry = lane63_u64(tr);
     }
     *miss = __ballot(m) != 0;
     *miss_own = __ballot(mo) != 0;
