@@ -251,13 +251,25 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
     const unsigned char* tree = lds + tree_off;
     const uint32_t tree_addr = lds_addr(tree);
     const uint32_t tree1 = tree_addr + R.bytes;
-    float4 box = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);   // empty: first row walks
     // a pair's own leaf boxes, decoded, beside their intersection: after a
     // walk only the walked tree's box is read again
-    float4 b0 = box, b1 = box;
+    float4 box, b0, b1 = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
     double v[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) v[t] = 0.0;
+    {
+        // the chunk's first row walks every tree on every lane, outside the
+        // group loop so that the loop's walks carry no first-row case
+        const float4 q0 = kv4[0];
+        int32_t k[NT];
+        walk<NF, NT>(tree_addr, R.bytes, depth, xf, q0.x, q0.y, xe, k);
+        v[0] = (double)leaf_value(tree_addr, k[0]);
+        b0 = leaf_box(tree_addr, R, k[0]);
+        box = b0;
+        if (NT == 2) {
+            v[NT - 1] = (double)leaf_value(tree1, k[NT - 1]);
+            b1 = leaf_box(tree1, R, k[NT - 1]);
+            box = box_meet(b0, b1);
+        }
+    }
 #pragma unroll
     for (int gi = 0; gi < J / kRowGroup; ++gi) {
         const uint64_t inside = __builtin_amdgcn_fcmpf(hull[gi][0], box.x, 3) &   // min KV >= kv_lo
@@ -284,9 +296,8 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
                         v[0] = (double)leaf_value(tree_addr, k[0]);
                         box = leaf_box(tree_addr, R, k[0]);
                     } else {
-                        // first row: both trees, every lane
-                        const bool n0 = (gi == 0 && i == 0) || !in_box(b0, kv, bs);
-                        const bool n1 = (gi == 0 && i == 0) || !in_box(b1, kv, bs);
+                        const bool n0 = !in_box(b0, kv, bs);
+                        const bool n1 = !in_box(b1, kv, bs);
                         if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
                             int32_t k[2];
                             walk<NF, 2>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
