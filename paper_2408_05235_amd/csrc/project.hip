@@ -28,7 +28,8 @@
 // checking the whole projected vector from the current iteration on.
 // Without a batch cap, up to 64 requests are tried at once at their FIFO
 // targets with one check of their summed contribution; when that fails the
-// batch shrinks, down to one request at a time.
+// batch shrinks, and below 8 requests a growing number of them are admitted
+// one at a time before batching again.
 #include "device_util.h"
 #include "tl_internal.h"
 
@@ -83,12 +84,56 @@ __device__ __forceinline__ void inflight_jumps(int32_t c, int32_t e, int32_t H, 
     }
 }
 
+// Adds (or, NEG, takes away) the KV blocks ceil((c + t - a) / N) of a request
+// with c cached tokens that starts at iteration a (Eq. 1) to KV[t] for every
+// t in [a, lim), a <= lim <= H, 64 iterations per step, by LDS adds that
+// return nothing.  POW2: N is a power of two no larger than 64 (log2 N =
+// divN.l), so the division is a shift and the value grows by exactly 64 / N
+// from one step to the next; the whole steps go 2 * UNROLL per loop trip.
+// Otherwise every step divides, UNROLL steps per trip.
+template <bool NEG, bool POW2, int UNROLL>
+__device__ __forceinline__ void add_request(int32_t* KV, int32_t c, int32_t a, int32_t lim, const DivU32& divN) {
+    const int lane = lane_id();
+    if (POW2) {
+        int32_t v = (int32_t)(((uint32_t)c + divN.d - 1u + (uint32_t)lane) >> divN.l);
+        if (NEG) v = -v;
+        const int32_t step = NEG ? -(kWave >> divN.l) : (kWave >> divN.l);
+        int32_t* q = KV + a + lane;
+        int32_t n = (int32_t)((uint32_t)(lim - a) / kWave);   // whole steps
+        for (; n >= 2 * UNROLL; n -= 2 * UNROLL) {
+#pragma unroll
+            for (int u = 0; u < 2 * UNROLL; ++u) atomicAdd(q + u * kWave, v + u * step);
+            q += 2 * UNROLL * kWave;
+            v += 2 * UNROLL * step;
+        }
+        for (; n > 0; --n) {
+            atomicAdd(q, v);
+            q += kWave;
+            v += step;
+        }
+        if (lane < ((lim - a) & (kWave - 1))) atomicAdd(q, v);
+    } else {
+#pragma unroll UNROLL
+        for (int32_t t0 = a; t0 < lim; t0 += kWave) {
+            const int32_t t = t0 + lane;
+            if (t < lim) {
+                const int32_t v = (int32_t)ceil_div_u32((uint32_t)(c + t - a), divN);
+                atomicAdd(&KV[t], NEG ? -v : v);
+            }
+        }
+    }
+}
+
 // BD_LDS: the batch difference array lives in LDS beside the KV curve, as a
 // batch cap needs (the admission loop reads its running sums).  Without a
 // cap it is only added to and finally prefix-summed, so it accumulates with
 // atomics in the scenario's own batch output row instead: half the LDS, twice
 // the scenario wavefronts per CU.
-template <bool BD_LDS>
+// Smallest batch of queued requests tried at once (no batch cap): below it the
+// admission loop takes requests one at a time.
+constexpr int32_t kMinBatch = 8;
+
+template <bool BD_LDS, bool POW2>
 __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     extern __shared__ int32_t lds[];
     const int32_t H = P.H;
@@ -303,21 +348,19 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                     const int32_t am = __builtin_amdgcn_readlane(a, m);
                     const int32_t cm = __builtin_amdgcn_readlane(q_c, m);
                     const int32_t lm = __builtin_amdgcn_readlane(q_len, m);
-                    const int32_t lim = (int32_t)min((int64_t)am + lm, (int64_t)H);
+                    const int32_t lim = lm >= H - am ? H : am + lm;
                     r_end = max(r_end, lim);
                     // LDS adds without a returned value: no wait per chunk
-                    for (int32_t t0 = am; t0 < lim; t0 += kWave) {
-                        const int32_t t = t0 + lane;
-                        if (t < lim) atomicAdd(&KV[t], (int32_t)ceil_div_u32((uint32_t)(cm + t - am), divN));
-                    }
+                    add_request<false, POW2, 1>(KV, cm, am, lim, divN);
                 }
                 const int32_t a_first = __builtin_amdgcn_readlane(a, __ffsll((unsigned long long)take) - 1);
                 bool bad = false;
-                if (!kv_fits)
-                    for (int32_t t0 = a_first; t0 < r_end; t0 += kWave) {
-                        const int32_t t = t0 + lane;
-                        if (t < r_end && KV[t] > cap) bad = true;
-                    }
+                if (!kv_fits) {
+                    int32_t t0 = a_first;
+#pragma unroll 4
+                    for (; t0 + kWave <= r_end; t0 += kWave) bad |= KV[t0 + lane] > cap;
+                    if (t0 + lane < r_end) bad |= KV[t0 + lane] > cap;
+                }
                 const bool fits = __ballot(bad) == 0;
                 if (!fits) {
                     // take the batch's contributions out again
@@ -326,18 +369,15 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                         const int32_t am = __builtin_amdgcn_readlane(a, m);
                         const int32_t cm = __builtin_amdgcn_readlane(q_c, m);
                         const int32_t lm = __builtin_amdgcn_readlane(q_len, m);
-                        const int32_t lim = (int32_t)min((int64_t)am + lm, (int64_t)H);
-                        for (int32_t t0 = am; t0 < lim; t0 += kWave) {
-                            const int32_t t = t0 + lane;
-                            if (t < lim) atomicAdd(&KV[t], -(int32_t)ceil_div_u32((uint32_t)(cm + t - am), divN));
-                        }
+                        const int32_t lim = lm >= H - am ? H : am + lm;
+                        add_request<true, POW2, 1>(KV, cm, am, lim, divN);
                     }
                     // shrink the batch; once down to single requests, admit
                     // a growing number of them one at a time before batching
                     // again (the capacity binds)
                     bsz >>= 2;
-                    if (bsz < 2) {
-                        bsz = 2;
+                    if (bsz < kMinBatch) {
+                        bsz = kMinBatch;
                         seq_left = backoff;
                         backoff = min(2 * backoff, 256);
                     }
@@ -388,7 +428,8 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                             const int32_t t = t0 + k * kWave + lane;
                             bool badt = false;
                             if (t < lim)
-                                badt = KV[t] + (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN) > cap;
+                                badt = KV[t] + (int32_t)(POW2 ? ((uint32_t)(h_c + t - j) + divN.d - 1u) >> divN.l
+                                                              : ceil_div_u32((uint32_t)(h_c + t - j), divN)) > cap;
                             m[k] = __ballot(badt);
                         }
 #pragma unroll
@@ -442,11 +483,7 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
             if (!admitted) break;
             const int64_t e = (int64_t)j + h_len;
             const int32_t lim = (int32_t)min(e, (int64_t)H);
-#pragma unroll 4
-            for (int32_t t0 = j; t0 < lim; t0 += kWave) {
-                const int32_t t = t0 + lane;
-                if (t < lim) KV[t] += (int32_t)ceil_div_u32((uint32_t)(h_c + t - j), divN);
-            }
+            add_request<false, POW2, 4>(KV, h_c, j, lim, divN);
             if (lane == 0) {
                 if (BD_LDS) {
                     BD[j] += 1;
@@ -582,15 +619,16 @@ hipError_t launch_project(const ProjectParams& p, hipStream_t stream) {
     // scenario); otherwise the LDS array is faster.
     const bool bd_lds = p.batch_cap != nullptr || p.n_requests < (int64_t)1024 * p.n_scenarios;
     const size_t lds = (size_t)(bd_lds ? 2 : 1) * p.H * sizeof(int32_t);
-    const void* kern = bd_lds ? (const void*)project_kernel<true> : (const void*)project_kernel<false>;
+    // block sizes that are powers of two up to 64 take shifts instead of
+    // divisions in the admission loops
+    const bool pow2 = p.N <= kWave && (p.N & (p.N - 1)) == 0;
+    void (*const kern)(ProjectParams) = bd_lds ? (pow2 ? project_kernel<true, true> : project_kernel<true, false>)
+                                               : (pow2 ? project_kernel<false, true> : project_kernel<false, false>);
     if (lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
-    if (bd_lds)
-        hipLaunchKernelGGL(project_kernel<true>, dim3((unsigned)p.n_scenarios), dim3(64), lds, stream, p);
-    else
-        hipLaunchKernelGGL(project_kernel<false>, dim3((unsigned)p.n_scenarios), dim3(64), lds, stream, p);
+    hipLaunchKernelGGL(kern, dim3((unsigned)p.n_scenarios), dim3(64), lds, stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !p.rows) return e;
     const int64_t blocks = p.n_scenarios * ((p.H + kRowsThreads - 1) / kRowsThreads);
