@@ -15,11 +15,11 @@
 // room for only two trees per block).  Leaves are accumulated in fp64 in tree
 // order and rounded once, as everywhere in the library.
 //
-// On horizons of at least 512 iterations and grids of at least one
-// workgroup per CU, forest_column_reuse_kernel gives each lane 8
-// consecutive iterations instead and reuses leaves along them (the grid
-// kernel's box test, per lane), unless the wavefront's batch changes on
-// most row-to-row steps.
+// On horizons of at least 64 x RPL iterations and grids of at least one
+// workgroup per CU, forest_column_reuse_kernel gives each lane RPL (16, else
+// 8) consecutive iterations instead and reuses leaves along them: every lane
+// walks its first and last row, and the rows in between take those leaves
+// where their boxes hold them (the grid kernel's box test, per lane).
 //
 // Forests too deep for LDS records are walked from global memory.
 //
@@ -190,76 +190,115 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
         if (o[r] >= 0) P.out[o[r]] = (float)acc[r];
 }
 
-// Leaf reuse along a lane's rows: a lane takes RPL consecutive iterations of
-// the scenario and keeps, for NT (1 or 2) consecutive staged trees, the
-// values of the leaves its last walks reached, their KV / batch boxes and
-// the intersection of the boxes (a row inside it reaches the same leaves:
-// the frequency and engine size are the scenario's).  A row outside walks
-// only the tree(s) whose own box it left, both in one interleaved pass when
-// the wavefront needs both.
-template <int NF, int NT, int RPL>
-__device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayout& R, int32_t depth, float xf,
-                                                 const float (&kv)[RPL], const float (&bs)[RPL], float xe,
-                                                 double (&acc)[RPL]) {
-    const uint32_t tree1 = tree + R.bytes;
-    float4 box = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
-    float4 b0 = box, b1 = box;   // the trees' own leaf boxes, decoded
-    double v[NT];
+// Leaf indices k[r][t] of NR rows (one frequency and engine size) through NT
+// consecutive staged trees, all NR x NT chains of dependent LDS reads
+// interleaved.
+template <int NF, int NT, int NR>
+__device__ __forceinline__ void walk_rows(uint32_t tree, uint32_t rec_bytes, int32_t depth, float xf,
+                                          const float (&kv)[NR], const float (&bs)[NR], float xe,
+                                          int32_t (&k)[NR][NT]) {
+    uint32_t a[NR][NT], cl[NT], cr[NT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) v[t] = 0.0;
+    for (int t = 0; t < NT; ++t) {
+        const uint32_t root = tree + t * rec_bytes;
+        cl[t] = 16u - root;
+        cr[t] = 32u - root;
+        asm volatile("" : "+v"(cl[t]), "+v"(cr[t]));
+#pragma unroll
+        for (int r = 0; r < NR; ++r) a[r][t] = root;
+    }
+    for (int32_t level = 0; level < depth; ++level) {
+        uint4 w[NR][NT];
+#pragma unroll
+        for (int r = 0; r < NR; ++r)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) w[r][t] = read_node(a[r][t]);
+#pragma unroll
+        for (int r = 0; r < NR; ++r)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const bool left = node_feature<NF>(w[r][t], xf, kv[r], bs[r], xe) < __uint_as_float(w[r][t].x);
+                a[r][t] = 2u * a[r][t] + (left ? cl[t] : cr[t]);
+            }
+    }
+    const int32_t n_int = (1 << depth) - 1;
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) k[r][t] = (int32_t)((a[r][t] - (tree + t * rec_bytes)) >> 4) - n_int;
+}
+
+// Leaf reuse along a lane's RPL consecutive rows with two anchors: every lane
+// walks its first and last row through NT (1 or 2) consecutive staged trees in
+// one interleaved pass (full wavefronts), keeps those leaves' values and KV /
+// batch boxes, and gives every row in between the value of an anchor leaf
+// whose box holds it (the frequency and engine size are the scenario's, so a
+// row inside a leaf's box reaches that leaf), or of the leaf of the lane's
+// last walk in between.  Only rows in none of these boxes walk, the trees
+// they need, both in one pass when the wavefront needs both.
+template <int NF, int NT, int RPL>
+__device__ __forceinline__ void add_leaves_anchored(uint32_t tree, const RecordLayout& R, int32_t depth, float xf,
+                                                    const float (&kv)[RPL], const float (&bs)[RPL], float xe,
+                                                    double (&acc)[RPL]) {
+    float va[2][NT];
+    float4 ba[2][NT];
+    {
+        const float kva[2] = {kv[0], kv[RPL - 1]}, bsa[2] = {bs[0], bs[RPL - 1]};
+        int32_t ka[2][NT];
+        walk_rows<NF, NT, 2>(tree, R.bytes, depth, xf, kva, bsa, xe, ka);
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                va[e][t] = leaf_value(tree + t * R.bytes, ka[e][t]);
+                ba[e][t] = leaf_box(tree + t * R.bytes, R, ka[e][t]);
+            }
+    }
+    float vl[NT];
+    float4 bl[NT];   // the last walk's leaf (none yet: empty box)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        vl[t] = 0.0f;
+        bl[t] = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
+    }
 #pragma unroll
     for (int r = 0; r < RPL; ++r) {
-        if (r == 0) {
-            // first row: every tree, every lane
-            int32_t k[NT];
-            walk<NF, NT>(tree, R.bytes, depth, xf, kv[0], bs[0], xe, k);
-            v[0] = (double)leaf_value(tree, k[0]);
-            b0 = leaf_box(tree, R, k[0]);
-            box = b0;
-            if (NT == 2) {
-                v[NT - 1] = (double)leaf_value(tree1, k[NT - 1]);
-                b1 = leaf_box(tree1, R, k[NT - 1]);
-                box = box_meet(b0, b1);
+        float v[NT];
+        if (r == 0 || r == RPL - 1) {
+#pragma unroll
+            for (int t = 0; t < NT; ++t) v[t] = va[r == 0 ? 0 : 1][t];
+        } else {
+            bool need[NT];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const bool in0 = in_box(ba[0][t], kv[r], bs[r]);
+                const bool in1 = in_box(ba[1][t], kv[r], bs[r]);
+                need[t] = !in0 && !in1 && !in_box(bl[t], kv[r], bs[r]);
+                v[t] = in0 ? va[0][t] : (in1 ? va[1][t] : vl[t]);
             }
-        } else if (!in_box(box, kv[r], bs[r])) {
-            if (NT == 1) {
-                int32_t k[1];
-                walk<NF, 1>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
-                v[0] = (double)leaf_value(tree, k[0]);
-                box = leaf_box(tree, R, k[0]);
+            if (NT == 2 && __builtin_amdgcn_ballot_w64(need[0]) != 0 &&
+                __builtin_amdgcn_ballot_w64(need[NT - 1]) != 0) {
+                int32_t k[NT];
+                walk<NF, NT>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    if (need[t]) {
+                        v[t] = vl[t] = leaf_value(tree + t * R.bytes, k[t]);
+                        bl[t] = leaf_box(tree + t * R.bytes, R, k[t]);
+                    }
             } else {
-                const bool n0 = !in_box(b0, kv[r], bs[r]);
-                const bool n1 = !in_box(b1, kv[r], bs[r]);
-                if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
-                    int32_t k[2];
-                    walk<NF, 2>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
-                    if (n0) {
-                        v[0] = (double)leaf_value(tree, k[0]);
-                        b0 = leaf_box(tree, R, k[0]);
-                    }
-                    if (n1) {
-                        v[NT - 1] = (double)leaf_value(tree1, k[1]);
-                        b1 = leaf_box(tree1, R, k[1]);
-                    }
-                } else {
-                    if (n0) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    if (need[t]) {
                         int32_t k[1];
-                        walk<NF, 1>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
-                        v[0] = (double)leaf_value(tree, k[0]);
-                        b0 = leaf_box(tree, R, k[0]);
+                        walk<NF, 1>(tree + t * R.bytes, R.bytes, depth, xf, kv[r], bs[r], xe, k);
+                        v[t] = vl[t] = leaf_value(tree + t * R.bytes, k[0]);
+                        bl[t] = leaf_box(tree + t * R.bytes, R, k[0]);
                     }
-                    if (n1) {
-                        int32_t k[1];
-                        walk<NF, 1>(tree1, R.bytes, depth, xf, kv[r], bs[r], xe, k);
-                        v[NT - 1] = (double)leaf_value(tree1, k[0]);
-                        b1 = leaf_box(tree1, R, k[0]);
-                    }
-                }
-                box = box_meet(b0, b1);
             }
         }
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc[r] += v[t];
+        for (int t = 0; t < NT; ++t) acc[r] += (double)v[t];
         asm volatile("" ::"v"(acc[r]));
     }
 }
@@ -267,10 +306,6 @@ __device__ __forceinline__ void add_leaves_reuse(uint32_t tree, const RecordLayo
 // M at one frequency per scenario with leaf reuse along each lane's RPL
 // consecutive iterations (a wavefront takes 64 x RPL consecutive
 // iterations of one scenario); staging as in forest_column_lds_kernel.
-// Reuse pays where the rows move slowly; a wavefront whose batch changes
-// on more than half of its row-to-row steps (arrivals and completions at
-// most iterations) walks every row instead, four rows x two trees
-// interleaved, as forest_column_lds_kernel does.
 template <int NF, int RPL>
 __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const uint4* __restrict__ records,
                                                                          int32_t n_trees, int32_t depth,
@@ -300,12 +335,6 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
         asm volatile("" ::"v"(kv[r]), "v"(bs[r]));
     }
     asm volatile("" ::"v"(xf), "v"(xe));
-    // how often the batch changes from one row to the next, over the wavefront
-    int32_t steps_changed = 0;
-#pragma unroll
-    for (int r = 1; r < RPL; ++r) steps_changed += __builtin_popcountll(__builtin_amdgcn_ballot_w64(bs[r] != bs[r - 1]));
-    const bool reuse = 2 * steps_changed <= kWave * (RPL - 1);   // wavefront-uniform
-    static_assert(RPL % 4 == 0, "the walk-every-row path takes four rows at a time");
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
     if (n_blocks > 0) stage_block(records, n_trees, tb, rec_words, 0, lds_addr(smem), wave, kColWaves);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -318,25 +347,9 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
             const int32_t cnt = min(tb, n_trees - b * tb);
             const uint32_t first = lds_addr(smem) + cur * buf_bytes;
             int32_t t = 0;
-            if (reuse) {
-                for (; t + 2 <= cnt; t += 2)
-                    add_leaves_reuse<NF, 2, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
-                if (t < cnt) add_leaves_reuse<NF, 1, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
-            } else {
-                const float xf4[4] = {xf, xf, xf, xf}, xe4[4] = {xe, xe, xe, xe};
-#pragma unroll
-                for (int h = 0; h < RPL / 4; ++h) {
-                    const float kv4[4] = {kv[4 * h], kv[4 * h + 1], kv[4 * h + 2], kv[4 * h + 3]};
-                    const float bs4[4] = {bs[4 * h], bs[4 * h + 1], bs[4 * h + 2], bs[4 * h + 3]};
-                    double a4[4] = {acc[4 * h], acc[4 * h + 1], acc[4 * h + 2], acc[4 * h + 3]};
-                    int32_t u = 0;
-                    for (; u + 2 <= cnt; u += 2)
-                        add_leaves<NF, 2, 4>(first + u * R.bytes, R.bytes, depth, xf4, kv4, bs4, xe4, a4);
-                    if (u < cnt) add_leaves<NF, 1, 4>(first + u * R.bytes, R.bytes, depth, xf4, kv4, bs4, xe4, a4);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[4 * h + i] = a4[i];
-                }
-            }
+            for (; t + 2 <= cnt; t += 2)
+                add_leaves_anchored<NF, 2, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
+            if (t < cnt) add_leaves_anchored<NF, 1, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
@@ -402,34 +415,40 @@ hipError_t launch_column_lds(const ForestDev& f, const ColumnParams& c, int32_t 
     return hipGetLastError();
 }
 
-#ifndef TL_COLUMN_REUSE_RPL
-#define TL_COLUMN_REUSE_RPL 8
-#endif
+// Launches forest_column_reuse_kernel<NF, RPL> when the horizon fills a
+// wavefront's 64 x RPL rows and the grid gives every CU a workgroup;
+// returns false (nothing launched) otherwise.
+template <int NF, int RPL>
+bool launch_column_reuse(const ForestDev& f, const ColumnParams& c, int32_t tb, size_t lds, int cus,
+                         hipStream_t stream, hipError_t* err) {
+    const int64_t items = c.S * ((c.H + kWave * RPL - 1) / (kWave * RPL));
+    if (c.H < kWave * RPL || items < (int64_t)kColWaves * cus) return false;
+    if (!grid_fits((items + kColWaves - 1) / kColWaves)) {
+        *err = hipErrorInvalidConfiguration;
+        return true;
+    }
+    const auto kern = forest_column_reuse_kernel<NF, RPL>;
+    *err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (*err != hipSuccess) return true;
+    hipLaunchKernelGGL(kern, dim3((unsigned)((items + kColWaves - 1) / kColWaves)), dim3(kColThreads), lds, stream,
+                       f.records, f.n_trees, f.depth, tb, f.base_score, c);
+    *err = hipGetLastError();
+    return true;
+}
 
 template <int NF>
 hipError_t launch_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream) {
     size_t lds = 0;
     const int32_t tb = column_trees_per_block(f, &lds);
-    if constexpr (TL_COLUMN_REUSE_RPL > 0) {
-        // leaf reuse along RPL consecutive rows a lane, on horizons that
-        // fill a wavefront's 64 x RPL rows and grids that still give every
-        // CU a workgroup (the reuse kernel has half the wavefronts)
-        constexpr int RPL = TL_COLUMN_REUSE_RPL;
-        const int64_t items = c.S * ((c.H + kWave * RPL - 1) / (kWave * RPL));
+    if (tb > 0) {
+        // leaf reuse along 16 (else 8) consecutive rows a lane where the grid
+        // still gives every CU a workgroup
         int dev = 0, cus = 0;
-        hipError_t e0 = hipGetDevice(&dev);
-        if (e0 == hipSuccess) e0 = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-        if (e0 != hipSuccess) return e0;
-        if (tb > 0 && c.H >= kWave * RPL && items >= (int64_t)kColWaves * cus) {
-            if (!grid_fits((items + kColWaves - 1) / kColWaves)) return hipErrorInvalidConfiguration;
-            const auto kern = forest_column_reuse_kernel<NF, RPL>;
-            const hipError_t e =
-                hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (e != hipSuccess) return e;
-            hipLaunchKernelGGL(kern, dim3((unsigned)((items + kColWaves - 1) / kColWaves)), dim3(kColThreads), lds,
-                               stream, f.records, f.n_trees, f.depth, tb, f.base_score, c);
-            return hipGetLastError();
-        }
+        hipError_t e = hipGetDevice(&dev);
+        if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        if (launch_column_reuse<NF, 16>(f, c, tb, lds, cus, stream, &e)) return e;
+        if (launch_column_reuse<NF, 8>(f, c, tb, lds, cus, stream, &e)) return e;
     }
     if (tb > 0) {
         // rows per lane: enough chains to overlap, without idle stripes on

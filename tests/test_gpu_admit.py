@@ -155,14 +155,14 @@ def test_admit_scaled_configs(gpu, ci, over):
     check_admit(inp, inp["forest"], float(inp["freqs_mhz"][-1]), cand, cfg["name"])
 
 
-@pytest.mark.parametrize("ci,S", [(3, 2048), (4, 1024)])
+@pytest.mark.parametrize("ci,S", [(3, 2048), (3, 4096), (4, 1024), (4, 2048)])
 def test_admit_model_at_reuse_sizes(gpu, ci, S):
     """Grids large enough for the column kernel with leaf reuse along each
-    lane's rows: c3's slowly changing rows take its reuse path, c4's batch
-    (arrivals and completions at most iterations) its walk-every-row path.
-    The model at the maximum frequency equals the oracle's on every
-    iteration of the projection the GPU returned (the projection itself is
-    checked against the oracle in the tests above)."""
+    lane's rows, 8 rows a lane (the smaller grids) and 16: c3's slowly
+    changing rows and c4's batch that changes at most iterations (arrivals
+    and completions).  The model at the maximum frequency equals the
+    oracle's on every iteration of the projection the GPU returned (the
+    projection itself is checked against the oracle in the tests above)."""
     cfg = synth.scaled(configs.get_config(ci), n_scenarios=S, forest_n_trees=60)
     inp = synth.make_inputs(cfg)
     cand = synth.make_candidates(cfg, inp)

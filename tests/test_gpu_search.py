@@ -91,12 +91,13 @@ def test_binary_search_random(gpu, S, F, H, T, d, nf, mono, seed):
     assert len(set(st.tolist())) >= 2
 
 
-@pytest.mark.parametrize("S,H", [(4096, 512), (2048, 1000)])
+@pytest.mark.parametrize("S,H", [(4096, 512), (2048, 1000), (4096, 1100)])
 def test_binary_search_at_reuse_sizes(gpu, S, H):
     """Grids large enough for the column kernel with leaf reuse along each
-    lane's rows (a whole and a ragged last wavefront of iterations); half of
-    the scenarios have a batch that changes at every iteration, which takes
-    that kernel's walk-every-row path.  Indices and statuses equal the
+    lane's rows: 8 rows a lane (a whole and a ragged last wavefront of
+    iterations) and 16 rows a lane (ragged).  Half of the scenarios have a
+    batch that changes at every iteration, so many rows lie outside both
+    anchor leaves' boxes and walk.  Indices and statuses equal the
     oracle's."""
     rng = np.random.default_rng(777 + H)
     F, T, d, nf = 5, 20, 6, 4
