@@ -148,7 +148,8 @@ def test_project_many_requests(gpu, H, N, seed, rmax, qfrac):
 
 
 @pytest.mark.parametrize("H,N,seed", [(1, 16, 0), (7, 1, 1), (64, 16, 2), (100, 3, 3), (513, 16, 4),
-                                      (1000, 64, 5), (257, 100, 6), (2048, 16, 7), (130, 7, 8)])
+                                      (1000, 64, 5), (257, 100, 6), (2048, 16, 7), (130, 7, 8),
+                                      (600, 128, 9)])
 def test_project_random_boards(gpu, H, N, seed):
     rng = np.random.default_rng(seed)
     inp = random_boards(rng, 300, H, N, unsorted=(seed % 2 == 1))
