@@ -71,14 +71,15 @@ __device__ __forceinline__ float column_freq(const ColumnParams& P, int64_t s) {
     return P.fidx ? P.freqs[max(P.fidx[s], 0)] : P.freq;
 }
 
-// Walks NT consecutive staged trees (records rec_bytes apart, the first at
-// LDS byte address `tree`) for the RPL rows of a lane, all RPL x NT chains
-// interleaved, and adds the leaves to each row's sum in tree order.
-template <int NF, int NT, int RPL>
-__device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, int32_t depth,
-                                           const float (&xf)[RPL], const float (&kv)[RPL], const float (&bs)[RPL],
-                                           const float (&xe)[RPL], double (&acc)[RPL]) {
-    uint32_t a[RPL][NT], cl[NT], cr[NT];
+// Leaf indices k[r][t] of NR rows (each with its own features) through NT
+// consecutive staged trees (records rec_bytes apart, the first at LDS byte
+// address `tree`), all NR x NT chains of dependent LDS reads interleaved:
+// every chain's node reads issue back to back, then the compares.
+template <int NF, int NT, int NR>
+__device__ __forceinline__ void walk_rows(uint32_t tree, uint32_t rec_bytes, int32_t depth, const float (&xf)[NR],
+                                          const float (&kv)[NR], const float (&bs)[NR], const float (&xe)[NR],
+                                          int32_t (&k)[NR][NT]) {
+    uint32_t a[NR][NT], cl[NT], cr[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
         const uint32_t root = tree + t * rec_bytes;
@@ -86,32 +87,41 @@ __device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, in
         cr[t] = 32u - root;
         asm volatile("" : "+v"(cl[t]), "+v"(cr[t]));
 #pragma unroll
-        for (int r = 0; r < RPL; ++r) a[r][t] = root;
+        for (int r = 0; r < NR; ++r) a[r][t] = root;
     }
     for (int32_t level = 0; level < depth; ++level) {
-        uint4 w[RPL][NT];
+        uint4 w[NR][NT];
 #pragma unroll
-        for (int r = 0; r < RPL; ++r)
+        for (int r = 0; r < NR; ++r)
 #pragma unroll
             for (int t = 0; t < NT; ++t) w[r][t] = read_node(a[r][t]);
 #pragma unroll
-        for (int r = 0; r < RPL; ++r)
+        for (int r = 0; r < NR; ++r)
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                const uint4& nd = w[r][t];
-                const bool left = node_feature<NF>(nd, xf[r], kv[r], bs[r], xe[r]) < __uint_as_float(nd.x);
+                const bool left = node_feature<NF>(w[r][t], xf[r], kv[r], bs[r], xe[r]) < __uint_as_float(w[r][t].x);
                 a[r][t] = 2u * a[r][t] + (left ? cl[t] : cr[t]);
             }
     }
     const int32_t n_int = (1 << depth) - 1;
 #pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) k[r][t] = (int32_t)((a[r][t] - (tree + t * rec_bytes)) >> 4) - n_int;
+}
+
+// Walks NT consecutive staged trees for the RPL rows of a lane and adds the
+// leaves to each row's sum in tree order.
+template <int NF, int NT, int RPL>
+__device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, int32_t depth,
+                                           const float (&xf)[RPL], const float (&kv)[RPL], const float (&bs)[RPL],
+                                           const float (&xe)[RPL], double (&acc)[RPL]) {
+    int32_t k[RPL][NT];
+    walk_rows<NF, NT, RPL>(tree, rec_bytes, depth, xf, kv, bs, xe, k);
+#pragma unroll
     for (int r = 0; r < RPL; ++r)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const uint32_t root = tree + t * rec_bytes;
-            const int32_t k = (int32_t)((a[r][t] - root) >> 4) - n_int;
-            acc[r] += (double)leaf_value(root, k);
-        }
+        for (int t = 0; t < NT; ++t) acc[r] += (double)leaf_value(tree + t * rec_bytes, k[r][t]);
 }
 
 template <int NF, int RPL, bool ROWS>
@@ -190,44 +200,6 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
         if (o[r] >= 0) P.out[o[r]] = (float)acc[r];
 }
 
-// Leaf indices k[r][t] of NR rows (one frequency and engine size) through NT
-// consecutive staged trees, all NR x NT chains of dependent LDS reads
-// interleaved.
-template <int NF, int NT, int NR>
-__device__ __forceinline__ void walk_rows(uint32_t tree, uint32_t rec_bytes, int32_t depth, float xf,
-                                          const float (&kv)[NR], const float (&bs)[NR], float xe,
-                                          int32_t (&k)[NR][NT]) {
-    uint32_t a[NR][NT], cl[NT], cr[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        const uint32_t root = tree + t * rec_bytes;
-        cl[t] = 16u - root;
-        cr[t] = 32u - root;
-        asm volatile("" : "+v"(cl[t]), "+v"(cr[t]));
-#pragma unroll
-        for (int r = 0; r < NR; ++r) a[r][t] = root;
-    }
-    for (int32_t level = 0; level < depth; ++level) {
-        uint4 w[NR][NT];
-#pragma unroll
-        for (int r = 0; r < NR; ++r)
-#pragma unroll
-            for (int t = 0; t < NT; ++t) w[r][t] = read_node(a[r][t]);
-#pragma unroll
-        for (int r = 0; r < NR; ++r)
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const bool left = node_feature<NF>(w[r][t], xf, kv[r], bs[r], xe) < __uint_as_float(w[r][t].x);
-                a[r][t] = 2u * a[r][t] + (left ? cl[t] : cr[t]);
-            }
-    }
-    const int32_t n_int = (1 << depth) - 1;
-#pragma unroll
-    for (int r = 0; r < NR; ++r)
-#pragma unroll
-        for (int t = 0; t < NT; ++t) k[r][t] = (int32_t)((a[r][t] - (tree + t * rec_bytes)) >> 4) - n_int;
-}
-
 // Leaf reuse along a lane's RPL consecutive rows with two anchors: every lane
 // walks its first and last row through NT (1 or 2) consecutive staged trees in
 // one interleaved pass (full wavefronts), keeps those leaves' values and KV /
@@ -243,9 +215,10 @@ __device__ __forceinline__ void add_leaves_anchored(uint32_t tree, const RecordL
     float va[2][NT];
     float4 ba[2][NT];
     {
-        const float kva[2] = {kv[0], kv[RPL - 1]}, bsa[2] = {bs[0], bs[RPL - 1]};
+        const float xfa[2] = {xf, xf}, kva[2] = {kv[0], kv[RPL - 1]}, bsa[2] = {bs[0], bs[RPL - 1]},
+                    xea[2] = {xe, xe};
         int32_t ka[2][NT];
-        walk_rows<NF, NT, 2>(tree, R.bytes, depth, xf, kva, bsa, xe, ka);
+        walk_rows<NF, NT, 2>(tree, R.bytes, depth, xfa, kva, bsa, xea, ka);
 #pragma unroll
         for (int e = 0; e < 2; ++e)
 #pragma unroll
