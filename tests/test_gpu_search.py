@@ -140,3 +140,35 @@ def test_binary_search_scaled_configs(gpu, ci, over):
     o = oracle.end_to_end(inp)
     oi, os_ = oracle.select_binary(o["ips"], o["deadline_at"], o["n_iters"], inp["tbt_slo_ns"], o["flags"])
     assert np.array_equal(_np(idx), oi) and np.array_equal(_np(st).view(np.uint32), os_)
+
+
+# (config, scenarios compared with the oracle at full size)
+PLAN_FULL = {1: [0, 1023], 3: [0, 1, 4095], 4: [0, 16383]}
+
+
+@pytest.mark.parametrize("ci", sorted(PLAN_FULL), ids=[configs.CONFIGS[c]["name"] for c in sorted(PLAN_FULL)])
+def test_binary_search_full_size(gpu, ci):
+    """The binary search at a workload's full size, in the configuration the
+    benchmark times (the column kernel with leaf reuse at every probe):
+    sampled scenarios' indices and statuses equal the oracle's binary search
+    over its model at every frequency.  The oracle runs in threads (its C
+    calls release the interpreter lock)."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+    import torch
+    from paper_2408_05235_amd import api
+    cfg = configs.get_config(ci)
+    inp = synth.make_inputs(cfg)
+    ctl = api.Controller(api.upload(inp), api.Forest.from_dict(inp["forest"]))
+    ctl.project()
+    idx, st = ctl.select_binary()
+    torch.cuda.synchronize()
+    idx, st = _np(idx), _np(st).view(np.uint32)
+
+    def run(s):
+        sub = synth.subset(inp, [s])
+        o = oracle.end_to_end(sub)
+        return s, oracle.select_binary(o["ips"], o["deadline_at"], o["n_iters"], sub["tbt_slo_ns"], o["flags"])
+    with ThreadPoolExecutor(max(1, min(16, len(os.sched_getaffinity(0))))) as ex:
+        for s, (oi, os_) in ex.map(run, PLAN_FULL[ci]):
+            assert int(idx[s]) == int(oi[0]) and int(st[s]) == int(os_[0]), (cfg["name"], s, idx[s], st[s], oi, os_)
