@@ -232,7 +232,7 @@ tl_status tl_forest_predict(const tl_forest* forest, const float* rows, int64_t 
  * features in the order (frequency, KV, batch[, engine size]).
  * 1 <= F <= TL_MAX_FREQS, 1 <= H <= TL_MAX_HORIZON.
  * Work is ordered by an estimate of its cost (results do not depend on the
- * order).  The ordering needs 16 bytes per (scenario, 32-iteration chunk)
+ * order).  The ordering needs 16 bytes per (scenario, 44-iteration chunk)
  * plus a radix sort's temporary storage of device scratch, which the forest
  * handle owns: it is allocated
  * on the first call, kept, and replaced only when a larger grid comes, so
@@ -252,9 +252,10 @@ tl_status tl_forest_predict_grid(const tl_forest* forest, int64_t n_scenarios, i
  * (code under stream capture, tight serving loops, hosts that forbid
  * allocation): same arguments, same results, no allocation of any kind.
  * The work order's scratch is a fixed 32 MiB array of the library on each
- * device (taken when the library is loaded); enough for 1,048,576
- * (scenario, 32-iteration chunk) pairs, e.g. 16384 scenarios x 2048
- * iterations.  A grid whose order needs more returns TL_EUNSUPPORTED and
+ * device (taken when the library is loaded): 16 bytes per (scenario,
+ * 44-iteration chunk) pair plus the sort's temporary storage must fit, as
+ * they do for 16384 scenarios x 2048 iterations (770,048 pairs) but not for
+ * 65536 x 1024.  A grid whose order needs more returns TL_EUNSUPPORTED and
  * enqueues nothing.  Every call on one device shares that array: calls that
  * overlap on one device (concurrent streams, other threads) race and must
  * be serialized by the caller; tl_forest_predict_grid does not use it.
