@@ -360,27 +360,25 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
     // the J (KV, batch) pairs of this wavefront are the same for every lane;
     // they sit in LDS after the two tree buffers and are read as broadcasts
     float2* kvb = (float2*)(smem + 2 * buf_bytes) + wave * J;
+    StageSync* sync = (StageSync*)(smem + 2 * buf_bytes + (size_t)kLdsWaves * J * sizeof(float2));
+    if (threadIdx.x == 0) stage_sync_init(sync);
     if (lane < J) {
         const int32_t j = g.j0 + min(lane, g.nj - 1);
         kvb[lane] = make_float2((float)P.kv[g.s * H + j], (float)P.batch[g.s * H + j]);
     }
 
-    // staging (stage_block): the copy of the next block runs while the
-    // current one is evaluated and is waited for (vmcnt) before the block
-    // barrier.
+    // staging: block 0 by every wavefront before the barrier, the others
+    // handed over without barriers (stage_acquire / stage_release)
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
     double acc[J];
 #pragma unroll
     for (int jj = 0; jj < J; ++jj) acc[jj] = (double)base;
-    auto stage = [&](int32_t b, int buf) {
-        stage_block(records, n_trees, tb, rec_words, b, lds_addr(smem + buf * buf_bytes), wave, kLdsWaves);
-    };
 
     // Make the lane's frequency / engine size complete here, before any
     // staging copy is in flight: otherwise the walks inside the loop would
-    // each wait for all outstanding copies, including the prefetch.
+    // each wait for all outstanding copies.
     asm volatile("" ::"v"(xf), "v"(xe));
-    if (n_blocks > 0) stage(0, 0);
+    if (n_blocks > 0) stage_block(records, n_trees, tb, rec_words, 0, lds_addr(smem), wave, kLdsWaves);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     // per row group, the (KV, batch) hull of its rows (wavefront-uniform)
@@ -402,9 +400,12 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
         hull[gi][2] = to_sgpr(blo);
         hull[gi][3] = to_sgpr(bhi);
     }
+    bool sync_ok = true;
     for (int32_t b = 0; b < n_blocks; ++b) {
         const int cur = b & 1;
-        if (b + 1 < n_blocks) stage(b + 1, cur ^ 1);
+        if (b > 0)
+            sync_ok &= stage_acquire(sync, b, kLdsWaves, records, n_trees, tb, rec_words,
+                                     lds_addr(smem + cur * buf_bytes));
         if (g.valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
             const uint32_t bp = cur * buf_bytes;
@@ -417,14 +418,13 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
                 eval_trees<NF, J, 2>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
             if (tt < cnt) eval_trees<NF, J, 1>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
         }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
+        stage_release(sync, b);
     }
     if (active) {
         float* o = P.out + ((int64_t)g.s * F + g.f) * H + g.j0;
 #pragma unroll
         for (int jj = 0; jj < J; ++jj)
-            if (jj < g.nj) o[jj] = (float)acc[jj];
+            if (jj < g.nj) o[jj] = sync_ok ? (float)acc[jj] : __builtin_nanf("");
     }
 }
 
@@ -513,7 +513,7 @@ hipError_t launch_nf(const ForestDev& f, const float* rows, int64_t n_rows, floa
 int32_t lds_trees_per_block(const ForestDev& f, size_t* lds_bytes) {
     if (!f.records || f.depth > kMaxRecordDepth) return 0;
     const RecordLayout R = record_layout(f.depth);
-    const size_t head = (size_t)kLdsWaves * kLdsJ * sizeof(float2);
+    const size_t head = (size_t)kLdsWaves * kLdsJ * sizeof(float2) + sizeof(StageSync);
     const size_t budget = (size_t)TL_LDS_BUDGET_KIB * 1024;
     auto fits = [&](int32_t tb) { return 2 * (size_t)stage_buffer_bytes(tb, R) + head <= budget; };
     int32_t tb = 64;

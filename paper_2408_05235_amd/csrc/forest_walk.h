@@ -68,10 +68,10 @@ __device__ __forceinline__ float4 leaf_box(uint32_t tree, const RecordLayout& R,
 }
 
 // Staging of tree blocks: block b is trees [b*tb, b*tb + cnt), one
-// contiguous range of 16-byte words in global memory and in LDS.  The
-// wavefronts of a workgroup copy it in pieces of 64 lanes x 16 bytes
-// straight from global memory into LDS (global_load_lds_dwordx4, no
-// registers), wavefront w of n taking pieces w, w + n, ...  Lanes past the
+// contiguous range of 16-byte words in global memory and in LDS.  It is
+// copied in pieces of 64 lanes x 16 bytes straight from global memory into
+// LDS (global_load_lds_dwordx4, no registers), wavefront w of n taking
+// pieces w, w + n, ... (n = 1: one wavefront copies it all).  Lanes past the
 // block's last word copy its first word into the buffer's padding (buffers
 // are whole pieces), so no lane writes outside its buffer.
 constexpr uint32_t kStagePiece = kWave * 16;
@@ -84,8 +84,9 @@ __host__ __device__ inline uint32_t stage_buffer_bytes(int32_t tb, const RecordL
 // lds + 16 l (lds the same in every lane).  Issued as an instruction the
 // compiler does not track, so it does not make the evaluation's LDS reads
 // wait for the copy (they read other buffers); a kernel waits for its copies
-// (vmcnt) before the block barrier that hands the buffer over, and has no
-// other vector-memory load in flight inside its block loop.
+// (vmcnt) before it hands the buffer over (a workgroup barrier, or
+// publishing `ready` in stage_acquire), and has no other vector-memory load
+// in flight inside its block loop.
 __device__ __forceinline__ void stage_piece(const uint4* src, uint32_t lds) {
     const uint32_t base = __builtin_amdgcn_readfirstlane(lds);   // wavefront-uniform by construction
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(base), "v"(src) : "memory", "m0");
@@ -102,6 +103,80 @@ __device__ __forceinline__ void stage_block(const uint4* records, int32_t n_tree
         const uint32_t i = pc * kWave + lane_id();
         stage_piece(src + (i < words ? i : 0u), dst + pc * kStagePiece);
     }
+}
+
+// Hand-over of two LDS buffers of tree blocks between the wavefronts of a
+// workgroup without block barriers.  Block b lives in buffer b & 1; block 0
+// is copied by every wavefront before the workgroup's one barrier.  Per
+// buffer: `claimed` = the last block a wavefront took on to copy into it,
+// `ready` = the last block whose copy is complete, `done` = how many
+// (wavefront, block) pairs have finished with it.  The first wavefront that
+// needs block b and finds it unclaimed claims it, waits until every
+// wavefront has finished block b - 2 (the buffer's previous occupant),
+// copies the whole block, waits for its copy and publishes `ready`; the others
+// wait for `ready`.  A wavefront can thus run up to a block ahead of the
+// slowest one instead of meeting it at every block.  Every wait is bounded
+// (kSyncSpins sleeps); one that runs out makes stage_acquire return false,
+// and the caller marks its results invalid, so every wavefront ends.
+struct StageSync {
+    int32_t claimed[2];
+    int32_t ready[2];
+    int32_t done[2];
+};
+constexpr int32_t kSyncSpins = 1 << 20;
+
+__device__ __forceinline__ void stage_sync_init(StageSync* sync) {
+    sync->claimed[0] = 0;   // block 0: copied by every wavefront
+    sync->ready[0] = 0;
+    sync->claimed[1] = -1;
+    sync->ready[1] = -1;
+    sync->done[0] = 0;
+    sync->done[1] = 0;
+}
+
+__device__ __forceinline__ int32_t sync_load(const int32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// Makes block b >= 1 (trees [b*tb, ...), rec_words 16-byte words per tree)
+// available in its buffer at LDS byte address buf; n_waves wavefronts share
+// the buffers.
+__device__ __forceinline__ bool stage_acquire(StageSync* sync, int32_t b, int n_waves, const uint4* records,
+                                              int32_t n_trees, int32_t tb, uint32_t rec_words, uint32_t buf) {
+    const int cur = b & 1;
+    const int32_t need_done = n_waves * (b >> 1);
+    int32_t spins = 0;
+    while (sync_load(&sync->ready[cur]) != b && spins < kSyncSpins) {
+        int32_t won = 0;
+        if (sync_load(&sync->claimed[cur]) == b - 2) {
+            if (lane_id() == 0) {
+                int32_t expect = b - 2;
+                won = __hip_atomic_compare_exchange_strong(&sync->claimed[cur], &expect, b, __ATOMIC_ACQ_REL,
+                                                           __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+            won = __builtin_amdgcn_readfirstlane(won);
+        }
+        if (won) {
+            while (sync_load(&sync->done[cur]) < need_done && spins < kSyncSpins) {
+                __builtin_amdgcn_s_sleep(1);
+                ++spins;
+            }
+            stage_block(records, n_trees, tb, rec_words, b, buf, 0, 1);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            if (lane_id() == 0) __hip_atomic_store(&sync->ready[cur], b, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        ++spins;
+    }
+    return spins < kSyncSpins;
+}
+
+// This wavefront has finished with block b (its reads have all returned).
+__device__ __forceinline__ void stage_release(StageSync* sync, int32_t b) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (lane_id() == 0)
+        __hip_atomic_fetch_add(&sync->done[b & 1], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // Walks NT consecutive staged trees (records rec_bytes apart, the first at
