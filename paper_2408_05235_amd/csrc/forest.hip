@@ -418,7 +418,7 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
                 eval_trees<NF, J, 2>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
             if (tt < cnt) eval_trees<NF, J, 1>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
         }
-        stage_release(sync, b);
+        stage_release(sync, b, kLdsWaves);
     }
     if (active) {
         float* o = P.out + ((int64_t)g.s * F + g.f) * H + g.j0;

@@ -115,9 +115,14 @@ __device__ __forceinline__ void stage_block(const uint4* records, int32_t n_tree
 // wavefront has finished block b - 2 (the buffer's previous occupant),
 // copies the whole block, waits for its copy and publishes `ready`; the others
 // wait for `ready`.  A wavefront can thus run up to a block ahead of the
-// slowest one instead of meeting it at every block.  Every wait is bounded
-// (kSyncSpins sleeps); one that runs out makes stage_acquire return false,
-// and the caller marks its results invalid, so every wavefront ends.
+// slowest one instead of meeting it at every block.  Issue priority follows
+// the order in which wavefronts finish a block: the later a wavefront leaves
+// block b among its workgroup's, the higher its priority (s_setprio) while it
+// evaluates block b + 1, and a wavefront that arrives at a block before its
+// copy is there drops to the lowest; the oldest wavefronts of a SIMD would
+// otherwise keep winning issue and the youngest set the pace.  Every wait is
+// bounded (kSyncSpins sleeps); one that runs out makes stage_acquire return
+// false, and the caller marks its results invalid, so every wavefront ends.
 struct StageSync {
     int32_t claimed[2];
     int32_t ready[2];
@@ -146,6 +151,7 @@ __device__ __forceinline__ bool stage_acquire(StageSync* sync, int32_t b, int n_
     const int cur = b & 1;
     const int32_t need_done = n_waves * (b >> 1);
     int32_t spins = 0;
+    if (sync_load(&sync->ready[cur]) != b) __builtin_amdgcn_s_setprio(0);   // ahead of the others
     while (sync_load(&sync->ready[cur]) != b && spins < kSyncSpins) {
         int32_t won = 0;
         if (sync_load(&sync->claimed[cur]) == b - 2) {
@@ -172,11 +178,19 @@ __device__ __forceinline__ bool stage_acquire(StageSync* sync, int32_t b, int n_
     return spins < kSyncSpins;
 }
 
-// This wavefront has finished with block b (its reads have all returned).
-__device__ __forceinline__ void stage_release(StageSync* sync, int32_t b) {
+// This wavefront has finished with block b (its reads have all returned);
+// n_waves share the buffers.
+__device__ __forceinline__ void stage_release(StageSync* sync, int32_t b, int n_waves) {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    int32_t before = 0;
     if (lane_id() == 0)
-        __hip_atomic_fetch_add(&sync->done[b & 1], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        before = __hip_atomic_fetch_add(&sync->done[b & 1], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    // how many wavefronts left block b before this one, in quarters
+    const int32_t quarter = 4 * (__builtin_amdgcn_readfirstlane(before) % n_waves) / n_waves;
+    if (quarter == 3) __builtin_amdgcn_s_setprio(3);
+    else if (quarter == 2) __builtin_amdgcn_s_setprio(2);
+    else if (quarter == 1) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
 }
 
 // Walks NT consecutive staged trees (records rec_bytes apart, the first at
