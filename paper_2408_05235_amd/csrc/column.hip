@@ -8,9 +8,10 @@
 // A wavefront takes RPL stripes of 64 consecutive iterations of one scenario,
 // RPL rows per lane; the rows differ, so every lane walks every tree (the grid
 // kernel's leaf reuse needs many frequencies on the same row sequence).
-// Sixteen wavefronts of a workgroup share double-buffered blocks of tree
-// records in LDS, loaded into registers while the current block is evaluated
-// and stored after it.  A lane walks its RPL rows through up to four trees at
+// Sixteen wavefronts of a workgroup share two LDS buffers of tree-record
+// blocks, copied straight from global memory and handed over without block
+// barriers (stage_acquire / stage_release, which also set the wavefronts'
+// issue priorities).  A lane walks its RPL rows through up to four trees at
 // once, so RPL x trees chains of dependent LDS reads overlap (deep trees leave
 // room for only two trees per block).  Leaves are accumulated in fp64 in tree
 // order and rounded once, as everywhere in the library.
@@ -173,14 +174,17 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     }
 
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
-    // staging (stage_block): the next block's copy runs during evaluation
+    StageSync* sync = (StageSync*)(smem + 2 * buf_bytes);
+    if (threadIdx.x == 0) stage_sync_init(sync);
     if (n_blocks > 0) stage_block(records, n_trees, tb, rec_words, 0, lds_addr(smem), wave, kColWaves);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    bool sync_ok = true;
     for (int32_t b = 0; b < n_blocks; ++b) {
         const int cur = b & 1;
-        if (b + 1 < n_blocks)
-            stage_block(records, n_trees, tb, rec_words, b + 1, lds_addr(smem) + (cur ^ 1) * buf_bytes, wave, kColWaves);
+        if (b > 0)
+            sync_ok &= stage_acquire(sync, b, kColWaves, records, n_trees, tb, rec_words,
+                                     lds_addr(smem) + cur * buf_bytes);
         if (valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
             const uint32_t first = lds_addr(smem) + cur * buf_bytes;
@@ -192,12 +196,11 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
                 add_leaves<NF, 2, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
             if (t < cnt) add_leaves<NF, 1, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
         }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
+        stage_release(sync, b, kColWaves);
     }
 #pragma unroll
     for (int r = 0; r < RPL; ++r)
-        if (o[r] >= 0) P.out[o[r]] = (float)acc[r];
+        if (o[r] >= 0) P.out[o[r]] = sync_ok ? (float)acc[r] : __builtin_nanf("");
 }
 
 // Leaf reuse along a lane's RPL consecutive rows with two anchors: every lane
@@ -309,13 +312,17 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
     }
     asm volatile("" ::"v"(xf), "v"(xe));
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
+    StageSync* sync = (StageSync*)(smem + 2 * buf_bytes);
+    if (threadIdx.x == 0) stage_sync_init(sync);
     if (n_blocks > 0) stage_block(records, n_trees, tb, rec_words, 0, lds_addr(smem), wave, kColWaves);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    bool sync_ok = true;
     for (int32_t b = 0; b < n_blocks; ++b) {
         const int cur = b & 1;
-        if (b + 1 < n_blocks)
-            stage_block(records, n_trees, tb, rec_words, b + 1, lds_addr(smem) + (cur ^ 1) * buf_bytes, wave, kColWaves);
+        if (b > 0)
+            sync_ok &= stage_acquire(sync, b, kColWaves, records, n_trees, tb, rec_words,
+                                     lds_addr(smem) + cur * buf_bytes);
         if (valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
             const uint32_t first = lds_addr(smem) + cur * buf_bytes;
@@ -324,13 +331,12 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
                 add_leaves_anchored<NF, 2, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
             if (t < cnt) add_leaves_anchored<NF, 1, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
         }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
+        stage_release(sync, b, kColWaves);
     }
     if (valid) {
 #pragma unroll
         for (int r = 0; r < RPL; ++r)
-            if (j0 + r < P.H) P.out[s * P.H + j0 + r] = (float)acc[r];
+            if (j0 + r < P.H) P.out[s * P.H + j0 + r] = sync_ok ? (float)acc[r] : __builtin_nanf("");
     }
 }
 
@@ -368,10 +374,12 @@ __global__ __launch_bounds__(256) void forest_column_global_kernel(const uint2* 
 int32_t column_trees_per_block(const ForestDev& f, size_t* lds) {
     if (!f.records || f.n_trees == 0) return 0;
     const RecordLayout R = record_layout(f.depth);
+    // two tree buffers and their hand-over counters
+    auto bytes = [&](int32_t n) { return 2 * (size_t)stage_buffer_bytes(n, R) + sizeof(StageSync); };
     int32_t tb = std::min<int32_t>(f.n_trees, 64);
-    while (tb > 1 && 2 * (size_t)stage_buffer_bytes(tb, R) > kColLdsBudget) --tb;
-    if (2 * (size_t)stage_buffer_bytes(tb, R) > kColLdsBudget) return 0;
-    *lds = (size_t)2 * stage_buffer_bytes(tb, R);
+    while (tb > 1 && bytes(tb) > kColLdsBudget) --tb;
+    if (bytes(tb) > kColLdsBudget) return 0;
+    *lds = bytes(tb);
     return tb;
 }
 

@@ -17,17 +17,18 @@
 // fp64 add per tree; a walk happens on roughly one row in twenty.
 //
 //   forest_grid_lds_kernel     (depth <= 11) A 1024-thread workgroup (16
-//       wavefronts, 16 x 32 x 64 rows) walks the ensemble in blocks of trees
-//       that are staged in LDS, double-buffered: the next block is fetched
-//       into registers while the current one is evaluated.  A tree is one
-//       record (nodes, leaf values, leaf boxes), so a block is one contiguous
-//       copy.  Tree walks read LDS only.  A node step picks the tested
-//       feature with byte permutes and compares once, all in vector
-//       registers (no lane-mask round trip).  Trees are taken in pairs that
-//       share one box test (a row that leaves it walks only the tree whose
-//       own box it left), and rows in groups of four whose (KV, batch) hull
-//       is tested before any single row.  The wavefronts of a workgroup take
-//       the same iteration chunk of consecutive scenarios.
+//       wavefronts, 16 x 44 x 64 rows) walks the ensemble in blocks of trees
+//       staged in two LDS buffers.  A tree is one record (nodes, leaf values,
+//       leaf boxes), so a block is one contiguous copy, made straight from
+//       global memory into LDS and handed from wavefront to wavefront without
+//       block barriers (stage_acquire / stage_release).  Tree walks read LDS
+//       only.  A node step picks the tested feature with byte permutes and
+//       compares once, all in vector registers (no lane-mask round trip).
+//       Trees are taken in pairs that share one box test (a row that leaves
+//       it walks only the tree whose own box it left), and rows in groups of
+//       four whose (KV, batch) hull is tested before any single row.  The
+//       (scenario, chunk) items are ordered by an estimate of their walks,
+//       so a workgroup's wavefronts do similar work.
 //   forest_grid_global_kernel  (deeper trees) The same per-lane scheme with
 //       nodes, leaves and boxes read from global memory, one row at a time.
 //
