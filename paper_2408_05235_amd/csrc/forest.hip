@@ -138,8 +138,9 @@ struct GridItem {
 // Items are numbered scenario-fastest: the wavefronts of one workgroup take
 // the same iteration chunk (and frequency group) of consecutive scenarios.
 // How many walks a chunk needs follows how fast KV and batch change there;
-// workgroups whose wavefronts do similar work lose less time at their block
-// barriers.  With a work order (P.order), item i of a frequency group takes
+// workgroups whose wavefronts do similar work lose less time waiting for
+// their slowest wavefront to release a tree buffer.  With a work order
+// (P.order), item i of a frequency group takes
 // the (scenario, chunk) pair order[i] instead: pairs sorted by estimated
 // cost, most expensive first.
 __device__ __forceinline__ GridItem grid_item(const GridParams& P, int64_t item, int J) {
