@@ -342,14 +342,14 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                 const uint64_t over = __ballot(mem && a >= H);
                 const uint64_t take = over ? (memm & ((over & (~over + 1)) - 1)) : memm;
                 if (take == 0) break;   // the head cannot start within the horizon
-                int32_t r_end = 0;
+                // each member's in-horizon end, on its own lane
+                const int32_t lim_l = q_len >= H - a ? H : a + q_len;
+                const int32_t r_end = wave_max(((take >> lane) & 1) ? lim_l : 0);
                 for (uint64_t mm = take; mm; mm &= mm - 1) {
                     const int m = __ffsll((unsigned long long)mm) - 1;
                     const int32_t am = __builtin_amdgcn_readlane(a, m);
                     const int32_t cm = __builtin_amdgcn_readlane(q_c, m);
-                    const int32_t lm = __builtin_amdgcn_readlane(q_len, m);
-                    const int32_t lim = lm >= H - am ? H : am + lm;
-                    r_end = max(r_end, lim);
+                    const int32_t lim = __builtin_amdgcn_readlane(lim_l, m);
                     // LDS adds without a returned value: no wait per chunk
                     add_request<false, POW2, 1>(KV, cm, am, lim, divN);
                 }
@@ -368,8 +368,7 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
                         const int m = __ffsll((unsigned long long)mm) - 1;
                         const int32_t am = __builtin_amdgcn_readlane(a, m);
                         const int32_t cm = __builtin_amdgcn_readlane(q_c, m);
-                        const int32_t lm = __builtin_amdgcn_readlane(q_len, m);
-                        const int32_t lim = lm >= H - am ? H : am + lm;
+                        const int32_t lim = __builtin_amdgcn_readlane(lim_l, m);
                         add_request<true, POW2, 1>(KV, cm, am, lim, divN);
                     }
                     // shrink the batch; once down to single requests, admit
