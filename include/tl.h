@@ -182,6 +182,15 @@ tl_status tl_adjust_lengths(int64_t n_scenarios, int64_t n_requests, const int64
  *   (freqs_mhz[f], kv[s][j], batch[s][j] [, engine_size[s]])
  * the query vector of Sec. 4.3.2 check 2 for every candidate frequency.
  * freqs_mhz must be ascending; index F-1 is the maximum frequency.
+ *
+ * Scoreboards with long FIFO loops (no batch_cap and on average 1024 or more
+ * requests per scenario) are projected heaviest first (results do not depend
+ * on the order).  The order takes 4 bytes per scenario of device scratch
+ * that the library owns, one per device: allocated on the first such call,
+ * kept, and replaced only when more scenarios come.  If that allocation
+ * fails the scenarios run in their own order (same results).  Calls share
+ * it: a call on another stream than the previous one first waits (on the
+ * device) for the previous projection.
  * ---------------------------------------------------------------------- */
 typedef struct tl_project_args {
     uint32_t struct_size;          /* sizeof(tl_project_args) */
@@ -371,7 +380,8 @@ tl_status tl_select_freq_binary(const tl_forest* forest, int64_t n_scenarios, in
  * its rows, n_freqs, freqs_mhz and n_features are ignored.  engine_size [S]
  * is read for 4-feature forests.  ips [S][H] receives M at max_freq_mhz (rows
  * of scenarios flagged TL_FLAG_OVERFLOW hold M on the zero curves).  All
- * arrays are device arrays of the caller; the call allocates nothing.
+ * arrays are device arrays of the caller; the only scratch is the
+ * projection's scenario order, as for tl_project.
  * Errors as for tl_project, plus a NULL forest, ips, decision, tbt_slo_ns,
  * cand_prompt or cand_len, or a forest without 3 or 4 features: TL_EINVAL.
  * ---------------------------------------------------------------------- */

@@ -308,7 +308,71 @@ tl_status project_params(const tl_project_args* a, const char* who, bool with_ro
     p->engine = rows ? a->engine_size : nullptr;
     p->cand_prompt = nullptr;
     p->cand_len = nullptr;
+    p->order_ws = nullptr;
     return TL_OK;
+}
+
+// The projection's scenario order (heaviest first, for long FIFO loops) needs
+// a workspace of one word per scenario: owned by the library, one per device,
+// allocated on first use and replaced only by a larger one.  A call on
+// another stream than the previous user first waits (on the device) for that
+// user's projection.  Without the workspace (allocation failure, device
+// number out of range) the scenarios run in their own order: same results.
+constexpr int kOrderDevices = 64;
+struct OrderWorkspace {
+    std::mutex m;
+    void* ptr = nullptr;
+    size_t bytes = 0;
+    hipEvent_t done = nullptr;
+    hipStream_t stream = nullptr;
+    bool used = false;
+};
+OrderWorkspace g_order_ws[kOrderDevices];
+
+hipError_t project_launch(tl::ProjectParams p, hipStream_t st) {
+    const size_t need = tl::project_order_bytes(p);
+    int dev = -1;
+    if (need == 0 || hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kOrderDevices)
+        return tl::launch_project(p, st);
+    OrderWorkspace& w = g_order_ws[dev];
+    std::lock_guard<std::mutex> lock(w.m);
+    hipError_t e = hipSuccess;
+    if (!w.done && hipEventCreateWithFlags(&w.done, hipEventDisableTiming) != hipSuccess) {
+        w.done = nullptr;
+        (void)hipGetLastError();
+        return tl::launch_project(p, st);
+    }
+    if (need > w.bytes) {
+        if (w.ptr) {
+            if (w.used) {
+                e = hipEventSynchronize(w.done);
+                if (e != hipSuccess) return e;
+            }
+            (void)hipFree(w.ptr);
+            w.ptr = nullptr;
+            w.bytes = 0;
+            w.used = false;
+        }
+        if (hipMalloc(&w.ptr, need) == hipSuccess) {
+            w.bytes = need;
+        } else {
+            w.ptr = nullptr;
+            (void)hipGetLastError();   // clear the allocation error before the launches check theirs
+        }
+    }
+    if (!w.ptr) return tl::launch_project(p, st);
+    if (w.used && w.stream != st) {
+        e = hipStreamWaitEvent(st, w.done, 0);
+        if (e != hipSuccess) return e;
+    }
+    p.order_ws = w.ptr;
+    e = tl::launch_project(p, st);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(w.done, st);
+    if (e != hipSuccess) return e;
+    w.stream = st;
+    w.used = true;
+    return hipSuccess;
 }
 
 }  // namespace
@@ -321,7 +385,7 @@ tl_status tl_project(const tl_project_args* a, void* stream) {
     const tl_status st = project_params(a, "tl_project", true, &p);
     if (st != TL_OK) return st;
     if (a->n_scenarios == 0) return ok();
-    return from_hip(tl::launch_project(p, (hipStream_t)stream), "tl_project: launch");
+    return from_hip(project_launch(p, (hipStream_t)stream), "tl_project: launch");
 }
 
 tl_status tl_admit(const tl_admit_args* a, void* stream) {
@@ -345,7 +409,7 @@ tl_status tl_admit(const tl_admit_args* a, void* stream) {
     const hipStream_t st_h = (hipStream_t)stream;
     p.cand_prompt = a->cand_prompt;
     p.cand_len = a->cand_len;
-    hipError_t e = tl::launch_project(p, st_h);
+    hipError_t e = project_launch(p, st_h);
     if (e != hipSuccess) return from_hip(e, "tl_admit: projection launch");
     tl::ColumnParams c{};
     c.S = S;

@@ -129,6 +129,48 @@ __device__ __forceinline__ void add_request(int32_t* KV, int32_t c, int32_t a, i
 // cap it is only added to and finally prefix-summed, so it accumulates with
 // atomics in the scenario's own batch output row instead: half the LDS, twice
 // the scenario wavefronts per CU.
+// Scenario order for long FIFO loops: one wavefront per scenario, whose time
+// grows with its number of requests; launched heaviest first, the last
+// wavefronts of the grid are short ones instead of whichever came last.  A
+// counting sort over kOrderBuckets classes of the request count (six per
+// doubling), heaviest class first; the order inside a class is whatever the
+// atomics give (each scenario's results do not depend on it).  Workspace:
+// the counters, then the order [S].
+constexpr int kOrderBuckets = 128;
+
+__device__ __forceinline__ int order_bucket(const int64_t* off, int64_t s) {
+    const int64_t n = off[s + 1] - off[s];
+    const float c = n > 0 ? (float)n : 0.0f;   // malformed offsets: lightest class
+    return kOrderBuckets - 1 - min(kOrderBuckets - 1, (int)(log2f(c + 1.0f) * 6.0f));
+}
+
+__global__ __launch_bounds__(kOrderBuckets) void order_clear_kernel(uint32_t* counts) {
+    counts[threadIdx.x] = 0;
+}
+
+__global__ __launch_bounds__(256) void order_count_kernel(const int64_t* off, int64_t S, uint32_t* counts) {
+    const int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (s < S) atomicAdd(&counts[order_bucket(off, s)], 1u);
+}
+
+// exclusive prefix of the class counts, in place: each becomes its class's
+// first position
+__global__ __launch_bounds__(kWave) void order_start_kernel(uint32_t* counts) {
+    uint32_t carry = 0;
+    for (int i0 = 0; i0 < kOrderBuckets; i0 += kWave) {
+        const uint32_t c = counts[i0 + lane_id()];
+        const uint32_t incl = (uint32_t)wave_incl_scan((int32_t)c) + carry;
+        counts[i0 + lane_id()] = incl - c;
+        carry = (uint32_t)__builtin_amdgcn_readlane((int32_t)incl, kWave - 1);
+    }
+}
+
+__global__ __launch_bounds__(256) void order_place_kernel(const int64_t* off, int64_t S, uint32_t* counts,
+                                                          int32_t* order) {
+    const int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (s < S) order[atomicAdd(&counts[order_bucket(off, s)], 1u)] = (int32_t)s;
+}
+
 // Smallest batch of queued requests tried at once (no batch cap): below it the
 // admission loop takes requests one at a time.
 constexpr int32_t kMinBatch = 8;
@@ -140,7 +182,7 @@ __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     const int32_t N = P.N;
     const DivU32 divN{(uint32_t)N, P.div_m, P.div_l};
     const int lane = lane_id();
-    const int64_t s = blockIdx.x;
+    const int64_t s = P.order_ws ? (int64_t)((const int32_t*)P.order_ws + kOrderBuckets)[blockIdx.x] : blockIdx.x;
     int32_t* outB = P.batch + s * H;
     int32_t* KV = lds;                      // comb diff, comb prefix, + jumps, then KV values
     int32_t* BI = BD_LDS ? lds + H : outB;  // batch difference array
@@ -612,11 +654,21 @@ hipError_t launch_adjust(const AdjustParams& p, hipStream_t stream) {
     return hipGetLastError();
 }
 
+// Long FIFO loops: no batch cap and on average 1024 or more requests per
+// scenario.
+bool long_fifo_loops(const ProjectParams& p) {
+    return p.batch_cap == nullptr && p.n_requests >= (int64_t)1024 * p.n_scenarios;
+}
+
+size_t project_order_bytes(const ProjectParams& p) {
+    if (!long_fifo_loops(p) || p.n_scenarios < 2 || p.n_scenarios > 0x7fffffffll) return 0;
+    return (size_t)(kOrderBuckets + p.n_scenarios) * sizeof(int32_t);
+}
+
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream) {
-    // The batch differences go to global memory where occupancy pays: no
-    // batch cap and long FIFO loops (on average 1024 or more requests per
-    // scenario); otherwise the LDS array is faster.
-    const bool bd_lds = p.batch_cap != nullptr || p.n_requests < (int64_t)1024 * p.n_scenarios;
+    // The batch differences go to global memory where occupancy pays (long
+    // FIFO loops); otherwise the LDS array is faster.
+    const bool bd_lds = !long_fifo_loops(p);
     const size_t lds = (size_t)(bd_lds ? 2 : 1) * p.H * sizeof(int32_t);
     // block sizes that are powers of two up to 64 take shifts instead of
     // divisions in the admission loops
@@ -626,6 +678,17 @@ hipError_t launch_project(const ProjectParams& p, hipStream_t stream) {
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
+    }
+    if (p.order_ws) {
+        uint32_t* counts = (uint32_t*)p.order_ws;
+        const unsigned nb = (unsigned)((p.n_scenarios + 255) / 256);
+        hipLaunchKernelGGL(order_clear_kernel, dim3(1), dim3(kOrderBuckets), 0, stream, counts);
+        hipLaunchKernelGGL(order_count_kernel, dim3(nb), dim3(256), 0, stream, p.off, p.n_scenarios, counts);
+        hipLaunchKernelGGL(order_start_kernel, dim3(1), dim3(kWave), 0, stream, counts);
+        hipLaunchKernelGGL(order_place_kernel, dim3(nb), dim3(256), 0, stream, p.off, p.n_scenarios, counts,
+                           (int32_t*)p.order_ws + kOrderBuckets);
+        const hipError_t e0 = hipGetLastError();
+        if (e0 != hipSuccess) return e0;
     }
     hipLaunchKernelGGL(kern, dim3((unsigned)p.n_scenarios), dim3(64), lds, stream, p);
     hipError_t e = hipGetLastError();

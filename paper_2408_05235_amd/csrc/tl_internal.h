@@ -38,6 +38,9 @@ struct ProjectParams {
     // (admission control); both nullable together
     const int32_t* cand_prompt;     // [S]
     const int32_t* cand_len;        // [S]
+    // nullable: workspace of project_order_bytes() bytes; with it the
+    // scenarios are projected heaviest first (same results, shorter tail)
+    void* order_ws;
 };
 
 // The model at one frequency per scenario on the projection grid:
@@ -192,6 +195,9 @@ hipError_t launch_lattice_column(const ForestDev& f, const LatticeDev& L, const 
 inline bool grid_fits(int64_t blocks) { return blocks >= 0 && blocks <= 0x7fffffffll; }
 
 hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
+// Workspace bytes for ordering the scenarios of a projection heaviest first;
+// 0 when the ordering does not pay (short FIFO loops).
+size_t project_order_bytes(const ProjectParams& p);
 hipError_t launch_adjust(const AdjustParams& p, hipStream_t stream);
 hipError_t launch_forest_rows(const ForestDev& f, const float* rows, int64_t n_rows, float* out,
                               hipStream_t stream);

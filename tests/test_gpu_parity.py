@@ -147,6 +147,27 @@ def test_project_many_requests(gpu, H, N, seed, rmax, qfrac):
     assert_projection_equal(gpu_project(inp), oracle.project(inp), f"H={H} N={N} rmax={rmax}")
 
 
+def test_project_order_workspace_grows_and_changes_stream(gpu):
+    """Long-FIFO boards are projected in an order kept in a per-device
+    workspace of the library: a larger board replaces it, and calls from
+    another stream wait for the previous user.  Every call equals the oracle."""
+    import torch
+    boards = []
+    for i, S in enumerate((40, 96, 40)):
+        inp = random_boards(np.random.default_rng(30 + i), S, 1024, 16, rmax=3000, qfrac=0.6)
+        inp["batch_cap"] = None
+        assert int(inp["req_offset"][-1]) >= 1024 * S
+        boards.append(inp)
+    side = torch.cuda.Stream()
+    for i, inp in enumerate(boards):
+        if i == 1:
+            with torch.cuda.stream(side):
+                g = gpu_project(inp)
+        else:
+            g = gpu_project(inp)
+        assert_projection_equal(g, oracle.project(inp), f"board {i} S={inp['n_scenarios']}")
+
+
 @pytest.mark.parametrize("H,N,seed", [(1, 16, 0), (7, 1, 1), (64, 16, 2), (100, 3, 3), (513, 16, 4),
                                       (1000, 64, 5), (257, 100, 6), (2048, 16, 7), (130, 7, 8),
                                       (600, 128, 9)])
