@@ -72,14 +72,15 @@ __device__ __forceinline__ float column_freq(const ColumnParams& P, int64_t s) {
     return P.fidx ? P.freqs[max(P.fidx[s], 0)] : P.freq;
 }
 
-// Leaf indices k[r][t] of NR rows (each with its own features) through NT
-// consecutive staged trees (records rec_bytes apart, the first at LDS byte
+// The leaves lf[r][t] that NR rows (each with its own features) reach in NT
+// consecutive staged trees (records R.bytes apart, the first at LDS byte
 // address `tree`), all NR x NT chains of dependent LDS reads interleaved:
 // every chain's node reads issue back to back, then the compares.
 template <int NF, int NT, int NR>
-__device__ __forceinline__ void walk_rows(uint32_t tree, uint32_t rec_bytes, int32_t depth, const float (&xf)[NR],
+__device__ __forceinline__ void walk_rows(uint32_t tree, const RecordLayout& R, int32_t depth, const float (&xf)[NR],
                                           const float (&kv)[NR], const float (&bs)[NR], const float (&xe)[NR],
-                                          int32_t (&k)[NR][NT]) {
+                                          LeafAt (&lf)[NR][NT]) {
+    const uint32_t rec_bytes = R.bytes;
     uint32_t a[NR][NT], cl[NT], cr[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -104,25 +105,24 @@ __device__ __forceinline__ void walk_rows(uint32_t tree, uint32_t rec_bytes, int
                 a[r][t] = 2u * a[r][t] + (left ? cl[t] : cr[t]);
             }
     }
-    const int32_t n_int = (1 << depth) - 1;
 #pragma unroll
     for (int r = 0; r < NR; ++r)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) k[r][t] = (int32_t)((a[r][t] - (tree + t * rec_bytes)) >> 4) - n_int;
+        for (int t = 0; t < NT; ++t) lf[r][t] = leaf_at(a[r][t], tree + t * rec_bytes, R, depth);
 }
 
 // Walks NT consecutive staged trees for the RPL rows of a lane and adds the
 // leaves to each row's sum in tree order.
 template <int NF, int NT, int RPL>
-__device__ __forceinline__ void add_leaves(uint32_t tree, uint32_t rec_bytes, int32_t depth,
+__device__ __forceinline__ void add_leaves(uint32_t tree, const RecordLayout& R, int32_t depth,
                                            const float (&xf)[RPL], const float (&kv)[RPL], const float (&bs)[RPL],
                                            const float (&xe)[RPL], double (&acc)[RPL]) {
-    int32_t k[RPL][NT];
-    walk_rows<NF, NT, RPL>(tree, rec_bytes, depth, xf, kv, bs, xe, k);
+    LeafAt k[RPL][NT];
+    walk_rows<NF, NT, RPL>(tree, R, depth, xf, kv, bs, xe, k);
 #pragma unroll
     for (int r = 0; r < RPL; ++r)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc[r] += (double)leaf_value(tree + t * rec_bytes, k[r][t]);
+        for (int t = 0; t < NT; ++t) acc[r] += (double)leaf_value(k[r][t]);
 }
 
 template <int NF, int RPL, bool ROWS>
@@ -191,10 +191,10 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
             int32_t t = 0;
             if (RPL == 1)
                 for (; t + 4 <= cnt; t += 4)
-                    add_leaves<NF, 4, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
+                    add_leaves<NF, 4, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
             for (; t + 2 <= cnt; t += 2)
-                add_leaves<NF, 2, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
-            if (t < cnt) add_leaves<NF, 1, RPL>(first + t * R.bytes, R.bytes, depth, xf, kv, bs, xe, acc);
+                add_leaves<NF, 2, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
+            if (t < cnt) add_leaves<NF, 1, RPL>(first + t * R.bytes, R, depth, xf, kv, bs, xe, acc);
         }
         stage_release(sync, b, kColWaves);
     }
@@ -220,14 +220,14 @@ __device__ __forceinline__ void add_leaves_anchored(uint32_t tree, const RecordL
     {
         const float xfa[2] = {xf, xf}, kva[2] = {kv[0], kv[RPL - 1]}, bsa[2] = {bs[0], bs[RPL - 1]},
                     xea[2] = {xe, xe};
-        int32_t ka[2][NT];
-        walk_rows<NF, NT, 2>(tree, R.bytes, depth, xfa, kva, bsa, xea, ka);
+        LeafAt ka[2][NT];
+        walk_rows<NF, NT, 2>(tree, R, depth, xfa, kva, bsa, xea, ka);
 #pragma unroll
         for (int e = 0; e < 2; ++e)
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                va[e][t] = leaf_value(tree + t * R.bytes, ka[e][t]);
-                ba[e][t] = leaf_box(tree + t * R.bytes, R, ka[e][t]);
+                va[e][t] = leaf_value(ka[e][t]);
+                ba[e][t] = leaf_box(ka[e][t]);
             }
     }
     float vl[NT];
@@ -254,22 +254,22 @@ __device__ __forceinline__ void add_leaves_anchored(uint32_t tree, const RecordL
             }
             if (NT == 2 && __builtin_amdgcn_ballot_w64(need[0]) != 0 &&
                 __builtin_amdgcn_ballot_w64(need[NT - 1]) != 0) {
-                int32_t k[NT];
-                walk<NF, NT>(tree, R.bytes, depth, xf, kv[r], bs[r], xe, k);
+                LeafAt k[NT];
+                walk<NF, NT>(tree, R, depth, xf, kv[r], bs[r], xe, k);
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
                     if (need[t]) {
-                        v[t] = vl[t] = leaf_value(tree + t * R.bytes, k[t]);
-                        bl[t] = leaf_box(tree + t * R.bytes, R, k[t]);
+                        v[t] = vl[t] = leaf_value(k[t]);
+                        bl[t] = leaf_box(k[t]);
                     }
             } else {
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
                     if (need[t]) {
-                        int32_t k[1];
-                        walk<NF, 1>(tree + t * R.bytes, R.bytes, depth, xf, kv[r], bs[r], xe, k);
-                        v[t] = vl[t] = leaf_value(tree + t * R.bytes, k[0]);
-                        bl[t] = leaf_box(tree + t * R.bytes, R, k[0]);
+                        LeafAt k[1];
+                        walk<NF, 1>(tree + t * R.bytes, R, depth, xf, kv[r], bs[r], xe, k);
+                        v[t] = vl[t] = leaf_value(k[0]);
+                        bl[t] = leaf_box(k[0]);
                     }
             }
         }

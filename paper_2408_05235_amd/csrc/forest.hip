@@ -261,14 +261,14 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
         // the chunk's first row walks every tree on every lane, outside the
         // group loop so that the loop's walks carry no first-row case
         const float4 q0 = kv4[0];
-        int32_t k[NT];
-        walk<NF, NT>(tree_addr, R.bytes, depth, xf, q0.x, q0.y, xe, k);
-        v[0] = (double)leaf_value(tree_addr, k[0]);
-        b0 = leaf_box(tree_addr, R, k[0]);
+        LeafAt k[NT];
+        walk<NF, NT>(tree_addr, R, depth, xf, q0.x, q0.y, xe, k);
+        v[0] = (double)leaf_value(k[0]);
+        b0 = leaf_box(k[0]);
         box = b0;
         if (NT == 2) {
-            v[NT - 1] = (double)leaf_value(tree1, k[NT - 1]);
-            b1 = leaf_box(tree1, R, k[NT - 1]);
+            v[NT - 1] = (double)leaf_value(k[NT - 1]);
+            b1 = leaf_box(k[NT - 1]);
             box = box_meet(b0, b1);
         }
     }
@@ -293,36 +293,36 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
                 const float bs = (i & 1) ? q.w : q.y;
                 if (!in_box(box, kv, bs)) {
                     if (NT == 1) {
-                        int32_t k[1];
-                        walk<NF, 1>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
-                        v[0] = (double)leaf_value(tree_addr, k[0]);
-                        box = leaf_box(tree_addr, R, k[0]);
+                        LeafAt k[1];
+                        walk<NF, 1>(tree_addr, R, depth, xf, kv, bs, xe, k);
+                        v[0] = (double)leaf_value(k[0]);
+                        box = leaf_box(k[0]);
                     } else {
                         const bool n0 = !in_box(b0, kv, bs);
                         const bool n1 = !in_box(b1, kv, bs);
                         if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
-                            int32_t k[2];
-                            walk<NF, 2>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
+                            LeafAt k[2];
+                            walk<NF, 2>(tree_addr, R, depth, xf, kv, bs, xe, k);
                             if (n0) {
-                                v[0] = (double)leaf_value(tree_addr, k[0]);
-                                b0 = leaf_box(tree_addr, R, k[0]);
+                                v[0] = (double)leaf_value(k[0]);
+                                b0 = leaf_box(k[0]);
                             }
                             if (n1) {
-                                v[NT - 1] = (double)leaf_value(tree1, k[1]);
-                                b1 = leaf_box(tree1, R, k[1]);
+                                v[NT - 1] = (double)leaf_value(k[1]);
+                                b1 = leaf_box(k[1]);
                             }
                         } else {
                             if (n0) {
-                                int32_t k[1];
-                                walk<NF, 1>(tree_addr, R.bytes, depth, xf, kv, bs, xe, k);
-                                v[0] = (double)leaf_value(tree_addr, k[0]);
-                                b0 = leaf_box(tree_addr, R, k[0]);
+                                LeafAt k[1];
+                                walk<NF, 1>(tree_addr, R, depth, xf, kv, bs, xe, k);
+                                v[0] = (double)leaf_value(k[0]);
+                                b0 = leaf_box(k[0]);
                             }
                             if (n1) {
-                                int32_t k[1];
-                                walk<NF, 1>(tree1, R.bytes, depth, xf, kv, bs, xe, k);
-                                v[NT - 1] = (double)leaf_value(tree1, k[0]);
-                                b1 = leaf_box(tree1, R, k[0]);
+                                LeafAt k[1];
+                                walk<NF, 1>(tree1, R, depth, xf, kv, bs, xe, k);
+                                v[NT - 1] = (double)leaf_value(k[0]);
+                                b1 = leaf_box(k[0]);
                             }
                         }
                         box = box_meet(b0, b1);

@@ -29,9 +29,11 @@ __device__ __forceinline__ bool in_box(const float4& b, float kv, float bs) {
     return (kv >= b.x) & (kv < b.y) & (bs >= b.z) & (bs < b.w);
 }
 
-// The intersection of two leaf boxes.
+// The intersection of two leaf boxes.  Box bounds are decoded integers or
+// infinities, never NaN, so fmaxf / fminf (one instruction each) give what
+// comparisons would.
 __device__ __forceinline__ float4 box_meet(const float4& a, const float4& b) {
-    return make_float4(a.x > b.x ? a.x : b.x, a.y < b.y ? a.y : b.y, a.z > b.z ? a.z : b.z, a.w < b.w ? a.w : b.w);
+    return make_float4(fmaxf(a.x, b.x), fminf(a.y, b.y), fmaxf(a.z, b.z), fminf(a.w, b.w));
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -52,17 +54,32 @@ __device__ __forceinline__ uint4 read_node(uint32_t a) {
     return make_uint4(w.x, w.y, w.z, w.w);
 }
 
-// The value of leaf L of the staged tree whose record starts at LDS byte
-// address `tree` (word 3 of node slot L).
-__device__ __forceinline__ float leaf_value(uint32_t tree, int32_t L) {
-    return *(lds_f32*)(uintptr_t)(tree + 16u * (uint32_t)L + 12u);
+// A leaf reached by a walk, as the LDS byte addresses of its value and of
+// its box.
+struct LeafAt {
+    uint32_t value, box;
+};
+
+// The leaf at which a walk of the staged tree whose record starts at LDS
+// byte address `tree` ended, from the walk's final address a = tree +
+// 16 (n_int + L) (heap slot n_int + L, leaf L): its value is word 3 of node
+// slot L, i.e. at a - 16 n_int + 12, and its box at tree + boxes + 8 L =
+// a / 2 + (tree / 2 + boxes - 8 n_int) (tree and a are multiples of 16).
+__device__ __forceinline__ LeafAt leaf_at(uint32_t a, uint32_t tree, const RecordLayout& R, int32_t depth) {
+    const uint32_t n_int16 = 16u * ((1u << depth) - 1u);
+    return LeafAt{a - (n_int16 - 12u), (a >> 1) + ((tree >> 1) + R.boxes - n_int16 / 2u)};
 }
 
-// The KV / batch box of leaf L of a staged tree, decoded from its packed
-// integer bounds into (kv_lo, kv_hi, batch_lo, batch_hi) as floats (exact:
-// all bounds are below 2^24).
-__device__ __forceinline__ float4 leaf_box(uint32_t tree, const RecordLayout& R, int32_t L) {
-    const u32x2 w = *(lds_u32x2*)(uintptr_t)(tree + R.boxes + 8u * (uint32_t)L);
+// The value of a leaf.
+__device__ __forceinline__ float leaf_value(const LeafAt& l) {
+    return *(lds_f32*)(uintptr_t)l.value;
+}
+
+// The KV / batch box of a leaf, decoded from its packed integer bounds into
+// (kv_lo, kv_hi, batch_lo, batch_hi) as floats (exact: all bounds are below
+// 2^24).
+__device__ __forceinline__ float4 leaf_box(const LeafAt& l) {
+    const u32x2 w = *(lds_u32x2*)(uintptr_t)l.box;
     return make_float4((float)(w.x & kBoxKvMax), (float)(w.y & kBoxKvMax), (float)(w.x >> 20),
                        (float)(w.y >> 20));
 }
@@ -193,13 +210,14 @@ __device__ __forceinline__ void stage_release(StageSync* sync, int32_t b, int n_
     else __builtin_amdgcn_s_setprio(0);
 }
 
-// Walks NT consecutive staged trees (records rec_bytes apart, the first at
-// LDS byte address `tree`) from the root for one row; k[t] = leaf index of
-// tree t.  The walks of two trees interleave, so their chains of dependent
-// LDS reads overlap.
+// Walks NT consecutive staged trees (records R.bytes apart, the first at
+// LDS byte address `tree`) from the root for one row; lf[t] = the leaf
+// reached in tree t.  The walks of two trees interleave, so their chains of
+// dependent LDS reads overlap.
 template <int NF, int NT>
-__device__ __forceinline__ void walk(uint32_t tree, uint32_t rec_bytes, int32_t depth, float xf, float kv, float bs,
-                                     float xe, int32_t (&k)[NT]) {
+__device__ __forceinline__ void walk(uint32_t tree, const RecordLayout& R, int32_t depth, float xf, float kv, float bs,
+                                     float xe, LeafAt (&lf)[NT]) {
+    const uint32_t rec_bytes = R.bytes;
     // the loop carries node byte addresses: child 2k+1 of the node at
     // a = root + 16 k sits at 2 a + (16 - root), child 2k+2 16 bytes later
     uint32_t a[NT], cl[NT], cr[NT];
@@ -220,9 +238,8 @@ __device__ __forceinline__ void walk(uint32_t tree, uint32_t rec_bytes, int32_t 
             a[t] = 2u * a[t] + (left ? cl[t] : cr[t]);
         }
     }
-    const int32_t n_int = (1 << depth) - 1;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) k[t] = (int32_t)((a[t] - (tree + t * rec_bytes)) >> 4) - n_int;
+    for (int t = 0; t < NT; ++t) lf[t] = leaf_at(a[t], tree + t * rec_bytes, R, depth);
 }
 
 }  // namespace
