@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 # 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz: one non-packed VALU lane
-# operation (an fp32 compare, an fp64 add) per lane per clock
+# operation (an fp32 compare or add) per lane per clock
 VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 FOREST_KERNEL = "forest_grid_lds_kernel"
 METRIC = "feature rows predicted/sec + scenarios/sec end-to-end; % of HBM peak"
@@ -523,7 +523,7 @@ def main():
 
     f = inp["forest"]
     # algorithmic work of the forest stage: every (row, tree) pair needs at
-    # least its leaf accumulated (one fp64 add); walks that leaf reuse avoids
+    # least its leaf accumulated (one fp32 add); walks that leaf reuse avoids
     # are not counted, so this is the floor any implementation must execute
     ops_per_row = f["n_trees"]
     forest_s = stage_ms[1] / 1e3
@@ -563,7 +563,7 @@ def main():
         "roofline": {"kernel": FOREST_KERNEL, "bound": "alu", "achieved": achieved,
                      "peak": VALU_PEAK_TOPS, "unit": "Tops/s", "frac": achieved / VALU_PEAK_TOPS,
                      "traffic": traffic, "ops_per_row": ops_per_row,
-                     "ops_note": "one fp64 leaf add per (row, tree); peak = non-packed VALU lane ops"},
+                     "ops_note": "one fp32 leaf add per (row, tree); peak = non-packed VALU lane ops"},
     }
     out["results_d2h_ms"] = d2h_results_ms(ctl)
     out["adjust_lengths"] = adjust_lengths_bench(inp, dev_in, args.steps, copy_gbs)

@@ -115,8 +115,10 @@ const char* tl_last_error(void);     /* message for the last non-OK status on th
  * after `depth` comparisons the node index minus (2^depth - 1) selects one of
  * the 2^depth leaves.  A shallower tree is expressed by padding with
  * threshold +inf (always 2k+1).  The prediction of a row is base_score plus
- * the selected leaf of every tree, accumulated in fp64 in tree order and
- * rounded once to fp32.
+ * the selected leaf of every tree as an fp32 running sum in tree order
+ * (acc = base_score, then acc += leaf_t for t = 0 .. n_trees-1, each add
+ * rounded to nearest even): the paper does not state the sum's precision,
+ * and this is how an ensemble that keeps its predictions in fp32 adds them.
  *
  * feature   host, uint8 [n_trees][2^depth - 1], each < n_features
  * threshold host, fp32  [n_trees][2^depth - 1]
@@ -241,7 +243,7 @@ tl_status tl_forest_predict(const tl_forest* forest, const float* rows, int64_t 
  * features in the order (frequency, KV, batch[, engine size]).
  * 1 <= F <= TL_MAX_FREQS, 1 <= H <= TL_MAX_HORIZON.
  * Work is ordered by an estimate of its cost (results do not depend on the
- * order).  The ordering needs 16 bytes per (scenario, 44-iteration chunk)
+ * order).  The ordering needs 16 bytes per (scenario, 64-iteration chunk)
  * plus a radix sort's temporary storage of device scratch, which the forest
  * handle owns: it is allocated
  * on the first call, kept, and replaced only when a larger grid comes, so
@@ -262,9 +264,9 @@ tl_status tl_forest_predict_grid(const tl_forest* forest, int64_t n_scenarios, i
  * allocation): same arguments, same results, no allocation of any kind.
  * The work order's scratch is a fixed 32 MiB array of the library on each
  * device (taken when the library is loaded): 16 bytes per (scenario,
- * 44-iteration chunk) pair plus the sort's temporary storage must fit, as
- * they do for 16384 scenarios x 2048 iterations (770,048 pairs) but not for
- * 65536 x 1024.  A grid whose order needs more returns TL_EUNSUPPORTED and
+ * 64-iteration chunk) pair plus the sort's temporary storage must fit, as
+ * they do for 16384 scenarios x 2048 iterations (524,288 pairs) but not for
+ * 65536 x 2048.  A grid whose order needs more returns TL_EUNSUPPORTED and
  * enqueues nothing.  Every call on one device shares that array: calls that
  * overlap on one device (concurrent streams, other threads) race and must
  * be serialized by the caller; tl_forest_predict_grid does not use it.
@@ -281,7 +283,7 @@ tl_status tl_forest_predict_grid_noalloc(const tl_forest* forest, int64_t n_scen
  * all inputs are bounded), so M can be evaluated once at every lattice point
  * and prediction becomes a table lookup:
  *   tl_lattice_create evaluates M (with tl_forest_predict_grid's kernels, so
- *   every value is the tree-order fp64 sum a walk gives) at every
+ *   every value is the fp32 tree-order sum a walk gives) at every
  *   (engine size, batch 0..batch_max, frequency, KV 0..kv_max); the table
  *   takes n_engines x (batch_max + 1) x n_freqs x 4096 x ceil((kv_max + 1) /
  *   4096) x 4 bytes (tl_lattice_bytes), at most 256 GiB.

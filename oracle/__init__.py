@@ -121,7 +121,8 @@ def rows(freqs, batch, kv, engine=None, n_features=3):
 
 
 def forest_predict(forest, x):
-    """Ensemble output for every row of ``x`` ([..., n_features] fp32)."""
+    """Ensemble output for every row of ``x`` ([..., n_features] fp32):
+    base_score plus every tree's leaf, an fp32 running sum in tree order."""
     lib = _load()
     nf = int(forest["n_features"])
     x = _c(x, np.float32)

@@ -18,9 +18,9 @@
  *
  * Precision: projection and selection are integer arithmetic (times are
  * integer nanoseconds); the only floating-point steps are the fp32 threshold
- * comparisons of the trees, the ensemble sum (accumulated in fp64 in tree
- * order, returned as fp32) and the per-iteration time 1e9 / IPS (one IEEE fp64
- * division, rounded up to whole nanoseconds).
+ * comparisons of the trees, the ensemble sum (an fp32 running sum in tree
+ * order) and the per-iteration time 1e9 / IPS (one IEEE fp64 division,
+ * rounded up to whole nanoseconds).
  *
  * Where the paper leaves a point open, the comment at each function states
  * the reading it follows (relative iterations, the token produced in an
@@ -255,8 +255,12 @@ int tlo_rows(int64_t S, int32_t F, int32_t H, int32_t n_features,
  * ensemble.  Each tree is complete of depth d, stored in heap order: internal
  * node k tests x[feature_k] < threshold_k and continues at 2k+1 if true, at
  * 2k+2 otherwise; after d tests the node index minus (2^d - 1) names the leaf.
- * The prediction is base_score plus the leaf of every tree, summed in tree
- * order in fp64 and rounded to fp32 once.
+ * The prediction is base_score plus the leaf of every tree as a running
+ * fp32 sum in tree order: acc = base_score, then acc = acc + leaf_t for
+ * t = 0 .. T-1, every add rounded to nearest even (no reassociation, nothing
+ * fused).  The paper does not state the sum's precision; single precision
+ * in tree order is how a gradient-boosted ensemble that keeps its
+ * predictions in fp32 (the XGBoost model of Sec. 4.3.1) adds its trees.
  */
 int tlo_forest_predict(int32_t n_trees, int32_t depth, int32_t n_features, float base_score,
                        const uint8_t* feature, const float* threshold, const float* leaf,
@@ -269,7 +273,7 @@ int tlo_forest_predict(int32_t n_trees, int32_t depth, int32_t n_features, float
         if (feature[i] >= n_features) return 1;
     for (int64_t r = 0; r < n_rows; ++r) {
         const float* x = rows + r * n_features;
-        double acc = (double)base_score;
+        float acc = base_score;
         for (int32_t t = 0; t < n_trees; ++t) {
             const uint8_t* ft = feature + (int64_t)t * n_int;
             const float* th = threshold + (int64_t)t * n_int;
@@ -278,9 +282,9 @@ int tlo_forest_predict(int32_t n_trees, int32_t depth, int32_t n_features, float
                 if (x[ft[k]] < th[k]) k = 2 * k + 1;
                 else k = 2 * k + 2;
             }
-            acc += (double)leaf[(int64_t)t * n_leaf + (k - n_int)];
+            acc += leaf[(int64_t)t * n_leaf + (k - n_int)];
         }
-        out[r] = (float)acc;
+        out[r] = acc;
     }
     return 0;
 }

@@ -13,8 +13,8 @@
 // barriers (stage_acquire / stage_release, which also set the wavefronts'
 // issue priorities).  A lane walks its RPL rows through up to four trees at
 // once, so RPL x trees chains of dependent LDS reads overlap (deep trees leave
-// room for only two trees per block).  Leaves are accumulated in fp64 in tree
-// order and rounded once, as everywhere in the library.
+// room for only two trees per block).  Leaves are added as an fp32 running sum
+// in tree order, as everywhere in the library.
 //
 // On horizons of at least 64 x RPL iterations and grids of at least one
 // workgroup per CU, forest_column_reuse_kernel gives each lane RPL (16, else
@@ -116,13 +116,13 @@ __device__ __forceinline__ void walk_rows(uint32_t tree, const RecordLayout& R, 
 template <int NF, int NT, int RPL>
 __device__ __forceinline__ void add_leaves(uint32_t tree, const RecordLayout& R, int32_t depth,
                                            const float (&xf)[RPL], const float (&kv)[RPL], const float (&bs)[RPL],
-                                           const float (&xe)[RPL], double (&acc)[RPL]) {
+                                           const float (&xe)[RPL], float (&acc)[RPL]) {
     LeafAt k[RPL][NT];
     walk_rows<NF, NT, RPL>(tree, R, depth, xf, kv, bs, xe, k);
 #pragma unroll
     for (int r = 0; r < RPL; ++r)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc[r] += (double)leaf_value(k[r][t]);
+        for (int t = 0; t < NT; ++t) acc[r] += leaf_value(k[r][t]);
 }
 
 template <int NF, int RPL, bool ROWS>
@@ -136,7 +136,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     const int wave = threadIdx.x / kWave;
     const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kColWaves + wave);
     float xf[RPL], kv[RPL], bs[RPL], xe[RPL];
-    double acc[RPL];
+    float acc[RPL];
     int64_t o[RPL];     // output index of each row, < 0: none
     bool valid;         // the wavefront has rows (uniform)
     if (ROWS) {
@@ -168,7 +168,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     }
 #pragma unroll
     for (int r = 0; r < RPL; ++r) {
-        acc[r] = (double)base;
+        acc[r] = base;
         // the rows are complete before any staging load is in flight
         asm volatile("" ::"v"(xf[r]), "v"(kv[r]), "v"(bs[r]), "v"(xe[r]));
     }
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
     }
 #pragma unroll
     for (int r = 0; r < RPL; ++r)
-        if (o[r] >= 0) P.out[o[r]] = sync_ok ? (float)acc[r] : __builtin_nanf("");
+        if (o[r] >= 0) P.out[o[r]] = sync_ok ? acc[r] : __builtin_nanf("");
 }
 
 // Leaf reuse along a lane's RPL consecutive rows with two anchors: every lane
@@ -214,7 +214,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_lds_kernel(const ui
 template <int NF, int NT, int RPL>
 __device__ __forceinline__ void add_leaves_anchored(uint32_t tree, const RecordLayout& R, int32_t depth, float xf,
                                                     const float (&kv)[RPL], const float (&bs)[RPL], float xe,
-                                                    double (&acc)[RPL]) {
+                                                    float (&acc)[RPL]) {
     float va[2][NT];
     float4 ba[2][NT];
     {
@@ -274,7 +274,7 @@ __device__ __forceinline__ void add_leaves_anchored(uint32_t tree, const RecordL
             }
         }
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc[r] += (double)v[t];
+        for (int t = 0; t < NT; ++t) acc[r] += v[t];
         asm volatile("" ::"v"(acc[r]));
     }
 }
@@ -301,13 +301,13 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
     const float xf = column_freq(P, s);
     const float xe = NF == 4 ? P.engine[s] : 0.0f;
     float kv[RPL], bs[RPL];
-    double acc[RPL];
+    float acc[RPL];
 #pragma unroll
     for (int r = 0; r < RPL; ++r) {
         const int32_t j = min(j0 + r, P.H - 1);
         kv[r] = (float)P.kv[s * P.H + j];
         bs[r] = (float)P.batch[s * P.H + j];
-        acc[r] = (double)base;
+        acc[r] = base;
         asm volatile("" ::"v"(kv[r]), "v"(bs[r]));
     }
     asm volatile("" ::"v"(xf), "v"(xe));
@@ -336,7 +336,7 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
     if (valid) {
 #pragma unroll
         for (int r = 0; r < RPL; ++r)
-            if (j0 + r < P.H) P.out[s * P.H + j0 + r] = sync_ok ? (float)acc[r] : __builtin_nanf("");
+            if (j0 + r < P.H) P.out[s * P.H + j0 + r] = sync_ok ? acc[r] : __builtin_nanf("");
     }
 }
 
@@ -356,7 +356,7 @@ __global__ __launch_bounds__(256) void forest_column_global_kernel(const uint2* 
     x[3] = NF == 4 ? P.engine[c.s] : 0.0f;
     const int64_t stride = (int64_t)1 << depth;
     const int32_t n_int = (1 << depth) - 1;
-    double acc = (double)base;
+    float acc = base;
     for (int32_t t = 0; t < n_trees; ++t) {
         const uint2* nd = nodes + t * stride;
         int32_t k = 0;
@@ -365,9 +365,9 @@ __global__ __launch_bounds__(256) void forest_column_global_kernel(const uint2* 
             const float v = x[w.y & 3u];
             k = 2 * k + (v < __uint_as_float(w.x) ? 1 : 2);
         }
-        acc += (double)leaves[t * stride + (k - n_int)];
+        acc += leaves[t * stride + (k - n_int)];
     }
-    P.out[c.s * P.H + c.j[0]] = (float)acc;
+    P.out[c.s * P.H + c.j[0]] = acc;
 }
 
 // Trees per staged block: double buffers within the LDS budget.

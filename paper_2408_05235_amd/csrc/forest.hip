@@ -1,7 +1,7 @@
 // Stage 2: the performance model M (Sec. 4.3.1), a gradient-boosted tree
 // ensemble, evaluated on fp32 feature rows.  Every kernel here computes, for
-// each row, base + the leaf of every tree, accumulated in fp64 in tree order
-// and rounded once to fp32.
+// each row, base + the leaf of every tree as an fp32 running sum in tree
+// order (every add rounded to nearest even).
 //
 // Grid kernels evaluate the rows of the projection grid without
 // materializing them: row (s, f, j) = (freq[f], kv[s][j], batch[s][j]
@@ -14,10 +14,10 @@
 // frequency and engine size are fixed for the lane, so a row inside the box
 // takes every decision of the path the same way.  Between consecutive future
 // iterations KV and batch move little, so most rows cost a box test and one
-// fp64 add per tree; a walk happens on roughly one row in twenty.
+// fp32 add per tree; a walk happens on roughly one row in twenty.
 //
 //   forest_grid_lds_kernel     (depth <= 11) A 1024-thread workgroup (16
-//       wavefronts, 16 x 44 x 64 rows) walks the ensemble in blocks of trees
+//       wavefronts, 16 x 64 x 64 rows) walks the ensemble in blocks of trees
 //       staged in two LDS buffers.  A tree is one record (nodes, leaf values,
 //       leaf boxes), so a block is one contiguous copy, made straight from
 //       global memory into LDS and handed from wavefront to wavefront without
@@ -26,7 +26,7 @@
 //       compares once, all in vector registers (no lane-mask round trip).
 //       Trees are taken in pairs that share one box test (a row that leaves
 //       it walks only the tree whose own box it left), and rows in groups of
-//       four whose (KV, batch) hull is tested before any single row.  The
+//       eight whose (KV, batch) hull is tested before any single row.  The
 //       (scenario, chunk) items are ordered by an estimate of their walks,
 //       so a workgroup's wavefronts do similar work.
 //   forest_grid_global_kernel  (deeper trees) The same per-lane scheme with
@@ -86,9 +86,9 @@ __global__ __launch_bounds__(256) void forest_rows_kernel(const uint2* __restric
             for (int c = 0; c < NF; ++c) x[r][c] = rows[(r0 + r) * NF + c];
         }
     }
-    double acc[RPT];
+    float acc[RPT];
 #pragma unroll
-    for (int r = 0; r < RPT; ++r) acc[r] = (double)base;
+    for (int r = 0; r < RPT; ++r) acc[r] = base;
     const int32_t n_int = (1 << depth) - 1;
     const int32_t n_leaf = 1 << depth;
     for (int32_t t = 0; t < n_trees; ++t) {
@@ -106,21 +106,21 @@ __global__ __launch_bounds__(256) void forest_rows_kernel(const uint2* __restric
             }
         }
 #pragma unroll
-        for (int r = 0; r < RPT; ++r) acc[r] += (double)lt[k[r] - n_int];
+        for (int r = 0; r < RPT; ++r) acc[r] += lt[k[r] - n_int];
     }
 #pragma unroll
     for (int r = 0; r < RPT; ++r)
-        if (r < nr) out[r0 + r] = (float)acc[r];
+        if (r < nr) out[r0 + r] = acc[r];
 }
 
 #ifndef TL_LDS_J
-#define TL_LDS_J 44
+#define TL_LDS_J 64
 #endif
 #ifndef TL_LDS_WAVES
 #define TL_LDS_WAVES 16
 #endif
 #ifndef TL_LDS_BUDGET_KIB
-#define TL_LDS_BUDGET_KIB 152
+#define TL_LDS_BUDGET_KIB 160
 #endif
 #ifndef TL_LDS_WAVES_PER_SIMD
 #define TL_LDS_WAVES_PER_SIMD 4
@@ -226,7 +226,7 @@ __device__ __forceinline__ float to_sgpr(float x) {
 }
 
 #ifndef TL_ROW_GROUP
-#define TL_ROW_GROUP 4
+#define TL_ROW_GROUP 8
 #endif
 constexpr int kRowGroup = TL_ROW_GROUP;   // rows whose (KV, batch) hull is tested as one
 
@@ -244,7 +244,7 @@ template <int NF, int J, int NT>
 __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tree_off, const RecordLayout& R,
                                            int32_t depth,
                                            const float4* kv4, const float (&hull)[J / kRowGroup][4], float xf,
-                                           float xe, double (&acc)[J]) {
+                                           float xe, float (&acc)[J]) {
     static_assert(J % kRowGroup == 0, "whole row groups");
     static_assert(NT == 1 || NT == 2, "one tree or a pair");
     // the pairs are re-read from LDS for each group that needs them rather
@@ -256,18 +256,18 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
     // a pair's own leaf boxes, decoded, beside their intersection: after a
     // walk only the walked tree's box is read again
     float4 box, b0, b1 = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
-    double v[NT];
+    float v[NT];
     {
         // the chunk's first row walks every tree on every lane, outside the
         // group loop so that the loop's walks carry no first-row case
         const float4 q0 = kv4[0];
         LeafAt k[NT];
         walk<NF, NT>(tree_addr, R, depth, xf, q0.x, q0.y, xe, k);
-        v[0] = (double)leaf_value(k[0]);
+        v[0] = leaf_value(k[0]);
         b0 = leaf_box(k[0]);
         box = b0;
         if (NT == 2) {
-            v[NT - 1] = (double)leaf_value(k[NT - 1]);
+            v[NT - 1] = leaf_value(k[NT - 1]);
             b1 = leaf_box(k[NT - 1]);
             box = box_meet(b0, b1);
         }
@@ -295,7 +295,7 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
                     if (NT == 1) {
                         LeafAt k[1];
                         walk<NF, 1>(tree_addr, R, depth, xf, kv, bs, xe, k);
-                        v[0] = (double)leaf_value(k[0]);
+                        v[0] = leaf_value(k[0]);
                         box = leaf_box(k[0]);
                     } else {
                         const bool n0 = !in_box(b0, kv, bs);
@@ -304,24 +304,24 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
                             LeafAt k[2];
                             walk<NF, 2>(tree_addr, R, depth, xf, kv, bs, xe, k);
                             if (n0) {
-                                v[0] = (double)leaf_value(k[0]);
+                                v[0] = leaf_value(k[0]);
                                 b0 = leaf_box(k[0]);
                             }
                             if (n1) {
-                                v[NT - 1] = (double)leaf_value(k[1]);
+                                v[NT - 1] = leaf_value(k[1]);
                                 b1 = leaf_box(k[1]);
                             }
                         } else {
                             if (n0) {
                                 LeafAt k[1];
                                 walk<NF, 1>(tree_addr, R, depth, xf, kv, bs, xe, k);
-                                v[0] = (double)leaf_value(k[0]);
+                                v[0] = leaf_value(k[0]);
                                 b0 = leaf_box(k[0]);
                             }
                             if (n1) {
                                 LeafAt k[1];
                                 walk<NF, 1>(tree1, R, depth, xf, kv, bs, xe, k);
-                                v[NT - 1] = (double)leaf_value(k[0]);
+                                v[NT - 1] = leaf_value(k[0]);
                                 b1 = leaf_box(k[0]);
                             }
                         }
@@ -329,7 +329,7 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
                     }
                 }
             }
-            double& a = acc[gi * kRowGroup + i];
+            float& a = acc[gi * kRowGroup + i];
 #pragma unroll
             for (int t = 0; t < NT; ++t) a += v[t];
             // consume the sum here so the adds are not sunk past later walks
@@ -364,17 +364,17 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
     float2* kvb = (float2*)(smem + 2 * buf_bytes) + wave * J;
     StageSync* sync = (StageSync*)(smem + 2 * buf_bytes + (size_t)kLdsWaves * J * sizeof(float2));
     if (threadIdx.x == 0) stage_sync_init(sync);
-    if (lane < J) {
-        const int32_t j = g.j0 + min(lane, g.nj - 1);
-        kvb[lane] = make_float2((float)P.kv[g.s * H + j], (float)P.batch[g.s * H + j]);
+    for (int r = lane; r < J; r += kWave) {
+        const int32_t j = g.j0 + min(r, g.nj - 1);
+        kvb[r] = make_float2((float)P.kv[g.s * H + j], (float)P.batch[g.s * H + j]);
     }
 
     // staging: block 0 by every wavefront before the barrier, the others
     // handed over without barriers (stage_acquire / stage_release)
     const int32_t n_blocks = (n_trees + tb - 1) / tb;
-    double acc[J];
+    float acc[J];
 #pragma unroll
-    for (int jj = 0; jj < J; ++jj) acc[jj] = (double)base;
+    for (int jj = 0; jj < J; ++jj) acc[jj] = base;
 
     // Make the lane's frequency / engine size complete here, before any
     // staging copy is in flight: otherwise the walks inside the loop would
@@ -426,7 +426,7 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
         float* o = P.out + ((int64_t)g.s * F + g.f) * H + g.j0;
 #pragma unroll
         for (int jj = 0; jj < J; ++jj)
-            if (jj < g.nj) o[jj] = sync_ok ? (float)acc[jj] : __builtin_nanf("");
+            if (jj < g.nj) o[jj] = sync_ok ? acc[jj] : __builtin_nanf("");
     }
 }
 
@@ -456,9 +456,9 @@ __global__ __launch_bounds__(256) void forest_grid_global_kernel(const uint2* __
     __syncthreads();
     if (!g.valid) return;
 
-    double acc[J];
+    float acc[J];
 #pragma unroll
-    for (int jj = 0; jj < J; ++jj) acc[jj] = (double)base;
+    for (int jj = 0; jj < J; ++jj) acc[jj] = base;
     const int32_t n_int = (1 << depth) - 1;
     const int32_t n_leaf = 1 << depth;
     for (int32_t t = 0; t < n_trees; ++t) {
@@ -466,7 +466,7 @@ __global__ __launch_bounds__(256) void forest_grid_global_kernel(const uint2* __
         const float* lv = leaves + (int64_t)t * n_leaf;
         const float4* bx = boxes + (int64_t)t * n_leaf;
         float lo_k = INFINITY, hi_k = -INFINITY, lo_b = INFINITY, hi_b = -INFINITY;
-        double val = 0.0;
+        float val = 0.0f;
 #pragma unroll
         for (int jj = 0; jj < J; ++jj) {
             const float2 v2 = kvb[wave][jj];
@@ -479,7 +479,7 @@ __global__ __launch_bounds__(256) void forest_grid_global_kernel(const uint2* __
                     k = 2 * k + ((x < __uint_as_float(nd.x)) ? 1 : 2);
                 }
                 const int32_t leaf = k - n_int;
-                val = (double)lv[leaf];
+                val = lv[leaf];
                 const float4 b = bx[leaf];
                 lo_k = b.x;
                 hi_k = b.y;
@@ -493,7 +493,7 @@ __global__ __launch_bounds__(256) void forest_grid_global_kernel(const uint2* __
         float* o = P.out + ((int64_t)g.s * F + g.f) * H + g.j0;
 #pragma unroll
         for (int jj = 0; jj < J; ++jj)
-            if (jj < g.nj) o[jj] = (float)acc[jj];
+            if (jj < g.nj) o[jj] = acc[jj];
     }
 }
 

@@ -3,7 +3,8 @@
 // fixed list of candidate frequencies, a few engine sizes, integer batch
 // sizes and integer KV-cache blocks.  Every lattice point's value is the
 // ensemble's output computed by the grid kernel (the same tree walks and the
-// same tree-order fp64 sums), so a lookup returns exactly what a walk would.
+// same fp32 running sums in tree order), so a lookup returns exactly what a
+// walk would.
 //
 // Layout: value(e, b, kv, f) at (((e * nB + b) * nC * kHc + kv) * F + f): the
 // F frequencies of one lattice point are contiguous, so a row of the
@@ -67,11 +68,11 @@ __global__ __launch_bounds__(256) void lattice_transpose_kernel(const float* __r
     }
 }
 
-// tree-order fp64 sum over heap-ordered trees in global memory
+// fp32 running sum in tree order over heap-ordered trees in global memory
 __device__ __forceinline__ float walk_global(const ForestDev& f, const float (&x)[4]) {
     const int64_t stride = (int64_t)1 << f.depth;
     const int32_t n_int = (1 << f.depth) - 1;
-    double acc = (double)f.base_score;
+    float acc = f.base_score;
     for (int32_t t = 0; t < f.n_trees; ++t) {
         const uint2* nd = f.nodes + t * stride;
         int32_t k = 0;
@@ -79,9 +80,9 @@ __device__ __forceinline__ float walk_global(const ForestDev& f, const float (&x
             const uint2 w = nd[k];
             k = 2 * k + (x[w.y & 3u] < __uint_as_float(w.x) ? 1 : 2);
         }
-        acc += (double)f.leaves[t * stride + (k - n_int)];
+        acc += f.leaves[t * stride + (k - n_int)];
     }
-    return (float)acc;
+    return acc;
 }
 
 constexpr int kGatherThreads = 256;

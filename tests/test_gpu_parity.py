@@ -310,7 +310,7 @@ def test_forest_random(gpu, T, d, nf, n):
     torch.cuda.synchronize()
     exp = oracle.forest_predict(fd, x)
     exact = assert_ips_close(got, exp, f"T={T} d={d}")
-    assert exact == n      # tree-order fp64 accumulation on both sides
+    assert exact == n      # fp32 running sums in tree order on both sides
 
 
 def test_forest_rows_at_an_offset(gpu):
@@ -345,7 +345,9 @@ def random_curves(rng, S, H, kvmax=5000, bmax=300):
 @pytest.mark.parametrize("S,F,H,T,d,nf", [(3, 64, 1024, 40, 10, 4), (5, 17, 100, 30, 6, 3), (2, 130, 70, 20, 8, 3),
                                           (4, 48, 33, 25, 8, 3), (1, 1, 1, 3, 2, 4), (2, 64, 64, 0, 4, 3),
                                           (3, 32, 95, 10, 0, 3), (2, 20, 40, 150, 3, 3), (3, 64, 50, 7, 12, 4),
-                                          (2, 40, 77, 5, 13, 3), (1, 64, 37, 3, 14, 4)])
+                                          (2, 40, 77, 5, 13, 3), (1, 64, 37, 3, 14, 4),
+                                          # several 64-iteration chunks with ragged tails of 8 and 1 rows
+                                          (3, 64, 200, 40, 10, 3), (2, 70, 129, 33, 8, 4), (4, 64, 65, 21, 9, 3)])
 def test_forest_grid(gpu, S, F, H, T, d, nf):
     """The fused grid kernel equals the oracle on the rows it stands for."""
     import torch

@@ -439,11 +439,16 @@ def test_forest_closed_forms():
     leaf = rng.normal(size=(7, 1 << d)).astype(np.float32)
     f_in = _forest(7, d, 3, 1, np.inf, 0, base=1.5)
     f_in["leaf"] = leaf
-    assert np.array_equal(oracle.forest_predict(f_in, X),
-                          np.full(100, np.float32(1.5 + leaf[:, 0].astype(np.float64).sum())))
+    # every row reaches leaf 0 (all thresholds +inf: always left) or the last
+    # leaf (-inf: always right) of every tree; the sum runs in fp32, tree order
+    def running_sum(base, vals):
+        acc = np.float32(base)
+        for v in vals:
+            acc = np.float32(acc + v)
+        return acc
+    assert np.array_equal(oracle.forest_predict(f_in, X), np.full(100, running_sum(1.5, leaf[:, 0])))
     f_in["threshold"][:] = -np.inf
-    assert np.array_equal(oracle.forest_predict(f_in, X),
-                          np.full(100, np.float32(1.5 + leaf[:, -1].astype(np.float64).sum())))
+    assert np.array_equal(oracle.forest_predict(f_in, X), np.full(100, running_sum(1.5, leaf[:, -1])))
     same = _forest(300, 3, 3, 2, 10.0, 0.5, base=2.0)
     assert np.all(oracle.forest_predict(same, X) == np.float32(2.0 + 0.5 * 300))
     # depth-1 stump on the frequency: closed form
@@ -452,7 +457,7 @@ def test_forest_closed_forms():
     assert np.array_equal(got, np.where(X[:, 0] < 1500.0, 3.0, 7.0).astype(np.float32))
 
 
-def test_forest_tie_nan_depth0_and_fp64_sum():
+def test_forest_tie_nan_depth0_and_fp32_running_sum():
     stump = _forest(1, 1, 3, 1, 100.0, [1.0, 2.0])
     x = np.array([[1000, 100, 0], [1000, 99.99999, 0], [1000, np.nan, 0]], np.float32)
     assert oracle.forest_predict(stump, x).tolist() == [2.0, 1.0, 2.0]   # x == thr and NaN go right
@@ -460,10 +465,27 @@ def test_forest_tie_nan_depth0_and_fp64_sum():
               feature=np.zeros((3, 0), np.uint8), threshold=np.zeros((3, 0), np.float32),
               leaf=np.array([[0.25], [0.5], [1.0]], np.float32))
     assert oracle.forest_predict(d0, x).tolist() == [2.75] * 3
-    # accumulated in fp64, rounded once: 1 + 3*2^-25 rounds to 1 + 2^-23
-    # (an fp32 running sum would stay at 1.0)
+    # an fp32 running sum from the base: each 2^-25 is below half an ulp of
+    # 1.0 and is lost (fp64 accumulation would give 1 + 3*2^-25 -> 1 + 2^-23)
     tiny = _forest(3, 1, 3, 0, 0.0, [2.0 ** -25, 2.0 ** -25], base=1.0)
-    assert oracle.forest_predict(tiny, x[:1])[0] == np.nextafter(np.float32(1), np.float32(2))
+    assert oracle.forest_predict(tiny, x[:1])[0] == np.float32(1.0)
+    # 1 + 2^-24 is a tie that rounds to even (1.0), twice; the two leaves
+    # added first would give 1 + 2^-23 exactly: the base comes first and the
+    # trees follow in order
+    tie = _forest(2, 1, 3, 0, 0.0, [2.0 ** -24, 2.0 ** -24], base=1.0)
+    assert oracle.forest_predict(tie, x[:1])[0] == np.float32(1.0)
+    # tree order: 2^24 + 1 - 2^24 is 0 in fp32 (2^24 + 1 rounds to 2^24),
+    # the reverse order 1 - 2^24 + 2^24 is 1
+    fwd = _forest(3, 1, 3, 0, 0.0, [0.0, 0.0])
+    fwd["leaf"] = np.array([[2.0 ** 24] * 2, [1.0] * 2, [-(2.0 ** 24)] * 2], np.float32)
+    assert oracle.forest_predict(fwd, x[:1])[0] == np.float32(0.0)
+    rev = dict(fwd, leaf=fwd["leaf"][::-1].copy())
+    assert oracle.forest_predict(rev, x[:1])[0] == np.float32(1.0)
+    # a running sum that crosses 2^24: (2^24 - 1) + 1 + 1 + 1 is exactly
+    # 2^24 + 2 (representable), but after the first add every 2^24 + 1 rounds
+    # back to 2^24 (even)
+    cross = _forest(3, 1, 3, 0, 0.0, [1.0, 1.0], base=2.0 ** 24 - 1)
+    assert oracle.forest_predict(cross, x[:1])[0] == np.float32(2.0 ** 24)
 
 
 def test_forest_rejects_bad_feature():

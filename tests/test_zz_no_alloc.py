@@ -58,7 +58,7 @@ def test_noalloc_refuses_grids_beyond_its_scratch(gpu):
     rng = np.random.default_rng(3)
     fd = synth.make_forest(rng, 4, 10, 3, "profile", 40.0, 65536, 128, synth.frequency_grid(8))
     f = api.Forest.from_dict(fd)
-    S, H = 65536, 1024                      # 2^21 (scenario, chunk) pairs: 32 MiB for the arrays alone
+    S, H = 65536, 2048                      # 2^21 (scenario, chunk) pairs: 32 MiB for the arrays alone
     kv = torch.zeros((S, H), dtype=torch.int32, device="cuda")
     bs = torch.zeros((S, H), dtype=torch.int32, device="cuda")
     freqs = torch.tensor([1500.0], dtype=torch.float32, device="cuda")
