@@ -29,11 +29,18 @@ __device__ __forceinline__ bool in_box(const float4& b, float kv, float bs) {
     return (kv >= b.x) & (kv < b.y) & (bs >= b.z) & (bs < b.w);
 }
 
-// The intersection of two leaf boxes.  Box bounds are decoded integers or
-// infinities, never NaN, so fmaxf / fminf (one instruction each) give what
-// comparisons would.
+// The intersection of two decoded leaf boxes.  Their bounds are
+// non-negative integers as floats, whose bit patterns order like the values,
+// so an integer max / min (one instruction each; fmaxf / fminf would first
+// canonicalize both operands) gives the float max / min exactly.
+__device__ __forceinline__ float bound_max(float a, float b) {
+    return __int_as_float(max(__float_as_int(a), __float_as_int(b)));
+}
+__device__ __forceinline__ float bound_min(float a, float b) {
+    return __int_as_float(min(__float_as_int(a), __float_as_int(b)));
+}
 __device__ __forceinline__ float4 box_meet(const float4& a, const float4& b) {
-    return make_float4(fmaxf(a.x, b.x), fminf(a.y, b.y), fmaxf(a.z, b.z), fminf(a.w, b.w));
+    return make_float4(bound_max(a.x, b.x), bound_min(a.y, b.y), bound_max(a.z, b.z), bound_min(a.w, b.w));
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));

@@ -347,7 +347,9 @@ def random_curves(rng, S, H, kvmax=5000, bmax=300):
                                           (3, 32, 95, 10, 0, 3), (2, 20, 40, 150, 3, 3), (3, 64, 50, 7, 12, 4),
                                           (2, 40, 77, 5, 13, 3), (1, 64, 37, 3, 14, 4),
                                           # several 64-iteration chunks with ragged tails of 8 and 1 rows
-                                          (3, 64, 200, 40, 10, 3), (2, 70, 129, 33, 8, 4), (4, 64, 65, 21, 9, 3)])
+                                          (3, 64, 200, 40, 10, 3), (2, 70, 129, 33, 8, 4), (4, 64, 65, 21, 9, 3),
+                                          # depth 11: one tree per staged block (every tree a single)
+                                          (2, 64, 130, 7, 11, 3)])
 def test_forest_grid(gpu, S, F, H, T, d, nf):
     """The fused grid kernel equals the oracle on the rows it stands for."""
     import torch
@@ -363,6 +365,54 @@ def test_forest_grid(gpu, S, F, H, T, d, nf):
     torch.cuda.synchronize()
     exp = oracle.forest_predict(fd, oracle.rows(freqs, bs, kv, eng, nf))
     assert assert_ips_close(got, exp, "grid") == exp.size
+
+
+def _order_sensitive_forest(rng, T, d, nf):
+    """Random trees whose leaves make the fp32 running sum depend on its
+    order: trees 3k add +2^24, trees 3k+1 a random value in (-4, 4) with a
+    fraction, trees 3k+2 subtract 2^24, so every middle value is rounded to
+    the 2-unit spacing at 2^24 before it is taken out again."""
+    fd = random_forest(rng, T, d, nf)
+    leaf = fd["leaf"]
+    leaf[0::3] = np.float32(2.0 ** 24)
+    leaf[1::3] = (rng.uniform(-4, 4, leaf[1::3].shape) + 0.25).astype(np.float32)
+    leaf[2::3] = np.float32(-(2.0 ** 24))
+    fd["base_score"] = np.float32(0.75)
+    return fd
+
+
+@pytest.mark.parametrize("T,d,nf", [(61, 8, 3), (31, 10, 4)])
+def test_forest_sum_order_is_tree_order(gpu, T, d, nf):
+    """fp32 running sums in tree order on every forest path: a forest whose
+    result changes with the order of the adds gives the oracle's values on
+    the row walks and on the grid kernel (both wide and with a short tail)."""
+    import torch
+    api = _api()
+    rng = np.random.default_rng(T + d)
+    fd = _order_sensitive_forest(rng, T, d, nf)
+    x = random_rows(rng, 4099, nf)
+    x[np.isnan(x)] = 1500.0
+    exp_rows = oracle.forest_predict(fd, x)
+    # the test can tell orders apart: an fp64 sum differs on most rows
+    f64 = np.full(x.shape[0], np.float64(fd["base_score"]))
+    for t in range(T):
+        sub = dict(fd, n_trees=1, feature=fd["feature"][t:t + 1], threshold=fd["threshold"][t:t + 1],
+                   leaf=fd["leaf"][t:t + 1], base_score=np.float32(0))
+        f64 += oracle.forest_predict(sub, x).astype(np.float64)
+    assert np.mean(f64.astype(np.float32) != exp_rows) > 0.5
+    f = api.Forest.from_dict(fd)
+    got = _np(f.tl_forest_predict(torch.from_numpy(x).cuda()))
+    torch.cuda.synchronize()
+    assert np.array_equal(got, exp_rows)
+    S, F, H = 3, 64, 131
+    kv, bs = random_curves(rng, S, H)
+    freqs = synth.frequency_grid(F)
+    eng = rng.choice([1.0, 2.0, 4.0, 8.0], S).astype(np.float32) if nf == 4 else None
+    t = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    grid = _np(f.tl_forest_predict_grid(t(freqs), t(kv), t(bs), t(eng)))
+    torch.cuda.synchronize()
+    assert np.array_equal(grid, oracle.forest_predict(fd, oracle.rows(freqs, bs, kv, eng, nf)))
+    f.close()
 
 
 def test_forest_grid_nan_and_infinite_thresholds(gpu):
