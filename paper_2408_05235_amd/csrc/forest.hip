@@ -18,7 +18,7 @@
 //
 //   forest_grid_lds_kernel     (depth <= 11) A 1024-thread workgroup (16
 //       wavefronts, 16 x 64 x 64 rows) walks the ensemble in blocks of trees
-//       staged in two LDS buffers.  A tree is one record (nodes, leaf values,
+//       staged in three LDS buffers.  A tree is one record (nodes, leaf values,
 //       leaf boxes), so a block is one contiguous copy, made straight from
 //       global memory into LDS and handed from wavefront to wavefront without
 //       block barriers (stage_acquire / stage_release).  Tree walks read LDS
@@ -122,6 +122,9 @@ __global__ __launch_bounds__(256) void forest_rows_kernel(const uint2* __restric
 #ifndef TL_LDS_BUDGET_KIB
 #define TL_LDS_BUDGET_KIB 160
 #endif
+// Tree buffers: three blocks of 2 trees at depth 10 (against two of 3) let a
+// wavefront run two blocks ahead of the slowest and pair every tree.
+constexpr int kLdsBuffers = 3;
 #ifndef TL_LDS_WAVES_PER_SIMD
 #define TL_LDS_WAVES_PER_SIMD 4
 #endif
@@ -362,9 +365,9 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
     const float xe = (NF == 4) ? P.engine[g.s] : 0.0f;
     // the J (KV, batch) pairs of this wavefront are the same for every lane;
     // they sit in LDS after the two tree buffers and are read as broadcasts
-    float2* kvb = (float2*)(smem + 2 * buf_bytes) + wave * J;
-    StageSync* sync = (StageSync*)(smem + 2 * buf_bytes + (size_t)kLdsWaves * J * sizeof(float2));
-    if (threadIdx.x == 0) stage_sync_init(sync);
+    float2* kvb = (float2*)(smem + kLdsBuffers * buf_bytes) + wave * J;
+    StageSync* sync = (StageSync*)(smem + kLdsBuffers * buf_bytes + (size_t)kLdsWaves * J * sizeof(float2));
+    if (threadIdx.x == 0) stage_sync_init<kLdsBuffers>(sync);
     for (int r = lane; r < J; r += kWave) {
         const int32_t j = g.j0 + min(r, g.nj - 1);
         kvb[r] = make_float2((float)P.kv[g.s * H + j], (float)P.batch[g.s * H + j]);
@@ -405,10 +408,10 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
     }
     bool sync_ok = true;
     for (int32_t b = 0; b < n_blocks; ++b) {
-        const int cur = b & 1;
+        const int cur = b % kLdsBuffers;
         if (b > 0)
-            sync_ok &= stage_acquire(sync, b, kLdsWaves, records, n_trees, tb, rec_words,
-                                     lds_addr(smem + cur * buf_bytes));
+            sync_ok &= stage_acquire<kLdsBuffers>(sync, b, kLdsWaves, records, n_trees, tb, rec_words,
+                                                  lds_addr(smem + cur * buf_bytes));
         if (g.valid) {
             const int32_t cnt = min(tb, n_trees - b * tb);
             const uint32_t bp = cur * buf_bytes;
@@ -421,7 +424,7 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
                 eval_trees<NF, J, 2>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
             if (tt < cnt) eval_trees<NF, J, 1>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
         }
-        stage_release(sync, b, kLdsWaves);
+        stage_release<kLdsBuffers>(sync, b, kLdsWaves);
     }
     if (active) {
         float* o = P.out + ((int64_t)g.s * F + g.f) * H + g.j0;
@@ -518,11 +521,11 @@ int32_t lds_trees_per_block(const ForestDev& f, size_t* lds_bytes) {
     const RecordLayout R = record_layout(f.depth);
     const size_t head = (size_t)kLdsWaves * kLdsJ * sizeof(float2) + sizeof(StageSync);
     const size_t budget = (size_t)TL_LDS_BUDGET_KIB * 1024;
-    auto fits = [&](int32_t tb) { return 2 * (size_t)stage_buffer_bytes(tb, R) + head <= budget; };
+    auto fits = [&](int32_t tb) { return kLdsBuffers * (size_t)stage_buffer_bytes(tb, R) + head <= budget; };
     int32_t tb = 64;
     while (tb > 1 && !fits(tb)) --tb;
     if (!fits(tb)) return 0;
-    *lds_bytes = 2 * (size_t)stage_buffer_bytes(tb, R) + head;
+    *lds_bytes = kLdsBuffers * (size_t)stage_buffer_bytes(tb, R) + head;
     return tb;
 }
 

@@ -129,16 +129,16 @@ __device__ __forceinline__ void stage_block(const uint4* records, int32_t n_tree
     }
 }
 
-// Hand-over of two LDS buffers of tree blocks between the wavefronts of a
-// workgroup without block barriers.  Block b lives in buffer b & 1; block 0
+// Hand-over of NB LDS buffers of tree blocks between the wavefronts of a
+// workgroup without block barriers.  Block b lives in buffer b % NB; block 0
 // is copied by every wavefront before the workgroup's one barrier.  Per
 // buffer: `claimed` = the last block a wavefront took on to copy into it,
 // `ready` = the last block whose copy is complete, `done` = how many
 // (wavefront, block) pairs have finished with it.  The first wavefront that
 // needs block b and finds it unclaimed claims it, waits until every
-// wavefront has finished block b - 2 (the buffer's previous occupant),
+// wavefront has finished block b - NB (the buffer's previous occupant),
 // copies the whole block, waits for its copy and publishes `ready`; the others
-// wait for `ready`.  A wavefront can thus run up to a block ahead of the
+// wait for `ready`.  A wavefront can thus run up to NB - 1 blocks ahead of the
 // slowest one instead of meeting it at every block.  Issue priority follows
 // the order in which wavefronts finish a block: the later a wavefront leaves
 // block b among its workgroup's, the higher its priority (s_setprio) while it
@@ -147,20 +147,24 @@ __device__ __forceinline__ void stage_block(const uint4* records, int32_t n_tree
 // otherwise keep winning issue and the youngest set the pace.  Every wait is
 // bounded (kSyncSpins sleeps); one that runs out makes stage_acquire return
 // false, and the caller marks its results invalid, so every wavefront ends.
+constexpr int kMaxStageBuffers = 3;
 struct StageSync {
-    int32_t claimed[2];
-    int32_t ready[2];
-    int32_t done[2];
+    int32_t claimed[kMaxStageBuffers];
+    int32_t ready[kMaxStageBuffers];
+    int32_t done[kMaxStageBuffers];
 };
 constexpr int32_t kSyncSpins = 1 << 20;
 
+template <int NB = 2>
 __device__ __forceinline__ void stage_sync_init(StageSync* sync) {
     sync->claimed[0] = 0;   // block 0: copied by every wavefront
     sync->ready[0] = 0;
-    sync->claimed[1] = -1;
-    sync->ready[1] = -1;
     sync->done[0] = 0;
-    sync->done[1] = 0;
+    for (int i = 1; i < NB; ++i) {
+        sync->claimed[i] = i - NB;   // block i claims buffer i from "block i - NB"
+        sync->ready[i] = -1;
+        sync->done[i] = 0;
+    }
 }
 
 __device__ __forceinline__ int32_t sync_load(const int32_t* p) {
@@ -170,17 +174,18 @@ __device__ __forceinline__ int32_t sync_load(const int32_t* p) {
 // Makes block b >= 1 (trees [b*tb, ...), rec_words 16-byte words per tree)
 // available in its buffer at LDS byte address buf; n_waves wavefronts share
 // the buffers.
+template <int NB = 2>
 __device__ __forceinline__ bool stage_acquire(StageSync* sync, int32_t b, int n_waves, const uint4* records,
                                               int32_t n_trees, int32_t tb, uint32_t rec_words, uint32_t buf) {
-    const int cur = b & 1;
-    const int32_t need_done = n_waves * (b >> 1);
+    const int cur = b % NB;
+    const int32_t need_done = n_waves * (b / NB);
     int32_t spins = 0;
     if (sync_load(&sync->ready[cur]) != b) __builtin_amdgcn_s_setprio(0);   // ahead of the others
     while (sync_load(&sync->ready[cur]) != b && spins < kSyncSpins) {
         int32_t won = 0;
-        if (sync_load(&sync->claimed[cur]) == b - 2) {
+        if (sync_load(&sync->claimed[cur]) == b - NB) {
             if (lane_id() == 0) {
-                int32_t expect = b - 2;
+                int32_t expect = b - NB;
                 won = __hip_atomic_compare_exchange_strong(&sync->claimed[cur], &expect, b, __ATOMIC_ACQ_REL,
                                                            __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
             }
@@ -204,11 +209,12 @@ __device__ __forceinline__ bool stage_acquire(StageSync* sync, int32_t b, int n_
 
 // This wavefront has finished with block b (its reads have all returned);
 // n_waves share the buffers.
+template <int NB = 2>
 __device__ __forceinline__ void stage_release(StageSync* sync, int32_t b, int n_waves) {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     int32_t before = 0;
     if (lane_id() == 0)
-        before = __hip_atomic_fetch_add(&sync->done[b & 1], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        before = __hip_atomic_fetch_add(&sync->done[b % NB], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     // how many wavefronts left block b before this one, in quarters
     const int32_t quarter = 4 * (__builtin_amdgcn_readfirstlane(before) % n_waves) / n_waves;
     if (quarter == 3) __builtin_amdgcn_s_setprio(3);
