@@ -349,7 +349,10 @@ def random_curves(rng, S, H, kvmax=5000, bmax=300):
                                           # several 64-iteration chunks with ragged tails of 8 and 1 rows
                                           (3, 64, 200, 40, 10, 3), (2, 70, 129, 33, 8, 4), (4, 64, 65, 21, 9, 3),
                                           # depth 11: one tree per staged block (every tree a single)
-                                          (2, 64, 130, 7, 11, 3)])
+                                          (2, 64, 130, 7, 11, 3),
+                                          # depth 10 (two-tree blocks in three buffers): one tree, one
+                                          # pair, an odd count whose last block holds a single tree
+                                          (2, 33, 70, 1, 10, 4), (3, 64, 100, 2, 10, 3), (2, 64, 150, 5, 10, 4)])
 def test_forest_grid(gpu, S, F, H, T, d, nf):
     """The fused grid kernel equals the oracle on the rows it stands for."""
     import torch
