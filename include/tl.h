@@ -190,9 +190,10 @@ tl_status tl_adjust_lengths(int64_t n_scenarios, int64_t n_requests, const int64
  * on the order).  The order takes 4 bytes per scenario of device scratch
  * that the library owns, one per device: allocated on the first such call,
  * kept, and replaced only when more scenarios come.  If that allocation
- * fails the scenarios run in their own order (same results).  Calls share
- * it: a call on another stream than the previous one first waits (on the
- * device) for the previous projection.
+ * fails the scenarios run in their own order (same results), as they do
+ * while the stream is being captured into a graph.  Calls share it: a call
+ * on another stream than the previous one first waits (on the device) for
+ * the previous projection.
  * ---------------------------------------------------------------------- */
 typedef struct tl_project_args {
     uint32_t struct_size;          /* sizeof(tl_project_args) */
@@ -247,8 +248,10 @@ tl_status tl_forest_predict(const tl_forest* forest, const float* rows, int64_t 
  * plus a radix sort's temporary storage of device scratch, which the forest
  * handle owns: it is allocated
  * on the first call, kept, and replaced only when a larger grid comes, so
- * repeated calls of one size allocate nothing.  If that allocation fails the
- * call runs without the ordering (same results).  Calls with one forest
+ * repeated calls of one size allocate nothing.  If that allocation fails, or
+ * the stream is being captured into a graph, the call runs without the
+ * ordering (same results; tl_forest_predict_grid_noalloc keeps it under
+ * capture).  Calls with one forest
  * share its scratch: a call on another stream than the previous one first
  * waits (on the device) for the previous call's work.  The forest's device
  * must be the current device.

@@ -208,16 +208,29 @@ void tl_forest_destroy(tl_forest* f) {
 
 namespace {
 
+// Whether `st` is being captured into a graph.  The optional workspaces are
+// then left out: growing them allocates, and handing them between streams
+// waits on events recorded outside the capture.  (A failed query counts as
+// capturing: leaving the workspace out only costs speed.)
+bool capturing(hipStream_t st) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) != hipSuccess) {
+        (void)hipGetLastError();
+        return true;
+    }
+    return cs != hipStreamCaptureStatusNone;
+}
+
 // The grid kernel with the forest's cached work-order workspace.  In the
 // steady state nothing is allocated; a larger grid than any before replaces
 // the workspace (after the last call that used it is done).  Without a
-// workspace (allocation failed) the kernel runs without the order, which
-// changes only its speed.
+// workspace (allocation failed, or the stream is being captured) the kernel
+// runs without the order, which changes only its speed.
 hipError_t grid_with_workspace(const tl_forest* f, const tl::GridParams& g, hipStream_t st) {
     size_t need = 0;
     hipError_t e = tl::grid_order_bytes(f->dev, g, &need);
     if (e != hipSuccess) return e;
-    if (need == 0) return tl::launch_forest_grid(f->dev, g, nullptr, 0, st);
+    if (need == 0 || capturing(st)) return tl::launch_forest_grid(f->dev, g, nullptr, 0, st);
     std::lock_guard<std::mutex> lock(f->ws_mutex);
     if (need > f->ws_bytes) {
         if (f->ws) {
@@ -317,7 +330,8 @@ tl_status project_params(const tl_project_args* a, const char* who, bool with_ro
 // allocated on first use and replaced only by a larger one.  A call on
 // another stream than the previous user first waits (on the device) for that
 // user's projection.  Without the workspace (allocation failure, device
-// number out of range) the scenarios run in their own order: same results.
+// number out of range, a stream being captured) the scenarios run in their
+// own order: same results.
 constexpr int kOrderDevices = 64;
 struct OrderWorkspace {
     std::mutex m;
@@ -332,7 +346,7 @@ OrderWorkspace g_order_ws[kOrderDevices];
 hipError_t project_launch(tl::ProjectParams p, hipStream_t st) {
     const size_t need = tl::project_order_bytes(p);
     int dev = -1;
-    if (need == 0 || hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kOrderDevices)
+    if (need == 0 || capturing(st) || hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kOrderDevices)
         return tl::launch_project(p, st);
     OrderWorkspace& w = g_order_ws[dev];
     std::lock_guard<std::mutex> lock(w.m);
