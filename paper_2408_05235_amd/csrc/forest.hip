@@ -241,8 +241,8 @@ constexpr int kRowGroup = TL_ROW_GROUP;   // rows whose (KV, batch) hull is test
 // intersection of the boxes.  A group whose hull lies inside that
 // intersection on every lane needs only its adds; other groups test row by
 // row.  A lane whose row leaves the intersection walks only the trees whose
-// own box it left, one after the other, and reads the new leaves' values and
-// boxes.
+// own box it left (both in one pass when the wavefront needs both) and reads
+// the new leaves' values and boxes.
 template <int NF, int J, int NT>
 __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tree_off, const RecordLayout& R,
                                            int32_t depth,
@@ -301,34 +301,33 @@ __device__ __forceinline__ void eval_trees(const unsigned char* lds, uint32_t tr
                         v[0] = leaf_value(k[0]);
                         box = leaf_box(k[0]);
                     } else {
-                        // the trees whose own box the row left (at least
-                        // one: the row left their intersection), walked
-                        // through a single walk site: a lane walks the
-                        // first tree it needs, then the second if it left
-                        // both boxes (one copy of the walk per row keeps the
-                        // unrolled kernel small enough for the instruction
-                        // cache)
-                        uint32_t need = (in_box(b0, kv, bs) ? 0u : 1u) | (in_box(b1, kv, bs) ? 0u : 2u);
-                        do {
-                            const bool first = (need & 1u) != 0;
-                            LeafAt k[1];
-                            walk<NF, 1>(first ? tree_addr : tree1, R, depth, xf, kv, bs, xe, k);
-                            const float nv = leaf_value(k[0]);
-                            const float4 nb = leaf_box(k[0]);
-                            // component-wise selects (a select of whole boxes
-                            // goes through scratch memory)
-                            v[0] = first ? nv : v[0];
-                            v[NT - 1] = first ? v[NT - 1] : nv;
-                            b0.x = first ? nb.x : b0.x;
-                            b0.y = first ? nb.y : b0.y;
-                            b0.z = first ? nb.z : b0.z;
-                            b0.w = first ? nb.w : b0.w;
-                            b1.x = first ? b1.x : nb.x;
-                            b1.y = first ? b1.y : nb.y;
-                            b1.z = first ? b1.z : nb.z;
-                            b1.w = first ? b1.w : nb.w;
-                            need &= need - 1u;
-                        } while (need != 0);
+                        const bool n0 = !in_box(b0, kv, bs);
+                        const bool n1 = !in_box(b1, kv, bs);
+                        if (__builtin_amdgcn_ballot_w64(n0) != 0 && __builtin_amdgcn_ballot_w64(n1) != 0) {
+                            LeafAt k[2];
+                            walk<NF, 2>(tree_addr, R, depth, xf, kv, bs, xe, k);
+                            if (n0) {
+                                v[0] = leaf_value(k[0]);
+                                b0 = leaf_box(k[0]);
+                            }
+                            if (n1) {
+                                v[NT - 1] = leaf_value(k[1]);
+                                b1 = leaf_box(k[1]);
+                            }
+                        } else {
+                            if (n0) {
+                                LeafAt k[1];
+                                walk<NF, 1>(tree_addr, R, depth, xf, kv, bs, xe, k);
+                                v[0] = leaf_value(k[0]);
+                                b0 = leaf_box(k[0]);
+                            }
+                            if (n1) {
+                                LeafAt k[1];
+                                walk<NF, 1>(tree1, R, depth, xf, kv, bs, xe, k);
+                                v[NT - 1] = leaf_value(k[0]);
+                                b1 = leaf_box(k[0]);
+                            }
+                        }
                         box = box_meet(b0, b1);
                     }
                 }
@@ -417,8 +416,8 @@ __global__ __launch_bounds__(kLdsThreads, TL_LDS_WAVES_PER_SIMD) void forest_gri
             const uint32_t bp = cur * buf_bytes;
             // Trees are taken two at a time and a lane keeps the intersection
             // of the two leaf boxes: a row inside it reaches both leaves
-            // again.  The chunk's first row walks both trees in one pass, so
-            // the two chains of dependent LDS reads overlap.
+            // again.  When a row leaves it, both trees are walked in one pass,
+            // so the two chains of dependent LDS reads overlap.
             int32_t tt = 0;
             for (; tt + 1 < cnt; tt += 2)
                 eval_trees<NF, J, 2>(smem, bp + tt * R.bytes, R, depth, kvb4, hull, xf, xe, acc);
