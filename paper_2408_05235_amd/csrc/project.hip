@@ -124,11 +124,6 @@ __device__ __forceinline__ void add_request(int32_t* KV, int32_t c, int32_t a, i
     }
 }
 
-// BD_LDS: the batch difference array lives in LDS beside the KV curve, as a
-// batch cap needs (the admission loop reads its running sums).  Without a
-// cap it is only added to and finally prefix-summed, so it accumulates with
-// atomics in the scenario's own batch output row instead: half the LDS, twice
-// the scenario wavefronts per CU.
 // Scenario order for long FIFO loops: one wavefront per scenario, whose time
 // grows with its number of requests; launched heaviest first, the last
 // wavefronts of the grid are short ones instead of whichever came last.  A
@@ -175,6 +170,11 @@ __global__ __launch_bounds__(256) void order_place_kernel(const int64_t* off, in
 // admission loop takes requests one at a time.
 constexpr int32_t kMinBatch = 8;
 
+// BD_LDS: the batch difference array lives in LDS beside the KV curve, as a
+// batch cap needs (the admission loop reads its running sums).  Without a
+// cap it is only added to and finally prefix-summed, so it accumulates with
+// atomics in the scenario's own batch output row instead: half the LDS, twice
+// the scenario wavefronts per CU.
 template <bool BD_LDS, bool POW2>
 __global__ __launch_bounds__(64) void project_kernel(ProjectParams P) {
     extern __shared__ int32_t lds[];
