@@ -346,7 +346,14 @@ tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs,
  * kv, batch, deadline_at, n_iters, proj_flags: as written by tl_project;
  * freqs_mhz [F] ascending; engine_size [S] for 4-feature forests.
  * Work arrays of the caller: ips_work [S][H] fp32 (left holding M at the
- * final probe) and search_work [3][S] int32.  Allocates nothing.
+ * final probe) and search_work [3][S] int32.  On grids that give every CU at
+ * least two workgroups of the model's kernel (16 wavefronts of 64 lanes x 16,
+ * else 8, consecutive iterations of one scenario), the wavefronts' work is
+ * ordered by an estimate of its cost, computed once per call (results do not
+ * depend on the order): 16 bytes per wavefront plus a radix sort's temporary
+ * storage, in the forest's device scratch, as for tl_forest_predict_grid (the
+ * larger of the two needs is kept; no ordering under stream capture or
+ * without the scratch).  Nothing else is allocated.
  * lattice (nullable): a table of the same forest and frequency count
  * (tl_lattice_create; TL_EINVAL otherwise); M at the probes is then read
  * from it, at the lattice's own frequencies (the same values when it was
@@ -386,7 +393,8 @@ tl_status tl_select_freq_binary(const tl_forest* forest, int64_t n_scenarios, in
  * is read for 4-feature forests.  ips [S][H] receives M at max_freq_mhz (rows
  * of scenarios flagged TL_FLAG_OVERFLOW hold M on the zero curves).  All
  * arrays are device arrays of the caller; the only scratch is the
- * projection's scenario order, as for tl_project.
+ * projection's scenario order, as for tl_project, and the model kernel's
+ * work order, as for tl_select_freq_binary.
  * Errors as for tl_project, plus a NULL forest, ips, decision, tbt_slo_ns,
  * cand_prompt or cand_len, or a forest without 3 or 4 features: TL_EINVAL.
  * ---------------------------------------------------------------------- */

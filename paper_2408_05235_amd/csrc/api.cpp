@@ -24,9 +24,9 @@ struct tl_forest {
     void* box_mem;
     void* records_mem;
     void* cuts_mem;   // [kMaxCuts] KV cuts, then [kMaxCuts] batch cuts
-    // Work-order scratch of the grid kernel, on the forest's device: kept
-    // from call to call and only replaced by a larger one when a larger grid
-    // comes.  ws_done is recorded on the stream of the last call that used
+    // Work-order scratch of the grid and column kernels, on the forest's
+    // device: kept from call to call and only replaced by a larger one when a
+    // larger grid comes.  ws_done is recorded on the stream of the last call that used
     // it; a call on another stream waits for it first.
     mutable std::mutex ws_mutex;
     mutable void* ws = nullptr;
@@ -221,17 +221,18 @@ bool capturing(hipStream_t st) {
     return cs != hipStreamCaptureStatusNone;
 }
 
-// The grid kernel with the forest's cached work-order workspace.  In the
-// steady state nothing is allocated; a larger grid than any before replaces
-// the workspace (after the last call that used it is done).  Without a
-// workspace (allocation failed, or the stream is being captured) the kernel
-// runs without the order, which changes only its speed.
-hipError_t grid_with_workspace(const tl_forest* f, const tl::GridParams& g, hipStream_t st) {
-    size_t need = 0;
-    hipError_t e = tl::grid_order_bytes(f->dev, g, &need);
-    if (e != hipSuccess) return e;
-    if (need == 0 || capturing(st)) return tl::launch_forest_grid(f->dev, g, nullptr, 0, st);
+// Runs launch(ws, ws_bytes) with the forest's cached work-order workspace
+// of at least `need` bytes, all of its launches on st.  In the steady state
+// nothing is allocated; a larger need than any before replaces the
+// workspace (after the last call that used it is done).  Without a
+// workspace (need 0, allocation failed, or the stream is being captured)
+// launch gets (nullptr, 0) and runs without the order, which changes only
+// its speed.
+template <class Launch>
+hipError_t with_workspace(const tl_forest* f, size_t need, hipStream_t st, Launch&& launch) {
+    if (need == 0 || capturing(st)) return launch(nullptr, (size_t)0);
     std::lock_guard<std::mutex> lock(f->ws_mutex);
+    hipError_t e;
     if (need > f->ws_bytes) {
         if (f->ws) {
             if (f->ws_used) {
@@ -250,18 +251,44 @@ hipError_t grid_with_workspace(const tl_forest* f, const tl::GridParams& g, hipS
             (void)hipGetLastError();   // clear the allocation error before the launches check theirs
         }
     }
-    if (!f->ws) return tl::launch_forest_grid(f->dev, g, nullptr, 0, st);
+    if (!f->ws) return launch(nullptr, (size_t)0);
     if (f->ws_used && f->ws_stream != st) {
         e = hipStreamWaitEvent(st, f->ws_done, 0);
         if (e != hipSuccess) return e;
     }
-    e = tl::launch_forest_grid(f->dev, g, f->ws, f->ws_bytes, st);
+    e = launch(f->ws, f->ws_bytes);
     if (e != hipSuccess) return e;
     e = hipEventRecord(f->ws_done, st);
     if (e != hipSuccess) return e;
     f->ws_stream = st;
     f->ws_used = true;
     return hipSuccess;
+}
+
+hipError_t grid_with_workspace(const tl_forest* f, const tl::GridParams& g, hipStream_t st) {
+    size_t need = 0;
+    const hipError_t e = tl::grid_order_bytes(f->dev, g, &need);
+    if (e != hipSuccess) return e;
+    return with_workspace(f, need, st,
+                          [&](void* ws, size_t bytes) { return tl::launch_forest_grid(f->dev, g, ws, bytes, st); });
+}
+
+// `run` (launches of the column kernel on c's rows, and whatever goes
+// between them) with c.order set from the forest's workspace when there is
+// one: the order is computed once, before run, and serves every launch.
+template <class Run>
+hipError_t column_with_order(const tl_forest* f, tl::ColumnParams& c, hipStream_t st, Run&& run) {
+    size_t need = 0;
+    const hipError_t e = tl::column_order_bytes(f->dev, c, &need);
+    if (e != hipSuccess) return e;
+    return with_workspace(f, need, st, [&](void* ws, size_t) {
+        c.order = nullptr;
+        if (ws) {
+            const hipError_t eo = tl::order_forest_column(f->dev, c, ws, st);
+            if (eo != hipSuccess) return eo;
+        }
+        return run();
+    });
 }
 
 // Host checks of a projection request and its translation to kernel
@@ -450,7 +477,7 @@ tl_status tl_admit(const tl_admit_args* a, void* stream) {
         gp.out = a->ips;
         e = tl::launch_lattice_column(f->dev, a->lattice->dev, gp, nullptr, lat_f, st_h);
     } else {
-        e = tl::launch_forest_column(f->dev, c, st_h);
+        e = column_with_order(f, c, st_h, [&]() { return tl::launch_forest_column(f->dev, c, st_h); });
     }
     if (e != hipSuccess) return from_hip(e, "tl_admit: model launch");
     tl::AdmitParams d{};
@@ -799,14 +826,19 @@ tl_status tl_select_freq_binary(const tl_forest* f, int64_t n_scenarios, int32_t
     };
     int32_t rounds = 0;
     while ((int64_t)1 << rounds < n_freqs) ++rounds;
-    hipError_t e = tl::launch_search_step(sp, 0, st);
-    for (int32_t r = 0; r < rounds && e == hipSuccess; ++r) {
-        e = model();
-        if (e == hipSuccess) e = tl::launch_search_step(sp, 1, st);
-    }
-    if (e == hipSuccess) e = tl::launch_search_step(sp, 3, st);
-    if (e == hipSuccess) e = model();
-    if (e == hipSuccess) e = tl::launch_search_step(sp, 2, st);
+    auto search = [&]() {
+        hipError_t e = tl::launch_search_step(sp, 0, st);
+        for (int32_t r = 0; r < rounds && e == hipSuccess; ++r) {
+            e = model();
+            if (e == hipSuccess) e = tl::launch_search_step(sp, 1, st);
+        }
+        if (e == hipSuccess) e = tl::launch_search_step(sp, 3, st);
+        if (e == hipSuccess) e = model();
+        if (e == hipSuccess) e = tl::launch_search_step(sp, 2, st);
+        return e;
+    };
+    // the probes walk the same rows every round: one work order serves them all
+    const hipError_t e = lattice ? search() : column_with_order(f, c, st, search);
     return from_hip(e, "tl_select_freq_binary: launch");
 }
 

@@ -295,9 +295,11 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
     const int32_t span = kWave * RPL;
     const int32_t n_cols = (P.H + span - 1) / span;
     bool valid = item < P.S * n_cols;
-    const int64_t s = valid ? item / n_cols : 0;
+    // the (scenario, column) pair: item itself, or its entry of the work order
+    const int64_t code = !valid ? 0 : P.order ? (int64_t)P.order[item] : item;
+    const int64_t s = code / n_cols;
     if (P.fidx && P.fidx[s] < 0) valid = false;
-    const int32_t j0 = (int32_t)(item % n_cols) * span + lane_id() * RPL;
+    const int32_t j0 = (int32_t)(code % n_cols) * span + lane_id() * RPL;
     const float xf = column_freq(P, s);
     const float xe = NF == 4 ? P.engine[s] : 0.0f;
     float kv[RPL], bs[RPL];
@@ -396,25 +398,95 @@ hipError_t launch_column_lds(const ForestDev& f, const ColumnParams& c, int32_t 
     return hipGetLastError();
 }
 
-// Launches forest_column_reuse_kernel<NF, RPL> when the horizon fills a
-// wavefront's 64 x RPL rows and the grid gives every CU a workgroup;
-// returns false (nothing launched) otherwise.
-template <int NF, int RPL>
-bool launch_column_reuse(const ForestDev& f, const ColumnParams& c, int32_t tb, size_t lds, int cus,
-                         hipStream_t stream, hipError_t* err) {
-    const int64_t items = c.S * ((c.H + kWave * RPL - 1) / (kWave * RPL));
-    if (c.H < kWave * RPL || items < (int64_t)kColWaves * cus) return false;
-    if (!grid_fits((items + kColWaves - 1) / kColWaves)) {
-        *err = hipErrorInvalidConfiguration;
-        return true;
+// Estimated cost of each (scenario, column) pair of the leaf-reuse kernel,
+// for its work order.  A row is taken to need a walk when its cell of the
+// KV / batch cut grid (the forest's threshold cuts) differs from the cells of
+// its lane's two anchors and of the lane's last walked row; the kernel pays
+// one walk time per row position at which any lane of the wavefront walks.
+// cost = (those positions << 10) | (walks over all lanes, at most 64 x 14).
+// One wavefront per pair; the cuts sit in LDS.  Writes cost[i] and the pair
+// code i = s * n_cols + col.
+constexpr int kColCostWaves = 4;
+
+__global__ __launch_bounds__(kColCostWaves* kWave) void column_cost_kernel(
+    const float* __restrict__ cuts_kv, int32_t n_kv, const float* __restrict__ cuts_bs, int32_t n_bs,
+    const int32_t* __restrict__ kv, const int32_t* __restrict__ batch, int64_t S, int32_t H, int32_t rpl,
+    uint32_t* __restrict__ cost, uint32_t* __restrict__ code) {
+    __shared__ float ck[kMaxCuts], cb[kMaxCuts];
+    for (int32_t i = threadIdx.x; i < n_kv; i += kColCostWaves * kWave) ck[i] = cuts_kv[i];
+    for (int32_t i = threadIdx.x; i < n_bs; i += kColCostWaves * kWave) cb[i] = cuts_bs[i];
+    __syncthreads();
+    const int32_t span = kWave * rpl;
+    const int32_t n_cols = (H + span - 1) / span;
+    const int64_t pair = (int64_t)blockIdx.x * kColCostWaves + threadIdx.x / kWave;
+    if (pair >= S * n_cols) return;
+    const int64_t s = pair / n_cols;
+    const int32_t j0 = (int32_t)(pair % n_cols) * span + lane_id() * rpl;
+    // number of cuts <= x
+    auto rank = [](const float* c, int32_t n, float x) {
+        int32_t lo = 0, hi = n;
+        while (lo < hi) {
+            const int32_t mid = (lo + hi) >> 1;
+            if (c[mid] <= x) lo = mid + 1;
+            else hi = mid;
+        }
+        return (uint32_t)lo;
+    };
+    // the cell of the lane's row r (rows past the horizon repeat the last, as
+    // in the kernel)
+    auto cell = [&](int32_t r) {
+        const int64_t i = s * H + min(j0 + r, H - 1);
+        return rank(ck, n_kv, (float)kv[i]) << 16 | rank(cb, n_bs, (float)batch[i]);
+    };
+    const uint32_t a0 = cell(0), a1 = cell(rpl - 1);
+    uint32_t last = a0, positions = 0, walks = 0;
+    for (int32_t r = 1; r < rpl - 1; ++r) {
+        const uint32_t c = cell(r);
+        const bool need = c != a0 && c != a1 && c != last;
+        if (need) last = c;
+        const uint64_t lanes = __builtin_amdgcn_ballot_w64(need);
+        positions += lanes != 0;
+        walks += (uint32_t)__builtin_popcountll(lanes);
     }
+    if (lane_id() == 0) {
+        cost[pair] = positions << 10 | walks;
+        code[pair] = (uint32_t)pair;
+    }
+}
+
+// Rows per lane of the leaf-reuse kernel for these rows: 16 (else 8) where
+// the horizon fills a wavefront's 64 x RPL rows and the grid still gives
+// every CU a workgroup; 0 when the kernel does not apply.  *cus: the
+// device's CUs.
+hipError_t reuse_rows_per_lane(const ForestDev& f, const ColumnParams& c, int* rpl, int* cus) {
+    *rpl = 0;
+    size_t lds = 0;
+    if (c.rows || column_trees_per_block(f, &lds) <= 0) return hipSuccess;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    for (int r : {16, 8}) {
+        const int64_t items = c.S * ((c.H + kWave * r - 1) / (kWave * r));
+        if (c.H >= kWave * r && items >= (int64_t)kColWaves * *cus) {
+            *rpl = r;
+            break;
+        }
+    }
+    return hipSuccess;
+}
+
+template <int NF, int RPL>
+hipError_t launch_column_reuse(const ForestDev& f, const ColumnParams& c, int32_t tb, size_t lds,
+                               hipStream_t stream) {
+    const int64_t items = c.S * ((c.H + kWave * RPL - 1) / (kWave * RPL));
+    if (!grid_fits((items + kColWaves - 1) / kColWaves)) return hipErrorInvalidConfiguration;
     const auto kern = forest_column_reuse_kernel<NF, RPL>;
-    *err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (*err != hipSuccess) return true;
+    const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3((unsigned)((items + kColWaves - 1) / kColWaves)), dim3(kColThreads), lds, stream,
                        f.records, f.n_trees, f.depth, tb, f.base_score, c);
-    *err = hipGetLastError();
-    return true;
+    return hipGetLastError();
 }
 
 template <int NF>
@@ -422,14 +494,11 @@ hipError_t launch_column(const ForestDev& f, const ColumnParams& c, hipStream_t 
     size_t lds = 0;
     const int32_t tb = column_trees_per_block(f, &lds);
     if (tb > 0) {
-        // leaf reuse along 16 (else 8) consecutive rows a lane where the grid
-        // still gives every CU a workgroup
-        int dev = 0, cus = 0;
-        hipError_t e = hipGetDevice(&dev);
-        if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        int rpl = 0, cus = 0;
+        const hipError_t e = reuse_rows_per_lane(f, c, &rpl, &cus);
         if (e != hipSuccess) return e;
-        if (launch_column_reuse<NF, 16>(f, c, tb, lds, cus, stream, &e)) return e;
-        if (launch_column_reuse<NF, 8>(f, c, tb, lds, cus, stream, &e)) return e;
+        if (rpl == 16) return launch_column_reuse<NF, 16>(f, c, tb, lds, stream);
+        if (rpl == 8) return launch_column_reuse<NF, 8>(f, c, tb, lds, stream);
     }
     if (tb > 0) {
         // rows per lane: enough chains to overlap, without idle stripes on
@@ -450,6 +519,45 @@ hipError_t launch_column(const ForestDev& f, const ColumnParams& c, hipStream_t 
 hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream) {
     if (c.S == 0) return hipSuccess;
     return f.n_features == 4 ? launch_column<4>(f, c, stream) : launch_column<3>(f, c, stream);
+}
+
+namespace {
+
+// The leaf-reuse kernel's work order for c's rows (p.n = 0: none).  It is
+// only planned for grids of at least two workgroups per CU: with one, the
+// kernel takes as long as its slowest wavefront whatever the order.
+hipError_t plan_column_order(const ForestDev& f, const ColumnParams& c, int* rpl, PairOrderPlan* p) {
+    *p = PairOrderPlan{0, 0, 0, 0};
+    if (c.S == 0) return hipSuccess;
+    int cus = 0;
+    const hipError_t e = reuse_rows_per_lane(f, c, rpl, &cus);
+    if (e != hipSuccess || *rpl == 0) return e;
+    const int64_t span = kWave * *rpl;
+    const int64_t items = c.S * ((c.H + span - 1) / span);
+    return pair_order_plan(f, items, 2 * (int64_t)kColWaves * cus, p);
+}
+
+}  // namespace
+
+hipError_t column_order_bytes(const ForestDev& f, const ColumnParams& c, size_t* bytes) {
+    int rpl = 0;
+    PairOrderPlan p;
+    const hipError_t e = plan_column_order(f, c, &rpl, &p);
+    *bytes = e == hipSuccess ? p.bytes : 0;
+    return e;
+}
+
+hipError_t order_forest_column(const ForestDev& f, ColumnParams& c, void* ws, hipStream_t stream) {
+    int rpl = 0;
+    PairOrderPlan p;
+    hipError_t e = plan_column_order(f, c, &rpl, &p);
+    if (e != hipSuccess || p.n == 0) return e;
+    hipLaunchKernelGGL(column_cost_kernel, dim3((unsigned)((p.n + kColCostWaves - 1) / kColCostWaves)),
+                       dim3(kColCostWaves * kWave), 0, stream, f.cuts_kv, f.n_cuts_kv, f.cuts_bs, f.n_cuts_bs, c.kv,
+                       c.batch, c.S, c.H, rpl, pair_order_cost(p, ws), pair_order_code(p, ws));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return pair_order_sort(p, ws, &c.order, stream);
 }
 
 hipError_t launch_forest_rows_lds(const ForestDev& f, const float* rows, int64_t n_rows, float* out,

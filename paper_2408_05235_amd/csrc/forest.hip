@@ -558,26 +558,9 @@ hipError_t launch_grid_global(const ForestDev& f, const GridParams& g, hipStream
 }  // namespace
 
 
-// Work order for the LDS kernel: (scenario, chunk) pairs by estimated cost,
-// most expensive first, so a workgroup's wavefronts do similar work and the
-// longest ones start first.  It needs four arrays of one 32-bit word per
-// pair plus the radix sort's temporary storage, all in one workspace.
-namespace {
-
-struct OrderPlan {
-    int64_t n;          // (scenario, chunk) pairs; 0 = no order
-    size_t arr;         // bytes per array, 256-aligned
-    size_t temp;        // sort temporary storage
-    size_t bytes;       // 4 * arr + temp
-};
-
-hipError_t plan_order(const ForestDev& f, const GridParams& g, OrderPlan* p) {
-    *p = OrderPlan{0, 0, 0, 0};
-    size_t lds = 0;
-    if (lds_trees_per_block(f, &lds) <= 0) return hipSuccess;   // the global kernel takes no order
-    const int64_t n_chunks = (g.H + kLdsJ - 1) / kLdsJ;
-    const int64_t n = g.S * n_chunks;
-    if (!f.cuts_kv || !f.cuts_bs || n < 2 * kLdsWaves || n >= (int64_t)1 << 31) return hipSuccess;
+hipError_t pair_order_plan(const ForestDev& f, int64_t n, int64_t min_pairs, PairOrderPlan* p) {
+    *p = PairOrderPlan{0, 0, 0, 0};
+    if (!f.cuts_kv || !f.cuts_bs || n < min_pairs || n >= (int64_t)1 << 31) return hipSuccess;
     size_t temp = 0;
     const hipError_t e = hipcub::DeviceRadixSort::SortPairsDescending(
         nullptr, temp, (const uint32_t*)nullptr, (uint32_t*)nullptr, (const uint32_t*)nullptr, (uint32_t*)nullptr,
@@ -590,31 +573,35 @@ hipError_t plan_order(const ForestDev& f, const GridParams& g, OrderPlan* p) {
     return hipSuccess;
 }
 
-// Enqueues the cost estimate and the sort into ws (at least p.bytes) and
-// points g.order at the result.
-hipError_t order_grid(const ForestDev& f, const OrderPlan& p, GridParams& g, void* ws, hipStream_t stream) {
+hipError_t pair_order_sort(const PairOrderPlan& p, void* ws, const uint32_t** order, hipStream_t stream) {
     unsigned char* base = (unsigned char*)ws;
-    uint32_t* cost = (uint32_t*)base;
-    uint32_t* code = (uint32_t*)(base + p.arr);
     uint32_t* cost_sorted = (uint32_t*)(base + 2 * p.arr);
-    uint32_t* order = (uint32_t*)(base + 3 * p.arr);
-    hipLaunchKernelGGL(grid_cost_kernel, dim3((unsigned)((p.n + kCostThreads - 1) / kCostThreads)),
-                       dim3(kCostThreads), 0, stream, f.cuts_kv, f.n_cuts_kv, f.cuts_bs, f.n_cuts_bs, g.kv, g.batch,
-                       g.S, g.H, kLdsJ, cost, code);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    uint32_t* sorted = (uint32_t*)(base + 3 * p.arr);
     size_t temp = p.temp;
-    e = hipcub::DeviceRadixSort::SortPairsDescending(base + 4 * p.arr, temp, cost, cost_sorted, code, order, (int)p.n,
-                                                     0, 32, stream);
+    const hipError_t e = hipcub::DeviceRadixSort::SortPairsDescending(
+        base + 4 * p.arr, temp, pair_order_cost(p, ws), cost_sorted, pair_order_code(p, ws), sorted, (int)p.n, 0, 32,
+        stream);
     if (e != hipSuccess) return e;
-    g.order = order;
+    *order = sorted;
     return hipSuccess;
+}
+
+// Work order for the LDS grid kernel: (scenario, chunk) pairs by estimated
+// cost, most expensive first, so a workgroup's wavefronts do similar work
+// and the longest ones start first.
+namespace {
+
+hipError_t plan_order(const ForestDev& f, const GridParams& g, PairOrderPlan* p) {
+    *p = PairOrderPlan{0, 0, 0, 0};
+    size_t lds = 0;
+    if (lds_trees_per_block(f, &lds) <= 0) return hipSuccess;   // the global kernel takes no order
+    return pair_order_plan(f, g.S * ((g.H + kLdsJ - 1) / kLdsJ), 2 * kLdsWaves, p);
 }
 
 }  // namespace
 
 hipError_t grid_order_bytes(const ForestDev& f, const GridParams& g, size_t* bytes) {
-    OrderPlan p;
+    PairOrderPlan p;
     const hipError_t e = plan_order(f, g, &p);
     *bytes = e == hipSuccess ? p.bytes : 0;
     return e;
@@ -627,13 +614,17 @@ hipError_t launch_forest_grid(const ForestDev& f, const GridParams& g_in, void* 
     size_t lds = 0;
     const int32_t tb = lds_trees_per_block(f, &lds);
     if (tb <= 0) return f.n_features == 4 ? launch_grid_global<4>(f, g, stream) : launch_grid_global<3>(f, g, stream);
-    OrderPlan p;
+    PairOrderPlan p;
     hipError_t e = plan_order(f, g, &p);
     if (e != hipSuccess) return e;
     // the order only speeds the kernel up: without room for it the items
     // keep their natural numbering
     if (p.n > 0 && ws && ws_bytes >= p.bytes) {
-        e = order_grid(f, p, g, ws, stream);
+        hipLaunchKernelGGL(grid_cost_kernel, dim3((unsigned)((p.n + kCostThreads - 1) / kCostThreads)),
+                           dim3(kCostThreads), 0, stream, f.cuts_kv, f.n_cuts_kv, f.cuts_bs, f.n_cuts_bs, g.kv,
+                           g.batch, g.S, g.H, kLdsJ, pair_order_cost(p, ws), pair_order_code(p, ws));
+        e = hipGetLastError();
+        if (e == hipSuccess) e = pair_order_sort(p, ws, &g.order, stream);
         if (e != hipSuccess) return e;
     }
     return f.n_features == 4 ? launch_grid_lds<4>(f, g, tb, lds, stream) : launch_grid_lds<3>(f, g, tb, lds, stream);

@@ -56,6 +56,10 @@ struct ColumnParams {
     const int32_t* fidx;            // nullable
     const float* engine;            // 4-feature forests
     float* out;
+    // optional work order of the leaf-reuse kernel: entry i is the
+    // (scenario, column) pair s * n_cols + col that item i takes, where a
+    // column is 64 x RPL consecutive iterations
+    const uint32_t* order;
     // rows mode (rows != NULL): out[i] = M(rows[i][0 .. n_features - 1]) for
     // i < n_rows; the fields above except `out` are not used
     const float* rows;
@@ -215,6 +219,30 @@ constexpr size_t kNoAllocScratchBytes = (size_t)32 << 20;
 hipError_t noalloc_scratch(void** ptr);
 hipError_t launch_select(const SelectParams& p, hipStream_t stream);
 hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipStream_t stream);
+// Scratch bytes a work order for launch_forest_column needs (0 when none
+// applies: the leaf-reuse kernel is not used, or no cuts); the order depends
+// only on the rows (KV, batch), not on the frequencies.
+hipError_t column_order_bytes(const ForestDev& f, const ColumnParams& c, size_t* bytes);
+// Enqueues the order into ws (at least column_order_bytes) and points
+// c.order at it; later launches with the same rows may reuse it.
+hipError_t order_forest_column(const ForestDev& f, ColumnParams& c, void* ws, hipStream_t stream);
+// A work order: n pairs sorted by an estimated cost, most expensive first.
+// Its workspace holds four arrays of one 32-bit word per pair (cost, code,
+// and their sorted copies) and the sort's temporary storage.  The caller
+// fills pair_order_cost / pair_order_code (pair i's cost and its code),
+// then pair_order_sort points *order at the codes sorted by cost.
+// pair_order_plan gives n = 0 (no order) when the forest has no cuts to
+// estimate costs with, or n < min_pairs.
+struct PairOrderPlan {
+    int64_t n;          // pairs; 0 = no order
+    size_t arr;         // bytes per array, 256-aligned
+    size_t temp;        // sort temporary storage
+    size_t bytes;       // 4 * arr + temp
+};
+hipError_t pair_order_plan(const ForestDev& f, int64_t n, int64_t min_pairs, PairOrderPlan* p);
+inline uint32_t* pair_order_cost(const PairOrderPlan&, void* ws) { return (uint32_t*)ws; }
+inline uint32_t* pair_order_code(const PairOrderPlan& p, void* ws) { return (uint32_t*)((unsigned char*)ws + p.arr); }
+hipError_t pair_order_sort(const PairOrderPlan& p, void* ws, const uint32_t** order, hipStream_t stream);
 // The same kernel on arbitrary rows [n_rows][n_features] (3 or 4 features,
 // LDS records present); hipErrorNotSupported when the forest has no records.
 hipError_t launch_forest_rows_lds(const ForestDev& f, const float* rows, int64_t n_rows, float* out,

@@ -155,12 +155,13 @@ def test_admit_scaled_configs(gpu, ci, over):
     check_admit(inp, inp["forest"], float(inp["freqs_mhz"][-1]), cand, cfg["name"])
 
 
-@pytest.mark.parametrize("ci,S", [(3, 2048), (3, 4096), (4, 1024), (4, 2048)])
+@pytest.mark.parametrize("ci,S", [(3, 2048), (3, 4096), (4, 1024), (4, 2048), (3, 8192), (4, 4096)])
 def test_admit_model_at_reuse_sizes(gpu, ci, S):
     """Grids large enough for the column kernel with leaf reuse along each
     lane's rows, 8 rows a lane (the smaller grids) and 16: c3's slowly
     changing rows and c4's batch that changes at most iterations (arrivals
-    and completions).  The model at the maximum frequency equals the
+    and completions); the two largest give 256 CUs two workgroups each, and
+    the items follow the estimated-cost work order.  The model at the maximum frequency equals the
     oracle's on every iteration of the projection the GPU returned (the
     projection itself is checked against the oracle in the tests above)."""
     cfg = synth.scaled(configs.get_config(ci), n_scenarios=S, forest_n_trees=60)

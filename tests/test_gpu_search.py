@@ -91,11 +91,13 @@ def test_binary_search_random(gpu, S, F, H, T, d, nf, mono, seed):
     assert len(set(st.tolist())) >= 2
 
 
-@pytest.mark.parametrize("S,H", [(4096, 512), (2048, 1000), (4096, 1100)])
+@pytest.mark.parametrize("S,H", [(4096, 512), (2048, 1000), (4096, 1100), (8192, 1024)])
 def test_binary_search_at_reuse_sizes(gpu, S, H):
     """Grids large enough for the column kernel with leaf reuse along each
     lane's rows: 8 rows a lane (a whole and a ragged last wavefront of
-    iterations) and 16 rows a lane (ragged).  Half of the scenarios have a
+    iterations) and 16 rows a lane (ragged; and on 256 CUs at 8192 x 1024,
+    two workgroups per CU, where the items follow the estimated-cost work
+    order, the odd scenarios' columns first).  Half of the scenarios have a
     batch that changes at every iteration, so many rows lie outside both
     anchor leaves' boxes and walk.  Indices and statuses equal the
     oracle's."""
