@@ -78,3 +78,80 @@ def test_captured_projection_and_grid_replays(gpu):
         assert np.array_equal(forest.tl_forest_predict_grid(dfr, dkv, dbs).cpu().numpy(), exp_grid)
         torch.cuda.synchronize()
     forest.close()
+
+
+def test_captured_binary_search_replays(gpu):
+    """The binary search at a size where eager calls order the column
+    kernel's work by estimated cost (8192 x 1024 iterations on 256 CUs: two
+    workgroups per CU), captured into a graph, where the order is left out:
+    every replay gives the eager call's indices, statuses and final-probe
+    model values, with eager calls (through the forest's scratch) between
+    the replays; sampled scenarios equal the oracle's search."""
+    import torch
+    from paper_2408_05235_amd import api
+    from test_gpu_search import random_checks
+    rng = np.random.default_rng(46)
+    S, H, F, nf = 8192, 1024, 5, 4
+    fd = random_forest(rng, 20, 6, nf, kvmax=3000, bmax=200)
+    fd["base_score"] = np.float32(45.0)
+    kv, bs = random_curves(rng, S, H, kvmax=3000, bmax=200)
+    # odd scenarios: a batch that changes at every iteration (costly columns)
+    fast = np.arange(S) % 2 == 1
+    nfast = int(fast.sum())
+    bs[fast] = np.clip(rng.integers(20, 180, (nfast, 1)) + np.cumsum(rng.choice([-1, 1], (nfast, H)), axis=1),
+                       0, None).astype(np.int32)
+    freqs = synth.frequency_grid(F)
+    eng = rng.choice([1.0, 2.0, 4.0, 8.0], S).astype(np.float32)
+    dl, n, tbt, flags = random_checks(rng, S, H, kv)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    args = (t(freqs), t(kv), t(bs), t(dl.view(np.int64)), t(n), t(tbt.view(np.int64)), t(flags.view(np.int32)))
+    deng = t(eng)
+    forest = api.Forest.from_dict(fd)
+
+    def bufs():
+        return dict(ips_work=torch.full((S, H), -1.0, dtype=torch.float32, device="cuda"),
+                    search_work=torch.zeros((3, S), dtype=torch.int32, device="cuda"),
+                    freq_idx=torch.full((S,), -1, dtype=torch.int32, device="cuda"),
+                    status=torch.full((S,), -1, dtype=torch.int32, device="cuda"))
+
+    def call(out):
+        return api.tl_select_freq_binary(forest, *args, engine_size=deng, out=out)
+
+    def host(out):
+        return {k: out[k].cpu().numpy() for k in ("ips_work", "freq_idx", "status")}
+
+    ref = bufs()
+    call(ref)
+    torch.cuda.synchronize()
+    eager = host(ref)
+    sample = np.array([0, 1, S // 2 + 1, S - 1])
+    ips = oracle.forest_predict(fd, oracle.rows(freqs, bs[sample], kv[sample], eng[sample], nf))
+    oi, os_ = oracle.select_binary(ips, dl[sample], n[sample], tbt[sample], flags[sample])
+    assert np.array_equal(eager["freq_idx"][sample], oi)
+    assert np.array_equal(eager["status"][sample].view(np.uint32), os_)
+
+    cap = bufs()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call(cap)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        call(cap)
+    for rep in range(3):
+        for v in cap.values():
+            v.fill_(-1)
+        graph.replay()
+        torch.cuda.synchronize()
+        got = host(cap)
+        for k in eager:
+            assert np.array_equal(got[k], eager[k]), (k, rep)
+        again = bufs()
+        call(again)
+        torch.cuda.synchronize()
+        got = host(again)
+        for k in eager:
+            assert np.array_equal(got[k], eager[k]), (k, "eager after replay", rep)
+    forest.close()
