@@ -403,7 +403,9 @@ hipError_t launch_column_lds(const ForestDev& f, const ColumnParams& c, int32_t 
 // KV / batch cut grid (the forest's threshold cuts) differs from the cells of
 // its lane's two anchors and of the lane's last walked row; the kernel pays
 // one walk time per row position at which any lane of the wavefront walks.
-// cost = (those positions << 10) | (walks over all lanes, at most 64 x 14).
+// cost = (those positions << 10) | (walks over all lanes, at most 64 x 14);
+// with many trees nearly every position has a walk, and the second term,
+// how fast the column's rows change, decides the order.
 // One wavefront per pair; the cuts sit in LDS.  Writes cost[i] and the pair
 // code i = s * n_cols + col.
 constexpr int kColCostWaves = 4;
