@@ -341,19 +341,24 @@ tl_status tl_select_freq(const float* ips, int64_t n_scenarios, int32_t n_freqs,
  * mid + 1; finally lo is checked: feasible -> freq_idx = lo (OK), else F-1
  * (INFEASIBLE).  Flags as in tl_select_freq (OVERFLOW -> INVALID, LOST ->
  * F-1 without a search).  It equals tl_select_freq whenever feasibility is
- * monotone in the frequency, and evaluates M on ceil(log2 F) + 1 rows per
- * (scenario, iteration) instead of F.
+ * monotone in the frequency, and evaluates M on at most ceil(log2 F) + 1
+ * rows per (scenario, iteration) instead of F: the check of lo evaluates
+ * nothing new when hi has moved below F-1, since hi only moves to a probe
+ * found feasible and then lo == hi.
  * kv, batch, deadline_at, n_iters, proj_flags: as written by tl_project;
  * freqs_mhz [F] ascending; engine_size [S] for 4-feature forests.
- * Work arrays of the caller: ips_work [S][H] fp32 (left holding M at the
- * final probe) and search_work [3][S] int32.  On grids that give every CU at
- * least two workgroups of the model's kernel (16 wavefronts of 64 lanes x 16,
- * else 8, consecutive iterations of one scenario), the wavefronts' work is
- * ordered by an estimate of its cost, computed once per call (results do not
- * depend on the order): 16 bytes per wavefront plus a radix sort's temporary
- * storage, in the forest's device scratch, as for tl_forest_predict_grid (the
- * larger of the two needs is kept; no ordering under stream capture or
- * without the scratch).  Nothing else is allocated.
+ * Work arrays of the caller: ips_work [S][H] fp32 (left holding, per
+ * scenario, M at the last frequency it evaluated; rows of scenarios flagged
+ * lost or overflow are not written) and search_work [3][S] int32.
+ * On grids that give every CU at least two workgroups of the model's kernel
+ * (16 wavefronts of 64 lanes x 16, else 8, consecutive iterations of one
+ * scenario), the wavefronts' work is ordered by an estimate of its cost,
+ * computed once per call, and the check of lo runs only the wavefronts of
+ * scenarios that need an evaluation, compacted (results depend on neither).
+ * Scratch: 20 bytes per wavefront plus a radix sort's temporary storage, in
+ * the forest's device scratch, as for tl_forest_predict_grid (the larger of
+ * the two needs is kept; neither ordering nor compaction under stream
+ * capture or without the scratch).  Nothing else is allocated.
  * lattice (nullable): a table of the same forest and frequency count
  * (tl_lattice_create; TL_EINVAL otherwise); M at the probes is then read
  * from it, at the lattice's own frequencies (the same values when it was

@@ -826,19 +826,36 @@ tl_status tl_select_freq_binary(const tl_forest* f, int64_t n_scenarios, int32_t
     };
     int32_t rounds = 0;
     while ((int64_t)1 << rounds < n_freqs) ++rounds;
-    auto search = [&]() {
+    // live (nullable): scratch for compacting the final probe's work to the
+    // scenarios that still probe
+    auto search = [&](void* live) {
         hipError_t e = tl::launch_search_step(sp, 0, st);
         for (int32_t r = 0; r < rounds && e == hipSuccess; ++r) {
             e = model();
             if (e == hipSuccess) e = tl::launch_search_step(sp, 1, st);
         }
         if (e == hipSuccess) e = tl::launch_search_step(sp, 3, st);
-        if (e == hipSuccess) e = model();
+        if (e == hipSuccess) e = live ? tl::launch_forest_column_live(f->dev, c, live, st) : model();
         if (e == hipSuccess) e = tl::launch_search_step(sp, 2, st);
         return e;
     };
-    // the probes walk the same rows every round: one work order serves them all
-    const hipError_t e = lattice ? search() : column_with_order(f, c, st, search);
+    if (lattice) return from_hip(search(nullptr), "tl_select_freq_binary: launch");
+    // The probes walk the same rows every round: one work order serves them
+    // all.  Scratch: the order, then the final probe's live items.
+    size_t need_order = 0, need_live = 0;
+    hipError_t e = tl::column_order_bytes(f->dev, c, &need_order);
+    if (e == hipSuccess) e = tl::column_live_bytes(f->dev, c, &need_live);
+    if (e != hipSuccess) return from_hip(e, "tl_select_freq_binary: launch");
+    need_order = (need_order + 255) & ~(size_t)255;
+    e = with_workspace(f, need_order + need_live, st, [&](void* ws, size_t) {
+        c.order = nullptr;
+        if (!ws) return search(nullptr);
+        if (need_order > 0) {
+            const hipError_t eo = tl::order_forest_column(f->dev, c, ws, st);
+            if (eo != hipSuccess) return eo;
+        }
+        return search(need_live > 0 ? (unsigned char*)ws + need_order : nullptr);
+    });
     return from_hip(e, "tl_select_freq_binary: launch");
 }
 

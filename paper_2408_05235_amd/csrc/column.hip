@@ -282,7 +282,8 @@ __device__ __forceinline__ void add_leaves_anchored(uint32_t tree, const RecordL
 // M at one frequency per scenario with leaf reuse along each lane's RPL
 // consecutive iterations (a wavefront takes 64 x RPL consecutive
 // iterations of one scenario); staging as in forest_column_lds_kernel.
-template <int NF, int RPL>
+// LIVE: the items are the first *P.n_live entries of P.order.
+template <int NF, int RPL, bool LIVE>
 __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const uint4* __restrict__ records,
                                                                          int32_t n_trees, int32_t depth,
                                                                          int32_t tb, float base, ColumnParams P) {
@@ -294,7 +295,10 @@ __global__ __launch_bounds__(kColThreads) void forest_column_reuse_kernel(const 
     const int64_t item = __builtin_amdgcn_readfirstlane((int64_t)blockIdx.x * kColWaves + wave);
     const int32_t span = kWave * RPL;
     const int32_t n_cols = (P.H + span - 1) / span;
-    bool valid = item < P.S * n_cols;
+    const int64_t n_items = LIVE ? (int64_t)*P.n_live : P.S * n_cols;
+    // a workgroup wholly past the live items has nothing to stage for
+    if (LIVE && (int64_t)blockIdx.x * kColWaves >= n_items) return;
+    bool valid = item < n_items;
     // the (scenario, column) pair: item itself, or its entry of the work order
     const int64_t code = !valid ? 0 : P.order ? (int64_t)P.order[item] : item;
     const int64_t s = code / n_cols;
@@ -483,7 +487,8 @@ hipError_t launch_column_reuse(const ForestDev& f, const ColumnParams& c, int32_
                                hipStream_t stream) {
     const int64_t items = c.S * ((c.H + kWave * RPL - 1) / (kWave * RPL));
     if (!grid_fits((items + kColWaves - 1) / kColWaves)) return hipErrorInvalidConfiguration;
-    const auto kern = forest_column_reuse_kernel<NF, RPL>;
+    const auto kern =
+        c.n_live ? forest_column_reuse_kernel<NF, RPL, true> : forest_column_reuse_kernel<NF, RPL, false>;
     const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3((unsigned)((items + kColWaves - 1) / kColWaves)), dim3(kColThreads), lds, stream,
@@ -525,6 +530,31 @@ hipError_t launch_forest_column(const ForestDev& f, const ColumnParams& c, hipSt
 
 namespace {
 
+__global__ void column_live_clear_kernel(int32_t* n_live) { *n_live = 0; }
+
+// The live items of the leaf-reuse kernel: entry i of the work order (or
+// item i) is kept when its scenario is selected (fidx >= 0); a wavefront's
+// kept entries stay in order and take consecutive slots from one atomic add.
+__global__ __launch_bounds__(256) void column_live_kernel(const uint32_t* __restrict__ order,
+                                                          const int32_t* __restrict__ fidx, int64_t n_items,
+                                                          int32_t n_cols, uint32_t* __restrict__ live,
+                                                          int32_t* __restrict__ n_live) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    uint32_t code = 0;
+    bool keep = false;
+    if (i < n_items) {
+        code = order ? order[i] : (uint32_t)i;
+        keep = fidx[code / (uint32_t)n_cols] >= 0;
+    }
+    const uint64_t m = __builtin_amdgcn_ballot_w64(keep);
+    if (m == 0) return;
+    int32_t base = 0;
+    if (lane_id() == 0) base = atomicAdd(n_live, (int32_t)__builtin_popcountll(m));
+    base = __shfl(base, 0);
+    const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    if (keep) live[base + (int32_t)below] = code;
+}
+
 // The leaf-reuse kernel's work order for c's rows (p.n = 0: none).  It is
 // only planned for grids of at least two workgroups per CU: with one, the
 // kernel takes as long as its slowest wavefront whatever the order.
@@ -560,6 +590,46 @@ hipError_t order_forest_column(const ForestDev& f, ColumnParams& c, void* ws, hi
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return pair_order_sort(p, ws, &c.order, stream);
+}
+
+hipError_t column_live_bytes(const ForestDev& f, const ColumnParams& c, size_t* bytes) {
+    *bytes = 0;
+    int rpl = 0, cus = 0;
+    if (c.S == 0 || !c.fidx) return hipSuccess;
+    const hipError_t e = reuse_rows_per_lane(f, c, &rpl, &cus);
+    if (e != hipSuccess || rpl == 0) return e;
+    const int64_t span = kWave * rpl;
+    const int64_t items = c.S * ((c.H + span - 1) / span);
+    // as for the work order: with one workgroup per CU the launch lasts as
+    // long as its slowest workgroup, compacted or not
+    if (items < 2 * (int64_t)kColWaves * cus) return hipSuccess;
+    *bytes = (((size_t)items * sizeof(uint32_t) + 255) & ~(size_t)255) + 256;
+    return hipSuccess;
+}
+
+hipError_t launch_forest_column_live(const ForestDev& f, const ColumnParams& c, void* ws, hipStream_t stream) {
+    int rpl = 0, cus = 0;
+    hipError_t e = hipSuccess;
+    if (ws && c.fidx && c.S > 0) e = reuse_rows_per_lane(f, c, &rpl, &cus);
+    if (e != hipSuccess) return e;
+    if (rpl == 0) return launch_forest_column(f, c, stream);
+    const int32_t span = kWave * rpl;
+    const int32_t n_cols = (c.H + span - 1) / span;
+    const int64_t items = c.S * n_cols;
+    uint32_t* live = (uint32_t*)ws;
+    int32_t* n_live = (int32_t*)((unsigned char*)ws + (((size_t)items * sizeof(uint32_t) + 255) & ~(size_t)255));
+    hipLaunchKernelGGL(column_live_clear_kernel, dim3(1), dim3(1), 0, stream, n_live);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (!grid_fits((items + 255) / 256)) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(column_live_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, stream, c.order,
+                       c.fidx, items, n_cols, live, n_live);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    ColumnParams d = c;
+    d.order = live;
+    d.n_live = n_live;
+    return launch_forest_column(f, d, stream);
 }
 
 hipError_t launch_forest_rows_lds(const ForestDev& f, const float* rows, int64_t n_rows, float* out,

@@ -235,12 +235,21 @@ __global__ __launch_bounds__(kSearchWaves * kWave) void search_kernel(SearchPara
     probe[s] = l < h ? l + (h - l) / 2 : -1;
 }
 
-// Before the final check every unsettled scenario probes lo.
+// Before the final check, lo == hi for every unsettled scenario.  hi only
+// moves to a probe found feasible, and no probe is ever F-1 (the midpoint of
+// lo < hi lies below hi), so hi < F-1 means lo was probed and found
+// feasible: the scenario is settled here with lo (OK), as the final check of
+// lo would settle it.  The others (hi still F-1) probe lo.
 __global__ __launch_bounds__(256) void search_final_probe_kernel(SearchParams P) {
     const int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (s >= P.S) return;
-    const int32_t l = P.work[s];
-    P.work[2 * P.S + s] = l;   // -1 stays -1 (settled)
+    const int32_t l = P.work[s], h = P.work[P.S + s];
+    const bool known = l >= 0 && l == h && h < P.F - 1;
+    if (known) {
+        P.freq_idx[s] = l;
+        P.status[s] = TL_STATUS_OK;
+    }
+    P.work[2 * P.S + s] = known ? -1 : l;   // -1 stays -1 (settled)
 }
 
 }  // namespace

@@ -60,6 +60,10 @@ struct ColumnParams {
     // (scenario, column) pair s * n_cols + col that item i takes, where a
     // column is 64 x RPL consecutive iterations
     const uint32_t* order;
+    // optional, with order: a device count of the entries of `order` to
+    // take; items from it on are skipped, and workgroups wholly past it
+    // return at once
+    const int32_t* n_live;
     // rows mode (rows != NULL): out[i] = M(rows[i][0 .. n_features - 1]) for
     // i < n_rows; the fields above except `out` are not used
     const float* rows;
@@ -226,6 +230,13 @@ hipError_t column_order_bytes(const ForestDev& f, const ColumnParams& c, size_t*
 // Enqueues the order into ws (at least column_order_bytes) and points
 // c.order at it; later launches with the same rows may reuse it.
 hipError_t order_forest_column(const ForestDev& f, ColumnParams& c, void* ws, hipStream_t stream);
+// launch_forest_column for c.fidx-selected scenarios, with the leaf-reuse
+// kernel's items of skipped scenarios (fidx < 0) compacted out first (in
+// c.order's order when it has one), so that the launch's work follows the
+// live scenarios only; scratch column_live_bytes in ws.  Without the
+// leaf-reuse kernel, fidx or ws, a plain launch_forest_column.
+hipError_t column_live_bytes(const ForestDev& f, const ColumnParams& c, size_t* bytes);
+hipError_t launch_forest_column_live(const ForestDev& f, const ColumnParams& c, void* ws, hipStream_t stream);
 // A work order: n pairs sorted by an estimated cost, most expensive first.
 // Its workspace holds four arrays of one 32-bit word per pair (cost, code,
 // and their sorted copies) and the sort's temporary storage.  The caller

@@ -19,18 +19,59 @@ def _np(t):
     return t.detach().cpu().numpy()
 
 
-def gpu_binary(fd, freqs, kv, bs, dl, n, tbt, flags, eng):
+def gpu_binary(fd, freqs, kv, bs, dl, n, tbt, flags, eng, want_ips=False):
+    """(freq_idx, status) of tl_select_freq_binary, and with want_ips its
+    ips_work (filled with NaN before the call)."""
     import torch
     from paper_2408_05235_amd import api
     t = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
     f = api.Forest.from_dict(fd)
+    work = {"ips_work": torch.full(kv.shape, float("nan"), dtype=torch.float32, device="cuda")}
     idx, st = api.tl_select_freq_binary(f, t(freqs), t(kv), t(bs), t(dl.view(np.int64)), t(n),
                                         t(tbt.view(np.int64)), None if flags is None else t(flags.view(np.int32)),
-                                        t(eng))
+                                        t(eng), work)
     torch.cuda.synchronize()
     out = _np(idx), _np(st).view(np.uint32)
+    if want_ips:
+        out = out + (work["ips_work"].cpu().numpy(),)
     f.close()
     return out
+
+
+def last_probes(ips, dl, n, tbt, flags):
+    """The frequency each scenario's binary search evaluated M at last, from
+    the oracle's feasibility at every frequency: the probes lo + (hi - lo) / 2
+    while lo < hi, then lo itself unless hi moved below F-1 (a feasible probe
+    at hi = lo, whose check needs no new evaluation); -1 for scenarios
+    flagged lost or overflow, which probe nothing."""
+    S, F = ips.shape[:2]
+    feas = np.stack([oracle.select(np.ascontiguousarray(ips[:, f:f + 1]), dl, n, tbt, None)[1] == oracle.STATUS_OK
+                     for f in range(F)], axis=1)
+    out = np.full(S, -1, np.int64)
+    for s in range(S):
+        if flags is not None and flags[s] & (oracle.FLAG_LOST | oracle.FLAG_OVERFLOW):
+            continue
+        lo, hi, last = 0, F - 1, -1
+        while lo < hi:
+            mid = lo + (hi - lo) // 2
+            last = mid
+            if feas[s, mid]:
+                hi = mid
+            else:
+                lo = mid + 1
+        out[s] = lo if hi == F - 1 else last
+    return out
+
+
+def assert_last_probe_ips(got, ips, last):
+    """ips_work: M at each scenario's last probe; untouched (NaN) rows for
+    scenarios that probe nothing."""
+    for s in range(got.shape[0]):
+        if last[s] < 0:
+            assert np.all(np.isnan(got[s])), s
+        else:
+            assert np.array_equal(got[s].view(np.uint32), ips[s, last[s]].astype(np.float32).view(np.uint32)), \
+                (s, int(last[s]))
 
 
 def random_checks(rng, S, H, kv):
@@ -81,10 +122,11 @@ def test_binary_search_random(gpu, S, F, H, T, d, nf, mono, seed):
     freqs = synth.frequency_grid(F)
     eng = rng.choice([1.0, 2.0, 4.0, 8.0], S).astype(np.float32) if nf == 4 else None
     dl, n, tbt, flags = random_checks(rng, S, H, kv)
-    idx, st = gpu_binary(fd, freqs, kv, bs, dl, n, tbt, flags, eng)
+    idx, st, work = gpu_binary(fd, freqs, kv, bs, dl, n, tbt, flags, eng, want_ips=True)
     ips = oracle.forest_predict(fd, oracle.rows(freqs, bs, kv, eng, nf))
     oi, os_ = oracle.select_binary(ips, dl, n, tbt, flags)
     assert np.array_equal(idx, oi) and np.array_equal(st, os_), np.nonzero((idx != oi) | (st != os_))[0][:5]
+    assert_last_probe_ips(work, ips, last_probes(ips, dl, n, tbt, flags))
     ei, es = oracle.select(ips, dl, n, tbt, flags)
     if mono:
         assert np.array_equal(idx, ei) and np.array_equal(st, es)
@@ -113,11 +155,15 @@ def test_binary_search_at_reuse_sizes(gpu, S, H):
     freqs = synth.frequency_grid(F)
     eng = rng.choice([1.0, 2.0, 4.0, 8.0], S).astype(np.float32)
     dl, n, tbt, flags = random_checks(rng, S, H, kv)
-    idx, st = gpu_binary(fd, freqs, kv, bs, dl, n, tbt, flags, eng)
+    idx, st, work = gpu_binary(fd, freqs, kv, bs, dl, n, tbt, flags, eng, want_ips=True)
     ips = oracle.forest_predict(fd, oracle.rows(freqs, bs, kv, eng, nf))
     oi, os_ = oracle.select_binary(ips, dl, n, tbt, flags)
     assert np.array_equal(idx, oi) and np.array_equal(st, os_), np.nonzero((idx != oi) | (st != os_))[0][:5]
     assert len(set(st.tolist())) >= 2
+    last = last_probes(ips, dl, n, tbt, flags)
+    # some scenarios settle without a final evaluation, others need one
+    assert np.any((last >= 0) & (last < F - 1)) and np.any(last == F - 1)
+    assert_last_probe_ips(work, ips, last)
 
 
 SCALED = [
