@@ -550,6 +550,42 @@ def test_binary_search_equals_sweep_when_monotone():
     assert (a[1] == 0).sum() > 20 and (a[1] == 1).sum() > 5
 
 
+def test_binary_search_check_of_lo_is_known_when_hi_moved():
+    """Sec. 4.5's search as the oracle runs it, replayed over the oracle's
+    own feasibility at every frequency (unsorted IPS: feasibility far from
+    monotone).  hi moves only to a probe found feasible and no probe is F-1
+    (the midpoint of lo < hi lies below hi), so whenever hi ends below F-1,
+    lo == hi was probed and found feasible: the final check of lo then
+    decides nothing new, and answering lo (OK) without it gives the oracle's
+    answer.  Only searches whose hi stayed at F-1 need that evaluation."""
+    rng = np.random.default_rng(12)
+    for F in (1, 2, 3, 5, 16, 48, 64, 100):
+        S, H = 120, 30
+        ips, dl, n, tbt = _sel_inputs(rng, S, F, H)
+        feas = np.stack([oracle.select(np.ascontiguousarray(ips[:, f:f + 1]), dl, n, tbt)[1] == 0
+                         for f in range(F)], axis=1)
+        idx, st = oracle.select_binary(ips, dl, n, tbt)
+        need_eval = 0
+        for s_ in range(S):
+            lo, hi, probed = 0, F - 1, {}
+            while lo < hi:
+                mid = lo + (hi - lo) // 2
+                assert mid < F - 1
+                probed[mid] = bool(feas[s_, mid])
+                if probed[mid]:
+                    hi = mid
+                else:
+                    lo = mid + 1
+            assert lo == hi
+            if hi < F - 1:
+                assert probed.get(lo) is True
+                assert (idx[s_], st[s_]) == (lo, 0)
+            else:
+                need_eval += 1
+                assert (idx[s_], st[s_]) == ((lo, 0) if feas[s_, lo] else (F - 1, 1))
+        assert 0 < need_eval <= S and (F == 1 or need_eval < S)
+
+
 def test_selection_monotone_in_slo_and_ips():
     rng = np.random.default_rng(6)
     S, F, H = 150, 12, 30
