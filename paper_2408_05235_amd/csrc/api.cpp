@@ -256,13 +256,15 @@ hipError_t with_workspace(const tl_forest* f, size_t need, hipStream_t st, Launc
         e = hipStreamWaitEvent(st, f->ws_done, 0);
         if (e != hipSuccess) return e;
     }
-    e = launch(f->ws, f->ws_bytes);
-    if (e != hipSuccess) return e;
+    const hipError_t el = launch(f->ws, f->ws_bytes);
+    // recorded also after a failed launch, whose earlier kernels may have
+    // been enqueued on st and use the workspace
     e = hipEventRecord(f->ws_done, st);
-    if (e != hipSuccess) return e;
-    f->ws_stream = st;
-    f->ws_used = true;
-    return hipSuccess;
+    if (e == hipSuccess) {
+        f->ws_stream = st;
+        f->ws_used = true;
+    }
+    return el != hipSuccess ? el : e;
 }
 
 hipError_t grid_with_workspace(const tl_forest* f, const tl::GridParams& g, hipStream_t st) {
@@ -407,13 +409,15 @@ hipError_t project_launch(tl::ProjectParams p, hipStream_t st) {
         if (e != hipSuccess) return e;
     }
     p.order_ws = w.ptr;
-    e = tl::launch_project(p, st);
-    if (e != hipSuccess) return e;
+    const hipError_t el = tl::launch_project(p, st);
+    // recorded also after a failed launch, whose order kernels may have been
+    // enqueued on st and use the workspace
     e = hipEventRecord(w.done, st);
-    if (e != hipSuccess) return e;
-    w.stream = st;
-    w.used = true;
-    return hipSuccess;
+    if (e == hipSuccess) {
+        w.stream = st;
+        w.used = true;
+    }
+    return el != hipSuccess ? el : e;
 }
 
 }  // namespace
